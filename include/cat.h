@@ -1,0 +1,210 @@
+/*
+ * cat.h -- C ABI of the block Concentration-Alignment Transform (CAT)
+ * W4A4 linear-layer library for MI355X (gfx950).
+ *
+ * Paper: "Dissecting Quantization Error: A Concentration-Alignment
+ * Perspective" (Federici, van Breugel, Whatmough, Nagel).  The layer is
+ * factored as Q(W T^-1) Q(T x) (Sec. 3, eq. 5), with T the block-diagonal
+ * transform T_b = H_k M_b of Sec. 4, eq. 10, whose blocks M_b come from the
+ * calibration second moment Sigma_x = E[x x^T] and Sigma_w = W^T W (eq. 7).
+ * The quality measure is the output SQNR of Sec. 2, eq. 1.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Return value: CAT_OK (0) or a negative cat_status.  On failure
+ *    cat_last_error() returns a thread-local message.  No C++ exception
+ *    crosses this boundary.
+ *  - Device calls (cov_accumulate, transform_quant, w4a4_linear, sqnr)
+ *    take DEVICE pointers, validate their arguments on the host, enqueue
+ *    kernels on `stream` (a hipStream_t passed as void*; NULL = the null
+ *    stream) and return without synchronising.  Results are visible after
+ *    the caller synchronises that stream.  Asynchronous faults surface at
+ *    that synchronisation.  They never allocate: scratch memory comes from
+ *    a caller-owned workspace whose size a *_workspace_bytes() query gives.
+ *  - Host calls (build_transform, quantize_weights) take HOST pointers,
+ *    run synchronously on the CPU in fp64 and touch no GPU.
+ *  - Ownership: every buffer belongs to the caller; the library keeps no
+ *    pointer after a call returns.
+ *  - Layout: all matrices row-major and densely packed (leading dimension
+ *    = row length).  Device pointers must be 16-byte aligned.
+ *  - Packed INT4: byte j of a row holds element 2j in bits 0-3 and element
+ *    2j+1 in bits 4-7, two's complement; codes lie in [-7, 7].
+ *  - Calls are stateless and may be issued from several threads.
+ *  - NaN / Inf inputs give undefined (but memory-safe) results.
+ */
+#ifndef CAT_H
+#define CAT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    CAT_OK = 0,
+    CAT_ERR_INVALID_ARG = -1,   /* null pointer, bad size, misalignment */
+    CAT_ERR_UNSUPPORTED = -2,   /* valid but not implemented (e.g. bits) */
+    CAT_ERR_WORKSPACE = -3,     /* workspace missing or too small */
+    CAT_ERR_HIP = -4,           /* HIP runtime / launch failure */
+    CAT_ERR_INTERNAL = -5       /* anything else (e.g. host allocation) */
+} cat_status;
+
+typedef enum {
+    CAT_F32 = 0,                /* IEEE binary32 */
+    CAT_BF16 = 1                /* bfloat16 (upper half of a binary32) */
+} cat_dtype;
+
+/* cat_cov_accumulate modes */
+#define CAT_COV_FULL 0          /* the whole d x d matrix */
+#define CAT_COV_BLOCK_DIAG 1    /* only the d/k diagonal k x k blocks */
+
+/* cat_build_transform flags */
+#define CAT_BUILD_HADAMARD 1    /* left factor H_k (normalised Sylvester) */
+#define CAT_BUILD_ALIGN 2       /* right factor M_b (alignment-optimal) */
+#define CAT_BUILD_CAT (CAT_BUILD_HADAMARD | CAT_BUILD_ALIGN)
+
+/* Largest supported d_in of cat_w4a4_linear: keeps the int32 accumulator
+ * exact (49 * 256 * d_in < 2^31 with the in-register 16x code unpack). */
+#define CAT_MAX_D_IN 131072
+#define CAT_MAX_BLOCK 512
+
+/* ------------------------------------------------------------------ (1)
+ * Calibration second moment (Sec. 4: Sigma_x = E[x x^T], non-centred;
+ * Sec. 6 "Calibration").
+ *
+ *   acc += X^T X        (an unnormalised sum; divide by the total token
+ *                         count afterwards)
+ *
+ * X     device, [n x d] row-major, x_dtype (CAT_BF16 or CAT_F32).
+ * n     tokens in this batch, n >= 1.  Calling again on the same acc
+ *       continues the accumulation (split batches give the one-shot sum up
+ *       to fp32 rounding).
+ * d     channels, 1 <= d, d % k == 0.
+ * mode  CAT_COV_FULL: acc is [d x d] fp32, both triangles written (the
+ *       kernel computes the upper triangle and mirrors it).
+ *       CAT_COV_BLOCK_DIAG: acc is [d/k x k x k] fp32, block b holding
+ *       X[:, bk:(b+1)k]^T X[:, bk:(b+1)k].
+ * k     block size: power of two in [1, CAT_MAX_BLOCK] (only read in
+ *       CAT_COV_BLOCK_DIAG mode).
+ * acc   device fp32, caller-owned, read and written.  Products are formed
+ *       exactly (bf16) and summed in fp32, with partial sums over at most
+ *       4096 tokens before they are added into acc.
+ */
+int cat_cov_accumulate(const void* X, int x_dtype, int64_t n, int64_t d,
+                       int mode, int64_t k, float* acc, void* stream);
+
+/* ------------------------------------------------------------------ (2)
+ * Block transform fused with symmetric per-token quantization
+ * (Sec. 3, eq. 5: Q(T x); Sec. 4, eq. 10: T = blockdiag(T_1..T_{d/k});
+ * Lemma 2.2: symmetric range r(x) = 2 max|x_i|; Sec. 6: dynamic per-token
+ * activation quantization).
+ *
+ * For every token t (row of X) and block b:
+ *   z[t, bk+j] = sum_i T_b[j, i] * X[t, bk+i]        (fp32 accumulation)
+ *   amax[t]    = max over the WHOLE row of |z[t, :]|
+ *   s_x[t]     = amax / qmax,  qmax = 2^(bits-1) - 1    (fp32, rounded)
+ *   inv        = qmax / amax                          (fp32, rounded)
+ *   code       = clamp(rint(z * inv), -qmax, qmax)     (ties to even)
+ * A row with amax == 0 gets s_x = 0 and all-zero codes.
+ *
+ * X        device [n x d], x_dtype.
+ * T        device [d/k x k x k], t_dtype; block b row-major (row j = output j).
+ * k        power of two in [1, CAT_MAX_BLOCK]; d % k == 0; d even.
+ * bits     4 (other widths return CAT_ERR_UNSUPPORTED).
+ * codes    device uint8 [n x d/2], packed INT4 (written).
+ * s_x      device fp32 [n] (written).
+ * workspace / workspace_bytes: device scratch of at least
+ *          cat_transform_quant_workspace_bytes(n, d, k) bytes; its
+ *          contents on entry are ignored and on exit undefined.
+ */
+size_t cat_transform_quant_workspace_bytes(int64_t n, int64_t d, int64_t k);
+int cat_transform_quant(const void* X, int x_dtype, int64_t n, int64_t d,
+                        const void* T, int t_dtype, int64_t k, int bits,
+                        uint8_t* codes, float* s_x, void* workspace,
+                        size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------ (3)
+ * W4A4 integer GEMM with dequantization (Sec. 3, eq. 5:
+ * Q(W T^-1) Q(T x)).
+ *
+ *   acc[t, o]     = sum_j qx[t, j] * qw[o, j]          (int32, exact)
+ *   y_tilde[t, o] = fl32(fl32(acc) * s_x[t]) * s_w[o]  (fp32, in this order)
+ *
+ * codes_x  device uint8 [n x d_in/2] packed INT4, s_x device fp32 [n].
+ * codes_w  device uint8 [d_out x d_in/2] packed INT4, s_w device fp32 [d_out].
+ * n, d_out >= 1; d_in a multiple of 32 and <= CAT_MAX_D_IN.
+ * y_tilde  device fp32 [n x d_out] (written).
+ * acc_out  device int32 [n x d_out] or NULL (written when non-NULL).
+ */
+int cat_w4a4_linear(const uint8_t* codes_x, const float* s_x,
+                    const uint8_t* codes_w, const float* s_w, int64_t n,
+                    int64_t d_in, int64_t d_out, float* y_tilde,
+                    int32_t* acc_out, void* stream);
+
+/* ------------------------------------------------------------------ (4)
+ * SQNR reduction (Sec. 2, eq. 1: E||W x||^2 / E||W x - W~ x~||^2, with
+ * the expectations replaced by sums over all tokens and outputs).
+ *
+ *   out[0] = sum y^2,  out[1] = sum (y - y_tilde)^2     (fp64 sums)
+ *   out[2] = 10 log10(out[0] / out[1])   (+inf if out[1] == 0 < out[0];
+ *                                          NaN if both are 0)
+ *
+ * y, y_tilde  device fp32 [count], count >= 1.
+ * workspace   device, >= cat_sqnr_workspace_bytes(count) bytes.
+ * out         device fp64 [3] (written).
+ * The reduction order is fixed: repeated calls give identical bits.
+ */
+size_t cat_sqnr_workspace_bytes(int64_t count);
+int cat_sqnr(const float* y, const float* y_tilde, int64_t count,
+             void* workspace, size_t workspace_bytes, double* out,
+             void* stream);
+
+/* ------------------------------------------------------------ host side
+ * Transform construction (Sec. 4, eq. 7 and eq. 10), on the CPU in fp64.
+ *
+ * For each block b of size k:
+ *   Sigma_w,b = W[:, b]^T W[:, b]
+ *   M_b       = (Sigma_w,b # Sigma_x,b^-1)^(1/2)        (if CAT_BUILD_ALIGN,
+ *                                                       else I)
+ *   T_b       = H_k M_b                                (if CAT_BUILD_HADAMARD,
+ *                                                       else M_b)
+ *   T_b is rounded to t_dtype; then W'[:, b] = W[:, b] T_b^-1 with the
+ *   ROUNDED T_b, so W' T x = W x holds to fp64 accuracy.
+ * Symmetric eigenproblems use cyclic Jacobi; eigenvalues below
+ * 1e-12 * lambda_max are raised to that floor.
+ *
+ * sigma_x_blocks  host fp64 [d_in/k x k x k]: the diagonal blocks of
+ *                 Sigma_x (already divided by the token count).
+ * W               host fp32 [d_out x d_in].
+ * k               power of two in [1, CAT_MAX_BLOCK], d_in % k == 0.
+ * T_out           host [d_in/k x k x k] in t_dtype (bf16 as uint16 bits).
+ * T_exact_out     host fp64 [d_in/k x k x k] before rounding, or NULL.
+ * W_prime_out     host fp64 [d_out x d_in], or NULL.
+ * n_threads       worker threads (<= 0: hardware concurrency).
+ */
+int cat_build_transform(const double* sigma_x_blocks, const float* W,
+                        int64_t d_out, int64_t d_in, int64_t k, int flags,
+                        int t_dtype, void* T_out, double* T_exact_out,
+                        double* W_prime_out, int n_threads);
+
+/* Per-output-channel symmetric weight quantization (Sec. 6: weights per
+ * channel, symmetric, round to nearest), on fp32(W_prime) with exactly
+ * the arithmetic of cat_transform_quant.
+ * W_prime host fp64 [d_out x d_in]; codes_w_out host uint8
+ * [d_out x d_in/2]; s_w_out host fp32 [d_out]; bits == 4; d_in even. */
+int cat_quantize_weights(const double* W_prime, int64_t d_out, int64_t d_in,
+                         int bits, uint8_t* codes_w_out, float* s_w_out);
+
+/* Thread-local message describing the last non-OK return on this thread. */
+const char* cat_last_error(void);
+
+/* Library version string. */
+const char* cat_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CAT_H */

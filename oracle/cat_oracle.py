@@ -181,7 +181,8 @@ def cat_transform(sigma_x, W, k: int, use_hadamard: bool = True,
 
     use_alignment=False gives the block-Hadamard baseline (M_b = I);
     use_hadamard=False gives the alignment-only transform."""
-    sigma_x = np.asarray(sigma_x, dtype=np.float64)
+    if use_alignment:
+        sigma_x = np.asarray(sigma_x, dtype=np.float64)
     W = np.asarray(W, dtype=np.float64)
     d = W.shape[1]
     if d % k:

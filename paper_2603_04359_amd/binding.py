@@ -1,0 +1,255 @@
+"""Thin ctypes binding of libcat.so (the C ABI declared in include/cat.h).
+
+Argument marshalling only: every function here checks that tensors have
+the dtype, device and contiguity the C call expects, passes raw pointers
+and sizes, and turns a non-zero status into CatError.  All arithmetic of
+the path runs in the library's HIP kernels (device calls) or its C++ host
+code (transform construction).  PyTorch only provides device memory and
+the current stream.  If the library is missing, every call raises: there
+is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libcat.so")
+
+CAT_OK = 0
+CAT_ERR_INVALID_ARG = -1
+CAT_ERR_UNSUPPORTED = -2
+CAT_ERR_WORKSPACE = -3
+CAT_ERR_HIP = -4
+CAT_ERR_INTERNAL = -5
+
+CAT_F32 = 0
+CAT_BF16 = 1
+
+CAT_COV_FULL = 0
+CAT_COV_BLOCK_DIAG = 1
+
+CAT_BUILD_HADAMARD = 1
+CAT_BUILD_ALIGN = 2
+CAT_BUILD_CAT = 3
+
+CAT_MAX_D_IN = 131072
+CAT_MAX_BLOCK = 512
+
+# every symbol include/cat.h declares
+EXPORTED = (
+    "cat_cov_accumulate", "cat_transform_quant_workspace_bytes", "cat_transform_quant",
+    "cat_w4a4_linear", "cat_sqnr_workspace_bytes", "cat_sqnr", "cat_build_transform",
+    "cat_quantize_weights", "cat_last_error", "cat_version",
+)
+
+
+class CatError(RuntimeError):
+    def __init__(self, fn: str, code: int, msg: str):
+        super().__init__(f"{fn} failed with status {code}: {msg}")
+        self.fn = fn
+        self.code = code
+
+
+_lib = None
+_c = ctypes
+_i64 = ctypes.c_int64
+_vp = ctypes.c_void_p
+_int = ctypes.c_int
+_sz = ctypes.c_size_t
+
+
+def lib() -> ctypes.CDLL:
+    """Load libcat.so (once).  Raises ImportError if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: build it with "
+                          "`python paper_2603_04359_amd/build.py` (or __graft_entry__.build())")
+    L = ctypes.CDLL(LIB_PATH)
+    L.cat_cov_accumulate.argtypes = [_vp, _int, _i64, _i64, _int, _i64, _vp, _vp]
+    L.cat_cov_accumulate.restype = _int
+    L.cat_transform_quant_workspace_bytes.argtypes = [_i64, _i64, _i64]
+    L.cat_transform_quant_workspace_bytes.restype = _sz
+    L.cat_transform_quant.argtypes = [_vp, _int, _i64, _i64, _vp, _int, _i64, _int, _vp, _vp,
+                                      _vp, _sz, _vp]
+    L.cat_transform_quant.restype = _int
+    L.cat_w4a4_linear.argtypes = [_vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp]
+    L.cat_w4a4_linear.restype = _int
+    L.cat_sqnr_workspace_bytes.argtypes = [_i64]
+    L.cat_sqnr_workspace_bytes.restype = _sz
+    L.cat_sqnr.argtypes = [_vp, _vp, _i64, _vp, _sz, _vp, _vp]
+    L.cat_sqnr.restype = _int
+    L.cat_build_transform.argtypes = [_vp, _vp, _i64, _i64, _i64, _int, _int, _vp, _vp, _vp, _int]
+    L.cat_build_transform.restype = _int
+    L.cat_quantize_weights.argtypes = [_vp, _i64, _i64, _int, _vp, _vp]
+    L.cat_quantize_weights.restype = _int
+    L.cat_last_error.argtypes = []
+    L.cat_last_error.restype = ctypes.c_char_p
+    L.cat_version.argtypes = []
+    L.cat_version.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def cat_last_error() -> str:
+    return lib().cat_last_error().decode()
+
+
+def cat_version() -> str:
+    return lib().cat_version().decode()
+
+
+def _check(fn: str, rc: int):
+    if rc != CAT_OK:
+        raise CatError(fn, rc, cat_last_error())
+
+
+# ------------------------------------------------------------ marshalling
+def _torch():
+    import torch
+    return torch
+
+
+def _dev_ptr(t, name, dtypes=None, allow_none=False):
+    if t is None:
+        if allow_none:
+            return None
+        raise ValueError(f"{name} is required")
+    torch = _torch()
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must live on the GPU")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtypes is not None and t.dtype not in dtypes:
+        raise TypeError(f"{name} has dtype {t.dtype}, expected one of {dtypes}")
+    return t.data_ptr()
+
+
+def _dtype_code(t):
+    torch = _torch()
+    if t.dtype == torch.bfloat16:
+        return CAT_BF16
+    if t.dtype == torch.float32:
+        return CAT_F32
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _stream_ptr(stream):
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+# ------------------------------------------------------------ device calls
+def cat_cov_accumulate(X, acc, mode: int = CAT_COV_FULL, k: int = 1, stream=None):
+    """acc += X^T X (FULL: acc [d, d]; BLOCK_DIAG: acc [d/k, k, k]), fp32."""
+    torch = _torch()
+    px = _dev_ptr(X, "X", (torch.bfloat16, torch.float32))
+    pa = _dev_ptr(acc, "acc", (torch.float32,))
+    if X.dim() != 2:
+        raise ValueError("X must be [n, d]")
+    n, d = X.shape
+    _check("cat_cov_accumulate",
+           lib().cat_cov_accumulate(px, _dtype_code(X), n, d, mode, k, pa, _stream_ptr(stream)))
+
+
+def cat_transform_quant_workspace_bytes(n: int, d: int, k: int) -> int:
+    return int(lib().cat_transform_quant_workspace_bytes(n, d, k))
+
+
+def cat_transform_quant(X, T, k: int, codes, s_x, workspace, bits: int = 4, stream=None):
+    """codes [n, d/2] uint8 and s_x [n] fp32 from X [n, d] and T [d/k, k, k]."""
+    torch = _torch()
+    px = _dev_ptr(X, "X", (torch.bfloat16, torch.float32))
+    pt = _dev_ptr(T, "T", (torch.bfloat16, torch.float32))
+    pc = _dev_ptr(codes, "codes", (torch.uint8,))
+    ps = _dev_ptr(s_x, "s_x", (torch.float32,))
+    pw = _dev_ptr(workspace, "workspace")
+    if X.dim() != 2:
+        raise ValueError("X must be [n, d]")
+    n, d = X.shape
+    wbytes = workspace.numel() * workspace.element_size()
+    _check("cat_transform_quant",
+           lib().cat_transform_quant(px, _dtype_code(X), n, d, pt, _dtype_code(T), k, bits, pc, ps,
+                                     pw, wbytes, _stream_ptr(stream)))
+
+
+def cat_w4a4_linear(codes_x, s_x, codes_w, s_w, y_tilde, acc_out=None, stream=None):
+    """y_tilde [n, d_out] fp32 (and optionally acc_out int32) from packed codes."""
+    torch = _torch()
+    pcx = _dev_ptr(codes_x, "codes_x", (torch.uint8,))
+    psx = _dev_ptr(s_x, "s_x", (torch.float32,))
+    pcw = _dev_ptr(codes_w, "codes_w", (torch.uint8,))
+    psw = _dev_ptr(s_w, "s_w", (torch.float32,))
+    py = _dev_ptr(y_tilde, "y_tilde", (torch.float32,))
+    pacc = _dev_ptr(acc_out, "acc_out", (torch.int32,), allow_none=True)
+    n, half = codes_x.shape
+    d_out = codes_w.shape[0]
+    if codes_w.shape[1] != half:
+        raise ValueError("codes_x and codes_w disagree on d_in")
+    _check("cat_w4a4_linear",
+           lib().cat_w4a4_linear(pcx, psx, pcw, psw, n, 2 * half, d_out, py, pacc,
+                                 _stream_ptr(stream)))
+
+
+def cat_sqnr_workspace_bytes(count: int) -> int:
+    return int(lib().cat_sqnr_workspace_bytes(count))
+
+
+def cat_sqnr(y, y_tilde, workspace, out, stream=None):
+    """out [3] fp64 = (sum y^2, sum (y - y~)^2, dB)."""
+    torch = _torch()
+    py = _dev_ptr(y, "y", (torch.float32,))
+    pt = _dev_ptr(y_tilde, "y_tilde", (torch.float32,))
+    pw = _dev_ptr(workspace, "workspace")
+    po = _dev_ptr(out, "out", (torch.float64,))
+    if y.numel() != y_tilde.numel():
+        raise ValueError("y and y_tilde differ in size")
+    wbytes = workspace.numel() * workspace.element_size()
+    _check("cat_sqnr", lib().cat_sqnr(py, pt, y.numel(), pw, wbytes, po, _stream_ptr(stream)))
+
+
+# -------------------------------------------------------------- host calls
+def _host(a, dtype, name):
+    a = np.ascontiguousarray(a, dtype=dtype)
+    return a, a.ctypes.data
+
+
+def cat_build_transform(sigma_x_blocks, W, k: int, flags: int = CAT_BUILD_CAT,
+                        t_dtype: int = CAT_BF16, want_exact: bool = False,
+                        want_w_prime: bool = True, n_threads: int = 0):
+    """Host transform construction.  Returns (T, T_exact or None, W_prime or None);
+    T is uint16 bf16 bits (t_dtype = CAT_BF16) or fp32, shape [d_in/k, k, k]."""
+    W, pw = _host(W, np.float32, "W")
+    d_out, d_in = W.shape
+    if sigma_x_blocks is not None:
+        sx, psx = _host(sigma_x_blocks, np.float64, "sigma_x_blocks")
+        if sx.shape != (d_in // k, k, k):
+            raise ValueError("sigma_x_blocks must be [d_in/k, k, k]")
+    else:
+        sx, psx = None, None
+    T = np.empty((d_in // k, k, k), dtype=np.uint16 if t_dtype == CAT_BF16 else np.float32)
+    Te = np.empty((d_in // k, k, k), dtype=np.float64) if want_exact else None
+    Wp = np.empty((d_out, d_in), dtype=np.float64) if want_w_prime else None
+    _check("cat_build_transform",
+           lib().cat_build_transform(psx, pw, d_out, d_in, k, flags, t_dtype, T.ctypes.data,
+                                     Te.ctypes.data if Te is not None else None,
+                                     Wp.ctypes.data if Wp is not None else None, n_threads))
+    return T, Te, Wp
+
+
+def cat_quantize_weights(W_prime, bits: int = 4):
+    """Host per-output-channel quantization: returns (codes uint8 [d_out, d_in/2], s_w fp32)."""
+    Wp, pwp = _host(W_prime, np.float64, "W_prime")
+    d_out, d_in = Wp.shape
+    codes = np.empty((d_out, d_in // 2), dtype=np.uint8)
+    s_w = np.empty(d_out, dtype=np.float32)
+    _check("cat_quantize_weights",
+           lib().cat_quantize_weights(pwp, d_out, d_in, bits, codes.ctypes.data, s_w.ctypes.data))
+    return codes, s_w

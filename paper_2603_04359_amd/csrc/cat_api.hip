@@ -1,0 +1,160 @@
+// C ABI of the CAT W4A4 linear-layer library: argument validation, launch
+// and error mapping for the four device calls.  Every check runs on the
+// host before anything is enqueued; nothing falls back silently.
+#include <hip/hip_runtime.h>
+
+#include <exception>
+#include <string>
+
+#include "cat_internal.h"
+#include "kernels.h"
+
+namespace {
+
+using cat::fail;
+
+int hip_fail(const char* where, hipError_t err) {
+    return fail(CAT_ERR_HIP, std::string(where) + ": " + hipGetErrorString(err));
+}
+
+bool valid_dtype(int t) { return t == CAT_F32 || t == CAT_BF16; }
+
+// Checks that a device is present and current before the first launch, so
+// that a missing GPU reports CAT_ERR_HIP instead of failing inside HIP.
+int require_device(const char* where) {
+    int count = 0;
+    const hipError_t err = hipGetDeviceCount(&count);
+    if (err != hipSuccess) return hip_fail(where, err);
+    if (count < 1) return fail(CAT_ERR_HIP, std::string(where) + ": no HIP device");
+    return CAT_OK;
+}
+
+}  // namespace
+
+extern "C" int cat_cov_accumulate(const void* X, int x_dtype, int64_t n, int64_t d, int mode,
+                                  int64_t k, float* acc, void* stream) {
+    const char* fn = "cat_cov_accumulate";
+    try {
+        if (!X || !acc) return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": NULL pointer");
+        if (!valid_dtype(x_dtype)) return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": bad x_dtype");
+        if (n < 1 || d < 1) return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": n and d must be >= 1");
+        if (mode != CAT_COV_FULL && mode != CAT_COV_BLOCK_DIAG)
+            return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": bad mode");
+        if (mode == CAT_COV_BLOCK_DIAG) {
+            if (!cat::is_pow2(k) || k > CAT_MAX_BLOCK)
+                return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": k must be a power of two <= 512");
+            if (d % k) return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": d % k != 0");
+        }
+        if (!cat::aligned16(X) || !cat::aligned16(acc))
+            return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": pointers must be 16-byte aligned");
+        if (int rc = require_device(fn)) return rc;
+        const hipError_t err = catk::launch_cov_accumulate(X, x_dtype == CAT_BF16, n, d, mode, k, acc,
+                                                           static_cast<hipStream_t>(stream));
+        if (err != hipSuccess) return hip_fail(fn, err);
+        return CAT_OK;
+    } catch (const std::exception& e) {
+        return fail(CAT_ERR_INTERNAL, std::string(fn) + ": " + e.what());
+    } catch (...) {
+        return fail(CAT_ERR_INTERNAL, std::string(fn) + ": unknown error");
+    }
+}
+
+extern "C" size_t cat_transform_quant_workspace_bytes(int64_t n, int64_t d, int64_t k) {
+    (void)d;
+    (void)k;
+    if (n < 1) return 0;
+    // one 32-bit running maximum per token, rounded up to 256 bytes
+    return static_cast<size_t>((n * 4 + 255) / 256 * 256);
+}
+
+extern "C" int cat_transform_quant(const void* X, int x_dtype, int64_t n, int64_t d, const void* T,
+                                   int t_dtype, int64_t k, int bits, uint8_t* codes, float* s_x,
+                                   void* workspace, size_t workspace_bytes, void* stream) {
+    const char* fn = "cat_transform_quant";
+    try {
+        if (!X || !T || !codes || !s_x)
+            return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": NULL pointer");
+        if (!valid_dtype(x_dtype) || !valid_dtype(t_dtype))
+            return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": bad dtype");
+        if (n < 1 || d < 2) return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": need n >= 1, d >= 2");
+        if (d % 2) return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": d must be even");
+        if (!cat::is_pow2(k) || k > CAT_MAX_BLOCK)
+            return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": k must be a power of two <= 512");
+        if (d % k) return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": d % k != 0");
+        if (bits != 4) return fail(CAT_ERR_UNSUPPORTED, std::string(fn) + ": only bits == 4");
+        if (!cat::aligned16(X) || !cat::aligned16(T) || !cat::aligned16(codes) ||
+            !cat::aligned16(s_x))
+            return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": pointers must be 16-byte aligned");
+        if (!workspace || workspace_bytes < cat_transform_quant_workspace_bytes(n, d, k))
+            return fail(CAT_ERR_WORKSPACE, std::string(fn) + ": workspace missing or too small");
+        if (!cat::aligned16(workspace))
+            return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": workspace must be 16-byte aligned");
+        if (int rc = require_device(fn)) return rc;
+        const hipError_t err = catk::launch_transform_quant(
+            X, x_dtype == CAT_BF16, n, d, T, t_dtype == CAT_BF16, k, codes, s_x,
+            static_cast<uint32_t*>(workspace), static_cast<hipStream_t>(stream));
+        if (err != hipSuccess) return hip_fail(fn, err);
+        return CAT_OK;
+    } catch (const std::exception& e) {
+        return fail(CAT_ERR_INTERNAL, std::string(fn) + ": " + e.what());
+    } catch (...) {
+        return fail(CAT_ERR_INTERNAL, std::string(fn) + ": unknown error");
+    }
+}
+
+extern "C" int cat_w4a4_linear(const uint8_t* codes_x, const float* s_x, const uint8_t* codes_w,
+                               const float* s_w, int64_t n, int64_t d_in, int64_t d_out,
+                               float* y_tilde, int32_t* acc_out, void* stream) {
+    const char* fn = "cat_w4a4_linear";
+    try {
+        if (!codes_x || !s_x || !codes_w || !s_w || !y_tilde)
+            return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": NULL pointer");
+        if (n < 1 || d_out < 1 || d_in < 32)
+            return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": need n, d_out >= 1 and d_in >= 32");
+        if (d_in % 32) return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": d_in must be a multiple of 32");
+        if (d_in > CAT_MAX_D_IN)
+            return fail(CAT_ERR_UNSUPPORTED, std::string(fn) + ": d_in exceeds CAT_MAX_D_IN");
+        if (!cat::aligned16(codes_x) || !cat::aligned16(codes_w) || !cat::aligned16(s_x) ||
+            !cat::aligned16(s_w) || !cat::aligned16(y_tilde) || (acc_out && !cat::aligned16(acc_out)))
+            return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": pointers must be 16-byte aligned");
+        if (int rc = require_device(fn)) return rc;
+        const hipError_t err = catk::launch_w4a4_linear(codes_x, s_x, codes_w, s_w, n, d_in, d_out,
+                                                        y_tilde, acc_out,
+                                                        static_cast<hipStream_t>(stream));
+        if (err != hipSuccess) return hip_fail(fn, err);
+        return CAT_OK;
+    } catch (const std::exception& e) {
+        return fail(CAT_ERR_INTERNAL, std::string(fn) + ": " + e.what());
+    } catch (...) {
+        return fail(CAT_ERR_INTERNAL, std::string(fn) + ": unknown error");
+    }
+}
+
+extern "C" size_t cat_sqnr_workspace_bytes(int64_t count) {
+    if (count < 1) return 0;
+    return static_cast<size_t>(catk::sqnr_grid(count)) * 2 * sizeof(double);
+}
+
+extern "C" int cat_sqnr(const float* y, const float* y_tilde, int64_t count, void* workspace,
+                        size_t workspace_bytes, double* out, void* stream) {
+    const char* fn = "cat_sqnr";
+    try {
+        if (!y || !y_tilde || !out) return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": NULL pointer");
+        if (count < 1) return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": count must be >= 1");
+        if (!cat::aligned16(y) || !cat::aligned16(y_tilde) || !cat::aligned16(out))
+            return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": pointers must be 16-byte aligned");
+        if (!workspace || workspace_bytes < cat_sqnr_workspace_bytes(count))
+            return fail(CAT_ERR_WORKSPACE, std::string(fn) + ": workspace missing or too small");
+        if (!cat::aligned16(workspace))
+            return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": workspace must be 16-byte aligned");
+        if (int rc = require_device(fn)) return rc;
+        const hipError_t err = catk::launch_sqnr(y, y_tilde, count, static_cast<double*>(workspace),
+                                                 out, static_cast<hipStream_t>(stream));
+        if (err != hipSuccess) return hip_fail(fn, err);
+        return CAT_OK;
+    } catch (const std::exception& e) {
+        return fail(CAT_ERR_INTERNAL, std::string(fn) + ": " + e.what());
+    } catch (...) {
+        return fail(CAT_ERR_INTERNAL, std::string(fn) + ": unknown error");
+    }
+}

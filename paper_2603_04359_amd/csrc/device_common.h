@@ -1,0 +1,57 @@
+// Device-side types and helpers shared by the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+namespace catk {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kWave = 64;
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint16_t b) {
+    return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// Load element i of a bf16 (raw bits) or fp32 array as fp32.
+template <typename T>
+__device__ __forceinline__ float load_as_f32(const T* p, int64_t i);
+template <>
+__device__ __forceinline__ float load_as_f32<float>(const float* p, int64_t i) {
+    return p[i];
+}
+template <>
+__device__ __forceinline__ float load_as_f32<uint16_t>(const uint16_t* p, int64_t i) {
+    return bf16_bits_to_f32(p[i]);
+}
+
+// Reinterpret four dwords as eight bf16 values (MFMA operand).
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) {
+    return __builtin_bit_cast(bf16x8, v);
+}
+
+// Unsigned view of a non-negative float: order-preserving for atomicMax.
+__device__ __forceinline__ uint32_t abs_bits(float v) {
+    return __float_as_uint(v) & 0x7FFFFFFFu;
+}
+
+// Packed INT4 (two's complement, element 2m in the low nibble of byte m)
+// to int8 values scaled by 16.  From one packed dword (8 codes):
+//   lo = bytes (e0, e2, e4, e6) * 16,  hi = bytes (e1, e3, e5, e7) * 16.
+// The product of two operands unpacked the same way sums the same index
+// pairs (a permutation of the reduction index), scaled by 256.
+__device__ __forceinline__ uint32_t unpack_lo16(uint32_t w) {
+    return (w << 4) & 0xF0F0F0F0u;
+}
+__device__ __forceinline__ uint32_t unpack_hi16(uint32_t w) {
+    return w & 0xF0F0F0F0u;
+}
+
+}  // namespace catk

@@ -1,0 +1,268 @@
+// Block transform fused with symmetric per-token INT4 quantization.
+//
+// For each token x (a row of X) and each diagonal block b of the
+// block-diagonal transform (Sec. 4, eq. 10):  z_b = T_b x_b.
+// The token's scale uses the range of the WHOLE transformed row
+// (dynamic per-token range, Lemma 2.2 / Sec. 6):
+//   amax = max |z|,  s = amax / 7,  code = clamp(rint(z * (7 / amax)), -7, 7).
+//
+// The row maximum couples all d/k blocks of a token, while reuse of T_b
+// wants many tokens per workgroup.  The kernels therefore split the work
+// by (block, token tile) and run two passes over the same tiles:
+//   pass 1 (amax)   computes z and folds max|z| into a per-token word with
+//                   an atomic max on the float's bit pattern (all values
+//                   are non-negative, so unsigned order = float order);
+//   pass 2 (quant)  recomputes z with the identical instruction sequence,
+//                   reads the finished row maximum and writes packed codes.
+// A fill kernel clears the per-token words first (no hipMemset, so the
+// sequence can be captured in a graph).
+//
+// bf16 path: v_mfma_f32_32x32x16_bf16 with A = rows of T_b (staged in LDS,
+// XOR-swizzled 16-byte units) and B = token rows of X (16-byte loads
+// straight from HBM), so Z^T tiles come out with one token per lane column;
+// the per-token maximum is a register max plus one lane swap, and codes are
+// packed 4 per lane, joined to 8 per dword with one lane swap.
+// fp32 (or small-k) path: plain fp32 FMA chains on the vector ALU.
+#include "device_common.h"
+#include "kernels.h"
+
+namespace catk {
+
+constexpr int kTqThreads = 256;
+constexpr float kQmax4 = 7.0f;
+
+__global__ void fill_zero_u32_kernel(uint32_t* p, int64_t n) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = 0u;
+}
+
+// Quantize one value given inv = 7/amax (amax > 0); returns the code in
+// [-7, 7] as an int.
+__device__ __forceinline__ int quant_code(float z, float inv) {
+    float u = z * inv;
+    u = __builtin_rintf(u);
+    u = fminf(fmaxf(u, -kQmax4), kQmax4);
+    return static_cast<int>(u);
+}
+
+// ------------------------------------------------------------ generic path
+template <typename XT, typename TT>
+__device__ __forceinline__ float tq_dot(const XT* __restrict__ X, const TT* __restrict__ T,
+                                        int64_t t, int64_t d, int64_t k, int64_t c) {
+    const int64_t b = c / k;
+    const int64_t j = c - b * k;
+    const TT* trow = T + (b * k + j) * k;
+    const XT* xrow = X + t * d + b * k;
+    float acc = 0.0f;
+    for (int64_t i = 0; i < k; ++i) acc = fmaf(load_as_f32(trow, i), load_as_f32(xrow, i), acc);
+    return acc;
+}
+
+template <typename XT, typename TT>
+__global__ __launch_bounds__(kTqThreads) void tq_generic_amax_kernel(
+    const XT* __restrict__ X, const TT* __restrict__ T, int64_t n, int64_t d, int64_t k,
+    uint32_t* __restrict__ amax_ws) {
+    const int64_t pairs = d / 2;
+    const int64_t u = static_cast<int64_t>(blockIdx.x) * kTqThreads + threadIdx.x;
+    if (u >= n * pairs) return;
+    const int64_t t = u / pairs;
+    const int64_t c = 2 * (u - t * pairs);
+    const float z0 = tq_dot(X, T, t, d, k, c);
+    const float z1 = tq_dot(X, T, t, d, k, c + 1);
+    const uint32_t m = max(abs_bits(z0), abs_bits(z1));
+    if (m) atomicMax(amax_ws + t, m);
+}
+
+template <typename XT, typename TT>
+__global__ __launch_bounds__(kTqThreads) void tq_generic_quant_kernel(
+    const XT* __restrict__ X, const TT* __restrict__ T, int64_t n, int64_t d, int64_t k,
+    const uint32_t* __restrict__ amax_ws, uint8_t* __restrict__ codes, float* __restrict__ s_x) {
+    const int64_t pairs = d / 2;
+    const int64_t u = static_cast<int64_t>(blockIdx.x) * kTqThreads + threadIdx.x;
+    if (u >= n * pairs) return;
+    const int64_t t = u / pairs;
+    const int64_t cp = u - t * pairs;
+    const float amax = __uint_as_float(amax_ws[t]);
+    if (cp == 0) s_x[t] = __fdiv_rn(amax, kQmax4);
+    uint8_t byte = 0;
+    if (amax > 0.0f) {
+        const float inv = __fdiv_rn(kQmax4, amax);
+        const float z0 = tq_dot(X, T, t, d, k, 2 * cp);
+        const float z1 = tq_dot(X, T, t, d, k, 2 * cp + 1);
+        byte = static_cast<uint8_t>((quant_code(z0, inv) & 0xF) | ((quant_code(z1, inv) & 0xF) << 4));
+    }
+    codes[t * pairs + cp] = byte;
+}
+
+// --------------------------------------------------------------- MFMA path
+// Workgroup = 4 waves; tile = 128 tokens (32 per wave) x JC output rows of
+// one block.  LDS holds the JC x K slice of T_b as 16-byte units, unit u of
+// row r stored at position u ^ swz(r) so that 16 lanes reading 16
+// consecutive rows at the same unit hit 16 distinct bank groups.
+template <int K>
+__device__ __forceinline__ int tq_swz(int r) {
+    constexpr int U = K / 8;                   // 16-byte units per row
+    constexpr int R = U >= 16 ? 1 : 16 / U;    // rows per 256 bytes
+    constexpr int M = (U >= 16 ? 16 : U) - 1;
+    return (r / R) & M;
+}
+
+template <int K, int JC, bool QUANT>
+__global__ __launch_bounds__(kTqThreads) void tq_mfma_kernel(
+    const uint16_t* __restrict__ X, const uint16_t* __restrict__ T, int64_t n, int64_t d,
+    uint32_t* __restrict__ amax_ws, uint8_t* __restrict__ codes, float* __restrict__ s_x) {
+    static_assert(K % 32 == 0 && JC % 32 == 0 && K % JC == 0, "tile shape");
+    constexpr int U = K / 8;
+    constexpr int NCHUNK = K / JC;
+    constexpr int NM = JC / 32;     // 32-row MFMA tiles per wave
+    constexpr int NS = K / 16;      // 16-deep MFMA steps
+    __shared__ u32x4 t_lds[JC * U];
+
+    const int64_t nblk = d / K;
+    const int64_t work = blockIdx.x;
+    const int64_t bj = work % (nblk * NCHUNK);
+    const int64_t tile = work / (nblk * NCHUNK);
+    const int64_t b = bj / NCHUNK;
+    const int jc = static_cast<int>(bj % NCHUNK);
+    const int64_t t0 = tile * 128;
+
+    // stage rows [jc*JC, jc*JC+JC) of T_b into LDS
+    const u32x4* tg = reinterpret_cast<const u32x4*>(T + (b * K + static_cast<int64_t>(jc) * JC) * K);
+    for (int i = threadIdx.x; i < JC * U; i += kTqThreads) {
+        const int r = i / U, u = i % U;
+        t_lds[r * U + (u ^ tq_swz<K>(r))] = tg[i];
+    }
+    __syncthreads();
+
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int col = lane & 31;      // token within the wave's 32
+    const int h = lane >> 5;        // which 8-element half of a 16-deep step
+    const int64_t t = t0 + wave * 32 + col;
+    const bool valid = t < n;
+    if (t0 + wave * 32 >= n) return;   // no barrier follows
+
+    // B operand: 8 consecutive bf16 of the token row per step
+    u32x4 xb[NS];
+    const u32x4* xg = reinterpret_cast<const u32x4*>(X + t * d + b * K);
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        if (valid) xb[s] = xg[2 * s + h];
+        else xb[s] = u32x4{0u, 0u, 0u, 0u};
+    }
+
+    f32x16 acc[NM];
+#pragma unroll
+    for (int m = 0; m < NM; ++m) {
+        acc[m] = f32x16{};
+        const int r = m * 32 + col;
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+            const u32x4 a = t_lds[r * U + ((2 * s + h) ^ tq_swz<K>(r))];
+            acc[m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(xb[s]),
+                                                             acc[m], 0, 0, 0);
+        }
+    }
+
+    if constexpr (!QUANT) {
+        uint32_t m_bits = 0;
+#pragma unroll
+        for (int m = 0; m < NM; ++m)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) m_bits = max(m_bits, abs_bits(acc[m][r]));
+        m_bits = max(m_bits, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m_bits), 32)));
+        if (valid && h == 0 && m_bits) atomicMax(amax_ws + t, m_bits);
+    } else {
+        const float amax = valid ? __uint_as_float(amax_ws[t]) : 0.0f;
+        if (valid && h == 0 && b == 0 && jc == 0) s_x[t] = __fdiv_rn(amax, kQmax4);
+        const bool nz = amax > 0.0f;
+        const float inv = nz ? __fdiv_rn(kQmax4, amax) : 0.0f;
+        uint32_t* crow = reinterpret_cast<uint32_t*>(codes + t * (d / 2) + b * (K / 2) +
+                                                     static_cast<int64_t>(jc) * (JC / 2));
+#pragma unroll
+        for (int m = 0; m < NM; ++m) {
+            // v[q]: codes of rows 32m + 8q + 4h + (0..3), packed in 16 bits
+            uint32_t v[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                uint32_t p = 0;
+                if (nz) {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        p |= static_cast<uint32_t>(quant_code(acc[m][4 * q + e], inv) & 0xF) << (4 * e);
+                }
+                v[q] = p;
+            }
+#pragma unroll
+            for (int qp = 0; qp < 4; qp += 2) {
+                // h=0 owns rows 8qp+0..7 of (qp), h=1 owns rows of (qp+1)
+                const uint32_t send = h ? v[qp] : v[qp + 1];
+                const uint32_t recv = static_cast<uint32_t>(__shfl_xor(static_cast<int>(send), 32));
+                const uint32_t word = h ? (recv | (v[qp + 1] << 16)) : (v[qp] | (recv << 16));
+                if (valid) crow[(m * 32 + 8 * (qp + h)) / 8] = word;
+            }
+        }
+    }
+}
+
+template <int K, int JC>
+hipError_t launch_tq_mfma(const uint16_t* X, int64_t n, int64_t d, const uint16_t* T,
+                          uint8_t* codes, float* s_x, uint32_t* ws, hipStream_t stream) {
+    const int64_t tiles = (n + 127) / 128;
+    const int64_t grid = tiles * (d / K) * (K / JC);
+    hipLaunchKernelGGL((tq_mfma_kernel<K, JC, false>), dim3(static_cast<uint32_t>(grid)),
+                       dim3(kTqThreads), 0, stream, X, T, n, d, ws, codes, s_x);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL((tq_mfma_kernel<K, JC, true>), dim3(static_cast<uint32_t>(grid)),
+                       dim3(kTqThreads), 0, stream, X, T, n, d, ws, codes, s_x);
+    return hipGetLastError();
+}
+
+template <typename XT, typename TT>
+hipError_t launch_tq_generic(const XT* X, int64_t n, int64_t d, const TT* T, int64_t k,
+                             uint8_t* codes, float* s_x, uint32_t* ws, hipStream_t stream) {
+    const int64_t units = n * (d / 2);
+    const int64_t grid = (units + kTqThreads - 1) / kTqThreads;
+    hipLaunchKernelGGL((tq_generic_amax_kernel<XT, TT>), dim3(static_cast<uint32_t>(grid)),
+                       dim3(kTqThreads), 0, stream, X, T, n, d, k, ws);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL((tq_generic_quant_kernel<XT, TT>), dim3(static_cast<uint32_t>(grid)),
+                       dim3(kTqThreads), 0, stream, X, T, n, d, k, ws, codes, s_x);
+    return hipGetLastError();
+}
+
+hipError_t launch_transform_quant(const void* X, int x_bf16, int64_t n, int64_t d, const void* T,
+                                  int t_bf16, int64_t k, uint8_t* codes, float* s_x,
+                                  uint32_t* amax_ws, hipStream_t stream) {
+    hipLaunchKernelGGL(fill_zero_u32_kernel, dim3(static_cast<uint32_t>((n + 255) / 256)),
+                       dim3(256), 0, stream, amax_ws, n);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    if (x_bf16 && t_bf16 && k >= 32) {
+        const uint16_t* Xb = static_cast<const uint16_t*>(X);
+        const uint16_t* Tb = static_cast<const uint16_t*>(T);
+        switch (k) {
+            case 32: return launch_tq_mfma<32, 32>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
+            case 64: return launch_tq_mfma<64, 64>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
+            case 128: return launch_tq_mfma<128, 128>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
+            case 256: return launch_tq_mfma<256, 128>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
+            case 512: return launch_tq_mfma<512, 64>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
+            default: break;
+        }
+    }
+    if (x_bf16 && t_bf16)
+        return launch_tq_generic(static_cast<const uint16_t*>(X), n, d,
+                                 static_cast<const uint16_t*>(T), k, codes, s_x, amax_ws, stream);
+    if (x_bf16)
+        return launch_tq_generic(static_cast<const uint16_t*>(X), n, d,
+                                 static_cast<const float*>(T), k, codes, s_x, amax_ws, stream);
+    if (t_bf16)
+        return launch_tq_generic(static_cast<const float*>(X), n, d,
+                                 static_cast<const uint16_t*>(T), k, codes, s_x, amax_ws, stream);
+    return launch_tq_generic(static_cast<const float*>(X), n, d, static_cast<const float*>(T), k,
+                             codes, s_x, amax_ws, stream);
+}
+
+}  // namespace catk

@@ -1,0 +1,34 @@
+// Launchers of the gfx950 kernels (host side).  Arguments are validated by
+// the C-ABI layer before any of these is called; each launcher enqueues
+// on `stream` and returns the launch status.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+#include "../../include/cat.h"
+
+namespace catk {
+
+// ---- SQNR (two passes)
+constexpr int kSqnrMaxBlocks = 2048;
+int sqnr_grid(int64_t count);
+hipError_t launch_sqnr(const float* y, const float* yt, int64_t count, double* partials,
+                       double* out, hipStream_t stream);
+
+// ---- transform + quantize
+// amax_ws: n uint32 words of scratch.
+hipError_t launch_transform_quant(const void* X, int x_bf16, int64_t n, int64_t d,
+                                  const void* T, int t_bf16, int64_t k, uint8_t* codes,
+                                  float* s_x, uint32_t* amax_ws, hipStream_t stream);
+
+// ---- W4A4 GEMM
+hipError_t launch_w4a4_linear(const uint8_t* codes_x, const float* s_x, const uint8_t* codes_w,
+                              const float* s_w, int64_t n, int64_t d_in, int64_t d_out,
+                              float* y, int32_t* acc_out, hipStream_t stream);
+
+// ---- second moment accumulation
+hipError_t launch_cov_accumulate(const void* X, int x_bf16, int64_t n, int64_t d, int mode,
+                                 int64_t k, float* acc, hipStream_t stream);
+
+}  // namespace catk

@@ -1,0 +1,83 @@
+"""Helpers shared by the GPU parity tests: device transfers and the
+comparison rules (integer exactness, the rounding-tie rule for codes,
+relative Frobenius error)."""
+import sys
+
+import numpy as np
+
+from oracle import cat_oracle as o
+
+
+def torch_mod():
+    import torch
+    if not torch.cuda.is_available():
+        raise RuntimeError("GPU tests need a HIP device (torch.cuda.is_available() is False)")
+    return torch
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def dev(a, dtype):
+    """numpy -> device tensor.  dtype 'bf16' expects values already
+    representable in bf16 (the conversion is then exact)."""
+    torch = torch_mod()
+    a = np.ascontiguousarray(a)
+    if dtype == "bf16":
+        t = torch.from_numpy(a.astype(np.float32)).to("cuda").to(torch.bfloat16)
+        back = t.float().cpu().numpy()
+        assert np.array_equal(back, a.astype(np.float32)), "value not representable in bf16"
+        return t
+    if dtype == "f32":
+        return torch.from_numpy(a.astype(np.float32)).to("cuda")
+    if dtype == "f64":
+        return torch.from_numpy(a.astype(np.float64)).to("cuda")
+    if dtype == "u8":
+        return torch.from_numpy(a.astype(np.uint8)).to("cuda")
+    if dtype == "i32":
+        return torch.from_numpy(a.astype(np.int32)).to("cuda")
+    raise ValueError(dtype)
+
+
+def host(t):
+    torch = torch_mod()
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def rel_fro(a, ref):
+    a = np.asarray(a, np.float64)
+    ref = np.asarray(ref, np.float64)
+    den = np.linalg.norm(ref)
+    return float(np.linalg.norm(a - ref) / den) if den > 0 else float(np.linalg.norm(a))
+
+
+def check_codes(codes_gpu_packed, X, T_blocks, bits=4, label=""):
+    """Codes must equal the oracle's except at exact rounding ties: a
+    mismatch must be off by one code and the oracle's exact multiplier
+    u* = z * qmax / amax (fp64) must lie within 2^-20 max(1, |u*|) of a
+    half-integer; at most 1e-6 of all codes (at least one allowed for
+    inputs with fewer than 1e6 codes) may be such ties.
+    Returns (n_mismatch, oracle codes, oracle scales)."""
+    q_or, s_or = o.transform_quant(X, T_blocks, bits)
+    q_gpu = o.unpack_int4(codes_gpu_packed)
+    mism = q_gpu != q_or
+    nm = int(mism.sum())
+    if nm:
+        Z = o.transform_rows(X, T_blocks)
+        amax = np.abs(Z).max(axis=1, keepdims=True)
+        with np.errstate(divide="ignore", invalid="ignore"):
+            u = Z * (o.qmax_of(bits) / amax)
+        um = np.abs(u[mism])
+        tie_dist = np.abs(um - np.floor(um) - 0.5)
+        is_tie = (np.abs(q_gpu[mism].astype(int) - q_or[mism].astype(int)) == 1) & \
+                 (tie_dist <= 2.0 ** -20 * np.maximum(1.0, um))
+        assert is_tie.all(), (
+            f"{label}: {int((~is_tie).sum())} non-tie code mismatches of {q_or.size}; "
+            f"first at {np.argwhere(mism)[:3].tolist()}")
+        allowed = max(1, int(1e-6 * q_or.size))
+        assert nm <= allowed, f"{label}: {nm} tie mismatches > {allowed}"
+    say(f"  {label}: codes {q_or.size}, tie mismatches {nm}")
+    return nm, q_or, s_or

@@ -1,0 +1,126 @@
+"""The C-ABI library loads, exports every symbol include/cat.h declares, and
+rejects invalid arguments with the documented status before touching the
+GPU.  No compute call runs here (no GPU in this environment)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2603_04359_amd as cat
+from paper_2603_04359_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cat.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(cat_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_header_declarations_match_binding_list():
+    assert _declared() == sorted(B.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol():
+    L = cat.lib()
+    for name in _declared():
+        assert hasattr(L, name), name
+        assert ctypes.cast(getattr(L, name), ctypes.c_void_p).value
+
+
+def test_version_and_error_strings():
+    assert cat.cat_version().startswith("cat-mi355x")
+    assert isinstance(cat.cat_last_error(), str)
+
+
+# Fake, 16-byte aligned addresses: every call below fails validation before
+# any pointer is dereferenced or any HIP call is made.
+P = 1 << 20
+
+
+def test_cov_invalid_args():
+    L = cat.lib()
+    assert L.cat_cov_accumulate(None, 1, 10, 64, 0, 1, P, None) == B.CAT_ERR_INVALID_ARG
+    assert "NULL" in cat.cat_last_error()
+    assert L.cat_cov_accumulate(P, 7, 10, 64, 0, 1, P, None) == B.CAT_ERR_INVALID_ARG
+    assert L.cat_cov_accumulate(P, 1, 0, 64, 0, 1, P, None) == B.CAT_ERR_INVALID_ARG
+    assert L.cat_cov_accumulate(P, 1, 10, 64, 5, 1, P, None) == B.CAT_ERR_INVALID_ARG
+    assert L.cat_cov_accumulate(P, 1, 10, 64, 1, 24, P, None) == B.CAT_ERR_INVALID_ARG
+    assert L.cat_cov_accumulate(P, 1, 10, 64, 1, 1024, P, None) == B.CAT_ERR_INVALID_ARG
+    assert L.cat_cov_accumulate(P, 1, 10, 96, 1, 64, P, None) == B.CAT_ERR_INVALID_ARG
+    assert L.cat_cov_accumulate(P + 2, 1, 10, 64, 0, 1, P, None) == B.CAT_ERR_INVALID_ARG
+    assert "aligned" in cat.cat_last_error()
+
+
+def test_transform_quant_invalid_args():
+    L = cat.lib()
+    ws = L.cat_transform_quant_workspace_bytes(8, 64, 16)
+    ok = dict(X=P, xd=1, n=8, d=64, T=P, td=1, k=16, bits=4, codes=P, s=P, ws=P, wsb=ws)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return L.cat_transform_quant(a["X"], a["xd"], a["n"], a["d"], a["T"], a["td"], a["k"],
+                                     a["bits"], a["codes"], a["s"], a["ws"], a["wsb"], None)
+    assert call(X=None) == B.CAT_ERR_INVALID_ARG
+    assert call(td=3) == B.CAT_ERR_INVALID_ARG
+    assert call(n=0) == B.CAT_ERR_INVALID_ARG
+    assert call(d=63) == B.CAT_ERR_INVALID_ARG
+    assert call(k=12) == B.CAT_ERR_INVALID_ARG
+    assert call(d=80, k=32) == B.CAT_ERR_INVALID_ARG
+    assert call(bits=8) == B.CAT_ERR_UNSUPPORTED
+    assert call(ws=None) == B.CAT_ERR_WORKSPACE
+    assert call(wsb=ws - 1) == B.CAT_ERR_WORKSPACE
+    assert call(codes=P + 8) == B.CAT_ERR_INVALID_ARG
+
+
+def test_w4a4_invalid_args():
+    L = cat.lib()
+    f = L.cat_w4a4_linear
+    assert f(None, P, P, P, 4, 64, 8, P, None, None) == B.CAT_ERR_INVALID_ARG
+    assert f(P, P, P, P, 0, 64, 8, P, None, None) == B.CAT_ERR_INVALID_ARG
+    assert f(P, P, P, P, 4, 48, 8, P, None, None) == B.CAT_ERR_INVALID_ARG
+    assert f(P, P, P, P, 4, 2 * B.CAT_MAX_D_IN, 8, P, None, None) == B.CAT_ERR_UNSUPPORTED
+    assert f(P, P, P, P, 4, 64, 8, P, P + 4, None) == B.CAT_ERR_INVALID_ARG
+
+
+def test_sqnr_invalid_args():
+    L = cat.lib()
+    ws = L.cat_sqnr_workspace_bytes(1000)
+    assert ws >= 16
+    assert L.cat_sqnr(None, P, 1000, P, ws, P, None) == B.CAT_ERR_INVALID_ARG
+    assert L.cat_sqnr(P, P, 0, P, ws, P, None) == B.CAT_ERR_INVALID_ARG
+    assert L.cat_sqnr(P, P, 1000, P, 8, P, None) == B.CAT_ERR_WORKSPACE
+    assert L.cat_sqnr(P, P, 1000, None, ws, P, None) == B.CAT_ERR_WORKSPACE
+
+
+def test_workspace_sizes_grow_and_are_bounded():
+    assert cat.cat_sqnr_workspace_bytes(1) == 16
+    assert cat.cat_sqnr_workspace_bytes(10 ** 10) == 2048 * 16
+    assert cat.cat_transform_quant_workspace_bytes(1, 64, 16) >= 4
+    assert cat.cat_transform_quant_workspace_bytes(8192, 4096, 128) >= 8192 * 4
+    assert cat.cat_transform_quant_workspace_bytes(0, 64, 16) == 0
+
+
+def test_host_calls_invalid_args():
+    L = cat.lib()
+    assert L.cat_build_transform(None, None, 8, 64, 16, 0, 1, None, None, None, 1) == \
+        B.CAT_ERR_INVALID_ARG
+    assert L.cat_build_transform(None, None, 8, 64, 16, 2, 1, P, None, None, 1) == \
+        B.CAT_ERR_INVALID_ARG
+    assert L.cat_build_transform(None, None, 8, 64, 12, 0, 1, P, None, None, 1) == \
+        B.CAT_ERR_INVALID_ARG
+    assert L.cat_build_transform(None, None, 8, 64, 16, 8, 1, P, None, None, 1) == \
+        B.CAT_ERR_INVALID_ARG
+    assert L.cat_quantize_weights(None, 4, 8, 4, P, P) == B.CAT_ERR_INVALID_ARG
+    assert L.cat_quantize_weights(P, 4, 7, 4, P, P) == B.CAT_ERR_INVALID_ARG
+
+
+def test_binding_rejects_cpu_tensors():
+    torch = pytest.importorskip("torch")
+    x = torch.zeros(4, 64, dtype=torch.bfloat16)
+    acc = torch.zeros(64, 64)
+    with pytest.raises(ValueError):
+        cat.cat_cov_accumulate(x, acc)

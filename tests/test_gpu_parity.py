@@ -1,0 +1,283 @@
+"""Parity of the four HIP kernels (through the C ABI) with the CPU oracle,
+at sizes the oracle finishes in seconds that span several tiles and ragged
+tails, plus the edge cases each kernel has."""
+import numpy as np
+import pytest
+
+import paper_2603_04359_amd as cat
+import workloads as wl
+from oracle import cat_oracle as o
+from paper_2603_04359_amd import binding as B
+
+from gpu_common import check_codes, dev, host, rel_fro, say, torch_mod
+
+pytestmark = pytest.mark.gpu
+
+
+# ------------------------------------------------------------------ SQNR
+@pytest.mark.parametrize("count", [1, 3, 1000, 4097, 4 * 256 * 2048 * 2 + 5])
+def test_sqnr_matches_oracle(count):
+    torch = torch_mod()
+    say(f"sqnr count={count}")
+    y, yt = wl.random_pair(count, seed=count % 1000)
+    S, E, dB = o.sqnr(y, yt)
+    ws = torch.empty(cat.cat_sqnr_workspace_bytes(count), dtype=torch.uint8, device="cuda")
+    out = torch.empty(3, dtype=torch.float64, device="cuda")
+    dy, dyt = dev(y, "f32"), dev(yt, "f32")
+    cat.cat_sqnr(dy, dyt, ws, out)
+    r = host(out)
+    assert r[0] == pytest.approx(S, rel=1e-12)
+    assert r[1] == pytest.approx(E, rel=1e-12)
+    assert abs(r[2] - dB) < 1e-6
+    # fixed reduction order: bit-reproducible
+    out2 = torch.empty_like(out)
+    cat.cat_sqnr(dy, dyt, ws, out2)
+    assert np.array_equal(host(out2), r)
+
+
+def test_sqnr_zero_error_is_infinite():
+    torch = torch_mod()
+    y, _ = wl.random_pair(777, seed=1)
+    dy = dev(y, "f32")
+    ws = torch.empty(cat.cat_sqnr_workspace_bytes(777), dtype=torch.uint8, device="cuda")
+    out = torch.empty(3, dtype=torch.float64, device="cuda")
+    cat.cat_sqnr(dy, dy.clone(), ws, out)
+    r = host(out)
+    assert r[1] == 0.0 and r[2] == np.inf
+
+
+# ------------------------------------------------------------------ GEMM
+def _gemm_case(n, d_in, d_out, seed, zero_rows=()):
+    torch = torch_mod()
+    qx = wl.random_codes(n, d_in, seed)
+    qw = wl.random_codes(d_out, d_in, seed + 1)
+    rng = np.random.default_rng(seed + 2)
+    sx = rng.uniform(0.01, 1.0, n).astype(np.float32)
+    sw = rng.uniform(0.01, 1.0, d_out).astype(np.float32)
+    for r in zero_rows:
+        qx[r] = 0
+        sx[r] = 0
+    acc_or, y_or = o.w4a4_linear(qx, sx, qw, sw)
+    y = torch.empty((n, d_out), dtype=torch.float32, device="cuda")
+    acc = torch.empty((n, d_out), dtype=torch.int32, device="cuda")
+    cat.cat_w4a4_linear(dev(o.pack_int4(qx), "u8"), dev(sx, "f32"), dev(o.pack_int4(qw), "u8"),
+                        dev(sw, "f32"), y, acc)
+    return host(acc), host(y), acc_or, y_or
+
+
+@pytest.mark.parametrize("n,d_in,d_out", [
+    (1, 32, 1), (130, 256, 200), (257, 4096, 384), (64, 160, 96), (300, 1024, 1000),
+])
+def test_w4a4_linear_matches_oracle(n, d_in, d_out):
+    say(f"w4a4 n={n} d_in={d_in} d_out={d_out}")
+    acc, y, acc_or, y_or = _gemm_case(n, d_in, d_out, seed=n + d_in, zero_rows=(0,))
+    assert np.array_equal(acc, acc_or)                 # int32 bit-exact
+    assert rel_fro(y, y_or) <= 1e-3                    # the stated bar
+    assert np.array_equal(y, y_or)                     # same fp32 epilogue order
+    assert not y[0].any()
+
+
+def test_w4a4_linear_extreme_codes_at_max_d_in():
+    torch = torch_mod()
+    d_in = B.CAT_MAX_D_IN
+    say(f"w4a4 extreme codes d_in={d_in}")
+    qx = np.full((2, d_in), 7, np.int8)
+    qx[1] = -7
+    qw = np.full((3, d_in), 7, np.int8)
+    qw[1] = -7
+    qw[2, ::2] = -7
+    sx = np.ones(2, np.float32)
+    sw = np.ones(3, np.float32)
+    acc_or, y_or = o.w4a4_linear(qx, sx, qw, sw)
+    y = torch.empty((2, 3), dtype=torch.float32, device="cuda")
+    acc = torch.empty((2, 3), dtype=torch.int32, device="cuda")
+    cat.cat_w4a4_linear(dev(o.pack_int4(qx), "u8"), dev(sx, "f32"), dev(o.pack_int4(qw), "u8"),
+                        dev(sw, "f32"), y, acc)
+    assert np.array_equal(host(acc), acc_or)
+    assert host(acc)[0, 0] == 49 * d_in
+
+
+# ------------------------------------------------------ transform + quant
+def _tq_gpu(X, T, k, x_dtype, t_dtype):
+    torch = torch_mod()
+    n, d = X.shape
+    dX = dev(X, x_dtype)
+    dT = dev(T, t_dtype)
+    codes = torch.empty((n, d // 2), dtype=torch.uint8, device="cuda")
+    s_x = torch.empty(n, dtype=torch.float32, device="cuda")
+    ws = torch.empty(cat.cat_transform_quant_workspace_bytes(n, d, k), dtype=torch.uint8,
+                     device="cuda")
+    cat.cat_transform_quant(dX, dT, k, codes, s_x, ws)
+    return host(codes), host(s_x)
+
+
+def _check_scales(s_gpu, s_or, label):
+    assert np.all((s_gpu == 0) == (s_or == 0)), label
+    nz = s_or != 0
+    rel = np.abs(s_gpu[nz].astype(np.float64) - s_or[nz]) / s_or[nz]
+    assert rel.max(initial=0) <= 1e-6, f"{label}: s_x rel err {rel.max()}"
+    say(f"  {label}: s_x max rel {rel.max(initial=0):.2e}, exact {np.mean(s_gpu == s_or):.4f}")
+
+
+def test_transform_quant_identity_is_exact_rtn():
+    # T = I: z = x exactly on both sides, so there is no tie ambiguity and
+    # every code and scale must be identical.
+    say("tq identity bf16 k=128")
+    X = wl.random_bf16_matrix(300, 512, seed=3, scale=2.0).astype(np.float64)
+    T = np.stack([np.eye(128)] * 4)
+    codes, s = _tq_gpu(X, T, 128, "bf16", "bf16")
+    q_or, s_or = o.transform_quant(X, T, 4)
+    assert np.array_equal(o.unpack_int4(codes), q_or)
+    assert np.array_equal(s, s_or)
+
+
+def _cat_T(X_cal, W, k, dtype):
+    S = o.second_moment(X_cal)
+    return o.round_storage(o.cat_transform(S, W, k), dtype)
+
+
+@pytest.mark.parametrize("k", [32, 64, 128, 256, 512])
+def test_transform_quant_cat_bf16(k):
+    say(f"tq CAT bf16 k={k}")
+    cfg = wl.get_config("attn4096", d_in=1024, d_out=512, k=k, n_cal=4096, n=257)
+    lay = wl.make_layer(cfg, seed=k)
+    X = lay["X"].astype(np.float64)
+    X[5] = 0.0                                   # a zero token row
+    T = _cat_T(lay["X_cal"], lay["W"], k, "bf16")
+    codes, s = _tq_gpu(X, T, k, "bf16", "bf16")
+    _, _, s_or = check_codes(codes, X, T, label=f"k={k}")
+    _check_scales(s, s_or, f"k={k}")
+    assert s[5] == 0 and not codes[5].any()
+
+
+def test_transform_quant_tiny_fp32_config():
+    say("tq tiny fp32 k=32")
+    cfg = wl.get_config("tiny")
+    lay = wl.make_layer(cfg, seed=0)
+    X = lay["X"].astype(np.float64)
+    T = _cat_T(lay["X_cal"], lay["W"], cfg.k, "f32")
+    codes, s = _tq_gpu(X, T, cfg.k, "f32", "f32")
+    _, _, s_or = check_codes(codes, X, T, label="tiny")
+    _check_scales(s, s_or, "tiny")
+
+
+@pytest.mark.parametrize("x_dtype,t_dtype,k,n", [
+    ("bf16", "f32", 64, 129), ("f32", "bf16", 64, 129), ("bf16", "bf16", 16, 70),
+    ("bf16", "bf16", 1, 33), ("f32", "f32", 8, 1), ("bf16", "bf16", 128, 1),
+])
+def test_transform_quant_other_paths(x_dtype, t_dtype, k, n):
+    say(f"tq {x_dtype}/{t_dtype} k={k} n={n}")
+    d = 256
+    rng = np.random.default_rng(k + n)
+    Xf = (rng.standard_normal((n, d)) * np.exp(rng.standard_normal(d))).astype(np.float32)
+    X = o.round_storage(Xf, x_dtype)
+    W = rng.standard_normal((96, d))
+    T = _cat_T(Xf[:, :] if n > 8 else rng.standard_normal((512, d)), W, k, t_dtype)
+    codes, s = _tq_gpu(X, T, k, x_dtype, t_dtype)
+    _, _, s_or = check_codes(codes, X, T, label=f"{x_dtype}/{t_dtype} k={k}")
+    _check_scales(s, s_or, f"{x_dtype}/{t_dtype} k={k}")
+
+
+# ------------------------------------------------------- second moment
+def _cov_gpu(X, dtype, mode, k, acc0=None, splits=None):
+    torch = torch_mod()
+    n, d = X.shape
+    shape = (d, d) if mode == B.CAT_COV_FULL else (d // k, k, k)
+    acc = torch.zeros(shape, dtype=torch.float32, device="cuda") if acc0 is None else acc0
+    dX = dev(X, dtype)
+    bounds = [0] + list(splits or []) + [n]
+    for a, b in zip(bounds[:-1], bounds[1:]):
+        cat.cat_cov_accumulate(dX[a:b], acc, mode, k)
+    return host(acc)
+
+
+def _blocks(S, k):
+    d = S.shape[0]
+    return np.stack([S[b * k:(b + 1) * k, b * k:(b + 1) * k] for b in range(d // k)])
+
+
+@pytest.mark.parametrize("d,n,dtype", [(256, 5000, "bf16"), (320, 1000, "bf16"),
+                                       (256, 2048, "f32"), (96, 300, "bf16")])
+def test_cov_full_matches_oracle(d, n, dtype):
+    say(f"cov full d={d} n={n} {dtype}")
+    cfg = wl.get_config("attn4096", d_in=d, d_out=d, n_cal=n, n=1)
+    X = wl.make_layer(cfg, seed=d + n, with_eval=False, with_weights=False)["X_cal"]
+    X = o.round_storage(X, dtype)
+    acc = _cov_gpu(X, dtype, B.CAT_COV_FULL, 1)
+    ref = o.second_moment_sum(X)
+    err = rel_fro(acc, ref)
+    say(f"  rel fro {err:.2e}")
+    assert err <= 1e-5
+    assert np.array_equal(acc, acc.T)
+
+
+@pytest.mark.parametrize("k,dtype", [(64, "bf16"), (128, "bf16"), (256, "bf16"), (32, "bf16"),
+                                     (32, "f32")])
+def test_cov_block_diag_matches_oracle(k, dtype):
+    say(f"cov block k={k} {dtype}")
+    d, n = 512, 4500
+    cfg = wl.get_config("attn4096", d_in=d, d_out=d, n_cal=n, n=1)
+    X = o.round_storage(wl.make_layer(cfg, seed=k, with_eval=False, with_weights=False)["X_cal"],
+                        dtype)
+    acc = _cov_gpu(X, dtype, B.CAT_COV_BLOCK_DIAG, k)
+    ref = _blocks(o.second_moment_sum(X), k)
+    err = rel_fro(acc, ref)
+    say(f"  rel fro {err:.2e}")
+    assert err <= 1e-5
+
+
+def test_cov_split_batches_equal_one_shot():
+    say("cov split batches")
+    cfg = wl.get_config("attn4096", d_in=256, d_out=256, n_cal=3000, n=1)
+    X = o.round_storage(wl.make_layer(cfg, seed=11, with_eval=False,
+                                      with_weights=False)["X_cal"], "bf16")
+    one = _cov_gpu(X, "bf16", B.CAT_COV_FULL, 1)
+    split = _cov_gpu(X, "bf16", B.CAT_COV_FULL, 1, splits=[1, 700, 2001])
+    assert rel_fro(split, one) <= 1e-6
+    assert rel_fro(split, o.second_moment_sum(X)) <= 1e-5
+
+
+# ------------------------------------------------------------ end to end
+@pytest.mark.parametrize("transform", ["I", "H", "CAT"])
+def test_end_to_end_tiny_layer_sqnr(transform):
+    """C1 (tiny, fp32): GPU Sigma_x -> host transform -> GPU transform+quant
+    -> GPU W4A4 GEMM -> GPU SQNR, against the oracle's own chain from the
+    same generator arrays; SQNR within 0.05 dB."""
+    torch = torch_mod()
+    say(f"end-to-end tiny T={transform}")
+    cfg = wl.get_config("tiny")
+    lay = wl.make_layer(cfg, seed=0)
+    Xc, X, W = lay["X_cal"], lay["X"], lay["W"]
+    k, d = cfg.k, cfg.d_in
+    flags = {"I": 0, "H": B.CAT_BUILD_HADAMARD, "CAT": B.CAT_BUILD_CAT}[transform]
+    # GPU calibration (block-diagonal second moment)
+    acc = torch.zeros((d // k, k, k), dtype=torch.float32, device="cuda")
+    cat.cat_cov_accumulate(dev(Xc, "f32"), acc, B.CAT_COV_BLOCK_DIAG, k)
+    sx_blocks = host(acc).astype(np.float64) / cfg.n_cal
+    T, _, Wp = cat.cat_build_transform(sx_blocks, W, k, flags, B.CAT_F32)
+    cw, sw = cat.cat_quantize_weights(Wp, 4)
+    n = X.shape[0]
+    codes = torch.empty((n, d // 2), dtype=torch.uint8, device="cuda")
+    s_x = torch.empty(n, dtype=torch.float32, device="cuda")
+    ws = torch.empty(cat.cat_transform_quant_workspace_bytes(n, d, k), dtype=torch.uint8,
+                     device="cuda")
+    cat.cat_transform_quant(dev(X, "f32"), dev(T, "f32"), k, codes, s_x, ws)
+    yt = torch.empty((n, cfg.d_out), dtype=torch.float32, device="cuda")
+    cat.cat_w4a4_linear(codes, s_x, dev(cw, "u8"), dev(sw, "f32"), yt)
+    y = o.reference_output(X, W).astype(np.float32)
+    sws = torch.empty(cat.cat_sqnr_workspace_bytes(y.size), dtype=torch.uint8, device="cuda")
+    out = torch.empty(3, dtype=torch.float64, device="cuda")
+    cat.cat_sqnr(dev(y, "f32"), yt, sws, out)
+    gpu_db = float(host(out)[2])
+    # oracle chain
+    if transform == "I":
+        To = np.stack([np.eye(k)] * (d // k))
+    elif transform == "H":
+        To = o.cat_transform(None, W, k, use_alignment=False)
+    else:
+        To = o.cat_transform(o.second_moment(Xc), W, k)
+    To = o.round_storage(To, "f32")
+    fw = o.quantized_forward(X.astype(np.float64), To, o.transform_weights(W, To), 4)
+    or_db = o.sqnr(y, fw["y_tilde"])[2]
+    say(f"  SQNR gpu {gpu_db:.4f} dB, oracle {or_db:.4f} dB")
+    assert abs(gpu_db - or_db) <= 0.05

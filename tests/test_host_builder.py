@@ -1,0 +1,114 @@
+"""The library's host-side transform construction and weight quantizer
+against the CPU oracle (independent implementations of Sec. 4, eq. 7 and
+eq. 10, and of the Sec. 6 weight quantizer)."""
+import numpy as np
+import pytest
+
+import paper_2603_04359_amd as cat
+import workloads as wl
+from oracle import cat_oracle as o
+from paper_2603_04359_amd import binding as B
+
+
+def _diag_blocks(S, k):
+    d = S.shape[0]
+    return np.stack([S[b * k:(b + 1) * k, b * k:(b + 1) * k] for b in range(d // k)])
+
+
+def _bf16_boundary_distance(v):
+    """Relative distance of fp64 values to the nearest bf16 rounding
+    boundary (midpoint between two bf16 neighbours), computed in fp64."""
+    f = np.abs(np.asarray(v, np.float64))
+    e = np.floor(np.log2(np.where(f > 0, f, 1.0)))
+    ulp = 2.0 ** (e - 7)
+    frac = f / ulp - np.floor(f / ulp)
+    return np.abs(frac - 0.5) * ulp / np.where(f > 0, f, 1.0)
+
+
+def _layer(d_in, d_out, k, n_cal, seed):
+    rng = np.random.default_rng(seed)
+    scale = np.exp(rng.standard_normal(d_in))
+    scale[rng.choice(d_in, 3, replace=False)] *= 30
+    X = (rng.standard_normal((n_cal, d_in)) * scale).astype(np.float32)
+    W = (rng.standard_normal((d_out, d_in)) / np.sqrt(d_in)).astype(np.float32)
+    return X, W
+
+
+@pytest.mark.parametrize("d_in,d_out,k,t_dtype", [
+    (64, 48, 16, "bf16"), (256, 256, 32, "f32"), (256, 200, 64, "bf16"), (512, 384, 128, "bf16"),
+])
+def test_build_transform_matches_oracle(d_in, d_out, k, t_dtype):
+    X, W = _layer(d_in, d_out, k, 4096, seed=d_in + k)
+    S = o.second_moment(X)
+    T_or = o.cat_transform(S, W, k)
+    td = B.CAT_BF16 if t_dtype == "bf16" else B.CAT_F32
+    T, Te, Wp = cat.cat_build_transform(_diag_blocks(S, k), W, k, B.CAT_BUILD_CAT, td,
+                                        want_exact=True, n_threads=4)
+    # fp64 transform before rounding (cond of the blocks is moderate here)
+    err = np.abs(Te - T_or).max() / np.abs(T_or).max()
+    assert err < 1e-9, err
+    # rounded transform: identical except where the fp64 value sits on a
+    # rounding boundary (relative distance below the solvers' disagreement)
+    T_or_r = o.round_storage(T_or, t_dtype)
+    T_lib = (wl.bf16_bits_to_f32(T) if t_dtype == "bf16" else T).astype(np.float64)
+    diff = T_lib != T_or_r
+    if t_dtype == "bf16":
+        assert np.all(_bf16_boundary_distance(T_or[diff]) < 1e-8)
+    else:
+        assert np.all(np.abs(Te[diff] - T_or[diff]) <= 1e-9 * np.abs(T_or[diff]))
+    assert diff.mean() < 1e-3
+    # W' = W T^-1 with the rounded T (oracle on its own rounded T)
+    if not diff.any():
+        Wp_or = o.transform_weights(W, T_or_r)
+        assert np.abs(Wp - Wp_or).max() <= 1e-9 * np.abs(Wp_or).max()
+    # function preservation W' T x = W x with the library's own outputs
+    Z = o.transform_rows(X[:64].astype(np.float64), T_lib)
+    ref = X[:64].astype(np.float64) @ W.astype(np.float64).T
+    assert np.abs(Z @ Wp.T - ref).max() <= 1e-9 * np.abs(ref).max()
+
+
+def test_build_transform_identity_and_hadamard_flags():
+    _, W = _layer(128, 64, 32, 16, seed=3)
+    T, _, Wp = cat.cat_build_transform(None, W, 32, 0, B.CAT_F32)
+    assert np.array_equal(T, np.stack([np.eye(32, dtype=np.float32)] * 4))
+    assert np.array_equal(Wp, W.astype(np.float64))
+    T, _, Wp = cat.cat_build_transform(None, W, 32, B.CAT_BUILD_HADAMARD, B.CAT_F32)
+    H = o.hadamard(32).astype(np.float32)
+    assert np.array_equal(T, np.stack([H] * 4))
+
+
+def test_build_transform_k1_closed_form():
+    X, W = _layer(32, 40, 1, 2048, seed=5)
+    S = o.second_moment(X)
+    T, Te, _ = cat.cat_build_transform(_diag_blocks(S, 1), W, 1, B.CAT_BUILD_ALIGN, B.CAT_F32,
+                                       want_exact=True)
+    m = (np.sum(W.astype(np.float64) ** 2, 0) / np.diag(S)) ** 0.25
+    np.testing.assert_allclose(Te[:, 0, 0], m, rtol=1e-12)
+
+
+def test_build_transform_ill_conditioned_block():
+    # nearly rank-deficient calibration block: the eigenvalue floor keeps the
+    # result finite and invertible
+    rng = np.random.default_rng(7)
+    k = 16
+    A = rng.standard_normal((k, 3))
+    S = A @ A.T + 1e-9 * np.eye(k)
+    W = rng.standard_normal((32, k)).astype(np.float32)
+    T, Te, Wp = cat.cat_build_transform(S[None], W, k, B.CAT_BUILD_CAT, B.CAT_F32, want_exact=True)
+    assert np.all(np.isfinite(Te)) and np.all(np.isfinite(Wp))
+    T_or = o.cat_transform(S, W, k)
+    # the two eigensolvers agree to about eps * cond(S) (cond ~ 3e10 here)
+    cond = np.linalg.cond(S)
+    assert np.abs(Te - T_or).max() / np.abs(T_or).max() < 1e-15 * cond
+
+
+def test_quantize_weights_matches_oracle_bit_exact():
+    rng = np.random.default_rng(9)
+    Wp = rng.standard_normal((70, 96)) * np.exp(rng.standard_normal(70))[:, None]
+    Wp[3] = 0.0
+    Wp[5, 7] = 1e3
+    codes, s_w = cat.cat_quantize_weights(Wp, 4)
+    q_or, s_or = o.quantize_weights(Wp, 4)
+    assert np.array_equal(codes, o.pack_int4(q_or))
+    assert np.array_equal(s_w, s_or)
+    assert s_w[3] == 0 and not codes[3].any()

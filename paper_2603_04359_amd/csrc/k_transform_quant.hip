@@ -30,6 +30,7 @@ namespace catk {
 
 constexpr int kTqThreads = 256;
 constexpr float kQmax4 = 7.0f;
+constexpr int64_t kTqTargetWorkgroups = 512;
 
 __global__ void fill_zero_u32_kernel(uint32_t* p, int64_t n) {
     const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
@@ -95,10 +96,15 @@ __global__ __launch_bounds__(kTqThreads) void tq_generic_quant_kernel(
 }
 
 // --------------------------------------------------------------- MFMA path
-// Workgroup = 4 waves; tile = 128 tokens (32 per wave) x JC output rows of
-// one block.  LDS holds the JC x K slice of T_b as 16-byte units, unit u of
-// row r stored at position u ^ swz(r) so that 16 lanes reading 16
-// consecutive rows at the same unit hit 16 distinct bank groups.
+// Persistent workgroups of 4 waves.  Workgroup w owns output rows
+// [jc*JC, jc*JC + JC) of block b (bj = w % NBJ) for the token tiles
+// r, r + R, r + 2R, ... (r = w / NBJ; a tile is 128 tokens, 32 per wave).
+// Its slice of T_b is staged in LDS once, as 16-byte units with unit u of
+// row r stored at position u ^ swz(r), so that 16 lanes reading 16
+// consecutive rows at the same unit hit 16 distinct bank groups.  The
+// next tile's activations are fetched into registers while the current
+// tile is multiplied.  Workgroups sharing a T_b slice are NBJ apart in
+// launch order, i.e. on the same XCD whenever NBJ is a multiple of 8.
 template <int K>
 __device__ __forceinline__ int tq_swz(int r) {
     constexpr int U = K / 8;                   // 16-byte units per row
@@ -110,23 +116,23 @@ __device__ __forceinline__ int tq_swz(int r) {
 template <int K, int JC, bool QUANT>
 __global__ __launch_bounds__(kTqThreads) void tq_mfma_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ T, int64_t n, int64_t d,
-    uint32_t* __restrict__ amax_ws, uint8_t* __restrict__ codes, float* __restrict__ s_x) {
+    int64_t R, uint32_t* __restrict__ amax_ws, uint8_t* __restrict__ codes,
+    float* __restrict__ s_x) {
     static_assert(K % 32 == 0 && JC % 32 == 0 && K % JC == 0, "tile shape");
     constexpr int U = K / 8;
     constexpr int NCHUNK = K / JC;
     constexpr int NM = JC / 32;     // 32-row MFMA tiles per wave
     constexpr int NS = K / 16;      // 16-deep MFMA steps
+    constexpr bool PREFETCH = NS <= 16;
     __shared__ u32x4 t_lds[JC * U];
 
-    const int64_t nblk = d / K;
-    const int64_t work = blockIdx.x;
-    const int64_t bj = work % (nblk * NCHUNK);
-    const int64_t tile = work / (nblk * NCHUNK);
+    const int64_t nbj = (d / K) * NCHUNK;
+    const int64_t bj = blockIdx.x % nbj;
+    const int64_t r0 = blockIdx.x / nbj;
     const int64_t b = bj / NCHUNK;
     const int jc = static_cast<int>(bj % NCHUNK);
-    const int64_t t0 = tile * 128;
+    const int64_t ntiles = (n + 127) / 128;
 
-    // stage rows [jc*JC, jc*JC+JC) of T_b into LDS
     const u32x4* tg = reinterpret_cast<const u32x4*>(T + (b * K + static_cast<int64_t>(jc) * JC) * K);
     for (int i = threadIdx.x; i < JC * U; i += kTqThreads) {
         const int r = i / U, u = i % U;
@@ -138,69 +144,85 @@ __global__ __launch_bounds__(kTqThreads) void tq_mfma_kernel(
     const int wave = threadIdx.x / kWave;
     const int col = lane & 31;      // token within the wave's 32
     const int h = lane >> 5;        // which 8-element half of a 16-deep step
-    const int64_t t = t0 + wave * 32 + col;
-    const bool valid = t < n;
-    if (t0 + wave * 32 >= n) return;   // no barrier follows
 
-    // B operand: 8 consecutive bf16 of the token row per step
+    // B operand: 8 consecutive bf16 of the token row per 16-deep step
+    auto load_x = [&](int64_t tile, u32x4* xb) {
+        const int64_t t = tile * 128 + wave * 32 + col;
+        const u32x4* xg = reinterpret_cast<const u32x4*>(X + t * d + b * K);
+#pragma unroll
+        for (int s = 0; s < NS; ++s) xb[s] = t < n ? xg[2 * s + h] : u32x4{0u, 0u, 0u, 0u};
+    };
+
     u32x4 xb[NS];
-    const u32x4* xg = reinterpret_cast<const u32x4*>(X + t * d + b * K);
-#pragma unroll
-    for (int s = 0; s < NS; ++s) {
-        if (valid) xb[s] = xg[2 * s + h];
-        else xb[s] = u32x4{0u, 0u, 0u, 0u};
-    }
+    u32x4 xn[PREFETCH ? NS : 1];
+    if (r0 < ntiles) load_x(r0, xb);
+    for (int64_t tile = r0; tile < ntiles; tile += R) {
+        if constexpr (PREFETCH) {
+            if (tile + R < ntiles) load_x(tile + R, xn);
+        }
+        const int64_t t = tile * 128 + wave * 32 + col;
+        const bool valid = t < n;
 
-    f32x16 acc[NM];
+        f32x16 acc[NM];
 #pragma unroll
-    for (int m = 0; m < NM; ++m) {
-        acc[m] = f32x16{};
-        const int r = m * 32 + col;
+        for (int m = 0; m < NM; ++m) acc[m] = f32x16{};
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
-            const u32x4 a = t_lds[r * U + ((2 * s + h) ^ tq_swz<K>(r))];
-            acc[m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(xb[s]),
-                                                             acc[m], 0, 0, 0);
+#pragma unroll
+            for (int m = 0; m < NM; ++m) {
+                const int r = m * 32 + col;
+                const u32x4 a = t_lds[r * U + ((2 * s + h) ^ tq_swz<K>(r))];
+                acc[m] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(a), as_bf16x8(xb[s]),
+                                                                 acc[m], 0, 0, 0);
+            }
         }
-    }
 
-    if constexpr (!QUANT) {
-        uint32_t m_bits = 0;
+        if constexpr (!QUANT) {
+            uint32_t m_bits = 0;
 #pragma unroll
-        for (int m = 0; m < NM; ++m)
+            for (int m = 0; m < NM; ++m)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) m_bits = max(m_bits, abs_bits(acc[m][r]));
-        m_bits = max(m_bits, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m_bits), 32)));
-        if (valid && h == 0 && m_bits) atomicMax(amax_ws + t, m_bits);
-    } else {
-        const float amax = valid ? __uint_as_float(amax_ws[t]) : 0.0f;
-        if (valid && h == 0 && b == 0 && jc == 0) s_x[t] = __fdiv_rn(amax, kQmax4);
-        const bool nz = amax > 0.0f;
-        const float inv = nz ? __fdiv_rn(kQmax4, amax) : 0.0f;
-        uint32_t* crow = reinterpret_cast<uint32_t*>(codes + t * (d / 2) + b * (K / 2) +
-                                                     static_cast<int64_t>(jc) * (JC / 2));
+                for (int q = 0; q < 16; ++q) m_bits = max(m_bits, abs_bits(acc[m][q]));
+            m_bits = max(m_bits, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m_bits), 32)));
+            if (valid && h == 0 && m_bits) atomicMax(amax_ws + t, m_bits);
+        } else {
+            const float amax = valid ? __uint_as_float(amax_ws[t]) : 0.0f;
+            if (valid && h == 0 && b == 0 && jc == 0) s_x[t] = __fdiv_rn(amax, kQmax4);
+            const bool nz = amax > 0.0f;
+            const float inv = nz ? __fdiv_rn(kQmax4, amax) : 0.0f;
+            uint32_t* crow = reinterpret_cast<uint32_t*>(codes + t * (d / 2) + b * (K / 2) +
+                                                         static_cast<int64_t>(jc) * (JC / 2));
 #pragma unroll
-        for (int m = 0; m < NM; ++m) {
-            // v[q]: codes of rows 32m + 8q + 4h + (0..3), packed in 16 bits
-            uint32_t v[4];
+            for (int m = 0; m < NM; ++m) {
+                // v[q]: codes of rows 32m + 8q + 4h + (0..3), packed in 16 bits
+                uint32_t v[4];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                uint32_t p = 0;
-                if (nz) {
+                for (int q = 0; q < 4; ++q) {
+                    uint32_t p = 0;
+                    if (nz) {
 #pragma unroll
-                    for (int e = 0; e < 4; ++e)
-                        p |= static_cast<uint32_t>(quant_code(acc[m][4 * q + e], inv) & 0xF) << (4 * e);
+                        for (int e = 0; e < 4; ++e)
+                            p |= static_cast<uint32_t>(quant_code(acc[m][4 * q + e], inv) & 0xF)
+                                 << (4 * e);
+                    }
+                    v[q] = p;
                 }
-                v[q] = p;
-            }
 #pragma unroll
-            for (int qp = 0; qp < 4; qp += 2) {
-                // h=0 owns rows 8qp+0..7 of (qp), h=1 owns rows of (qp+1)
-                const uint32_t send = h ? v[qp] : v[qp + 1];
-                const uint32_t recv = static_cast<uint32_t>(__shfl_xor(static_cast<int>(send), 32));
-                const uint32_t word = h ? (recv | (v[qp + 1] << 16)) : (v[qp] | (recv << 16));
-                if (valid) crow[(m * 32 + 8 * (qp + h)) / 8] = word;
+                for (int qp = 0; qp < 4; qp += 2) {
+                    // h=0 stores rows 8qp+0..7 of group qp, h=1 those of group qp+1
+                    const uint32_t send = h ? v[qp] : v[qp + 1];
+                    const uint32_t recv =
+                        static_cast<uint32_t>(__shfl_xor(static_cast<int>(send), 32));
+                    const uint32_t word = h ? (recv | (v[qp + 1] << 16)) : (v[qp] | (recv << 16));
+                    if (valid) crow[(m * 32 + 8 * (qp + h)) / 8] = word;
+                }
             }
+        }
+        if constexpr (PREFETCH) {
+#pragma unroll
+            for (int s = 0; s < NS; ++s) xb[s] = xn[s];
+        } else {
+            if (tile + R < ntiles) load_x(tile + R, xb);
         }
     }
 }
@@ -209,15 +231,21 @@ template <int K, int JC>
 hipError_t launch_tq_mfma(const uint16_t* X, int64_t n, int64_t d, const uint16_t* T,
                           uint8_t* codes, float* s_x, uint32_t* ws, hipStream_t stream) {
     const int64_t tiles = (n + 127) / 128;
-    const int64_t grid = tiles * (d / K) * (K / JC);
+    const int64_t nbj = (d / K) * (K / JC);
+    // about two resident workgroups per CU, each looping over R token tiles
+    int64_t R = (kTqTargetWorkgroups + nbj - 1) / nbj;
+    if (R > tiles) R = tiles;
+    if (R < 1) R = 1;
+    const int64_t grid = nbj * R;
     hipLaunchKernelGGL((tq_mfma_kernel<K, JC, false>), dim3(static_cast<uint32_t>(grid)),
-                       dim3(kTqThreads), 0, stream, X, T, n, d, ws, codes, s_x);
+                       dim3(kTqThreads), 0, stream, X, T, n, d, R, ws, codes, s_x);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
     hipLaunchKernelGGL((tq_mfma_kernel<K, JC, true>), dim3(static_cast<uint32_t>(grid)),
-                       dim3(kTqThreads), 0, stream, X, T, n, d, ws, codes, s_x);
+                       dim3(kTqThreads), 0, stream, X, T, n, d, R, ws, codes, s_x);
     return hipGetLastError();
 }
+
 
 template <typename XT, typename TT>
 hipError_t launch_tq_generic(const XT* X, int64_t n, int64_t d, const TT* T, int64_t k,

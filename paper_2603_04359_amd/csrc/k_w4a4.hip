@@ -2,163 +2,339 @@
 //   acc[t, o] = sum_j qx[t, j] qw[o, j]                   (int32, exact)
 //   y[t, o]   = fl32(fl32(acc) * s_x[t]) * s_w[o]
 //
-// gfx950 int8 MFMA (v_mfma_i32_32x32x32_i8) on INT4 codes.  Tiles of packed
-// codes (half the bytes of int8) are staged in LDS; each lane reads 16
-// packed bytes and widens them in registers to int8 values 16*code with
-// two bit operations per dword (low nibbles and high nibbles go to
-// separate dwords).  Both operands are widened identically, so each MFMA
-// sums the same index pairs (a permutation of the reduction index) and
-// the int32 result is 256 * acc; an arithmetic shift by 8 recovers acc
-// exactly for d_in <= 131072.
+// gfx950 int8 MFMA (v_mfma_i32_32x32x32_i8) on INT4 codes.
 //
-// Workgroup: 256 threads (4 waves, 2 x 2), output tile 128 x 128, each
-// wave 64 x 64 = 2 x 2 MFMA tiles.  K step 128 codes (64 packed bytes per
-// row); the next step's tiles are fetched into registers while the current
-// step runs out of the other LDS buffer.  16-byte LDS units are
-// XOR-swizzled per row so fragment reads of 16 consecutive rows are
-// bank-conflict free.
+// Tiles: 256 x 128 outputs per workgroup of 256 threads = 4 waves in a
+// 2 x 2 grid, each wave 128 x 64 = 4 x 2 MFMA tiles with int32
+// accumulators; two workgroups are resident per CU, so one workgroup's
+// barrier waits and output stores overlap the other's MFMAs.  One K step
+// covers 128 codes (64 packed bytes per row).
+//
+// Operand path: packed INT4 tiles go straight from global memory into an
+// LDS ring of kStages steps with global_load_lds_dwordx4 (no register
+// staging, no LDS store instructions), issued kStages-1 steps ahead of
+// use, with one barrier per step that waits for LDS traffic only (a plain
+// workgroup barrier would also drain the loads in flight).  Each lane reads
+// 16 packed bytes (32 codes, two MFMA steps) per fragment and widens them
+// in registers to int8 values 16*code: a packed dword (8 codes) becomes one
+// dword of its low nibbles and one of its high nibbles, two bit operations
+// each.  The widening of the next 32-code step is independent of the MFMAs
+// of the current one, so it co-issues with them.  Both operands are widened
+// identically, so each MFMA sums the same index pairs (a permutation of the
+// reduction index) and the int32 result is 256 * acc; an arithmetic shift
+// by 8 recovers acc exactly for d_in <= 131072.
+//
+// LDS layout: each operand stage is rows x 4 units of 16 bytes; unit u of
+// row r sits at slot 4r + (u ^ swz(r)), which keeps 16- and 32-lane groups
+// of fragment reads (32 consecutive rows, one unit) free of bank
+// conflicts.  The direct loads fill 64 consecutive slots per wave
+// instruction, so each lane loads the global unit that belongs in its slot
+// (a permutation inside each 64-byte row segment).  Rows past the end of a
+// matrix load a clamped in-bounds row (their outputs are never stored);
+// units past d_in in a ragged last step load any in-bounds unit and the
+// loading thread clears them in LDS before the step's barrier, which
+// zeroes their products.
+//
+// Persistent launch: kWgPerCu workgroups per CU walk lists of tiles in an
+// XCD-aware order (workgroups are dealt to the 8 XCDs round-robin; those of
+// XCD x walk one contiguous range of tiles, in groups of kGroupM row
+// panels, so tiles resident on one XCD share panels in its L2).  The first
+// steps of the next tile are requested before the current tile's output is
+// stored.  Output rows stream out with nontemporal stores.
 #include "device_common.h"
 #include "kernels.h"
 
 namespace catk {
 
 constexpr int kGemmThreads = 256;
-constexpr int kBM = 128;          // tokens per tile
-constexpr int kBN = 128;          // outputs per tile
-constexpr int kBKB = 64;          // packed bytes per row per K step (128 codes)
-constexpr int kUnits = kBKB / 16; // 16-byte units per row per step
+constexpr int kBM = 256;           // tokens per tile
+constexpr int kBN = 128;           // outputs per tile
+constexpr int kKBP = 64;           // packed bytes per row per K step (128 codes)
+constexpr int kUP = kKBP / 16;     // 16-byte units per row per step
+constexpr int kStages = 3;         // LDS ring depth (steps)
+constexpr int kAUnits = kBM * kUP;                   // A units per stage
+constexpr int kBUnits = kBN * kUP;                   // B units per stage
+constexpr int kLoadsA = kAUnits / kGemmThreads;      // direct loads per thread, A
+constexpr int kLoadsB = kBUnits / kGemmThreads;      // direct loads per thread, B
+constexpr int kWgPerCu = 2;
+constexpr int kGroupM = 4;         // row panels per tile group
+constexpr int kXcd = 8;
 
-__device__ __forceinline__ int gemm_swz(int r) { return (r >> 2) & 3; }
+__device__ __forceinline__ int gemm_swz(int r) {
+    const int q = r & 31;
+    return ((q >> 2) ^ (q >> 4)) & 3;
+}
 
-__device__ __forceinline__ i32x4 widen_lo_pair(u32x4 v, int half) {
-    // 8 packed bytes (dwords 2*half, 2*half+1) -> 16 int8 values * 16
+// s_waitcnt with only the vector-memory counter limited (gfx9 encoding:
+// vmcnt in bits 3:0 and 15:14; expcnt and lgkmcnt left at their maxima).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Workgroup barrier that only waits for this wave's own LDS operations;
+// vector-memory loads in flight stay in flight (a plain __syncthreads()
+// would also drain them, which defeats a multi-step prefetch).
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0), vmcnt/expcnt unlimited
+    __builtin_amdgcn_s_barrier();
+}
+
+struct GemmTile {
+    int64_t m0, n0;
+};
+
+__device__ __forceinline__ bool gemm_tile(int64_t k, int64_t n, int64_t d_out, GemmTile& t) {
+    const int64_t tiles_m = (n + kBM - 1) / kBM;
+    const int64_t tiles_n = (d_out + kBN - 1) / kBN;
+    const int64_t T = tiles_m * tiles_n;
+    const int64_t per_xcd = (T + kXcd - 1) / kXcd;
+    const int64_t wg_per_xcd = gridDim.x / kXcd;
+    const int64_t x = blockIdx.x % kXcd, j = blockIdx.x / kXcd;
+    const int64_t local = j + k * wg_per_xcd;
+    if (local >= per_xcd) return false;
+    const int64_t tau = x * per_xcd + local;
+    if (tau >= T) return false;
+    const int64_t group = tau / (kGroupM * tiles_n);
+    const int64_t first_m = group * kGroupM;
+    const int64_t gm = (tiles_m - first_m) < kGroupM ? (tiles_m - first_m) : kGroupM;
+    const int64_t in_group = tau % (kGroupM * tiles_n);
+    t.m0 = (first_m + in_group % gm) * kBM;
+    t.n0 = (in_group / gm) * kBN;
+    return true;
+}
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+__device__ __forceinline__ i32x4 widen8(u32x4 v, int half) {
     const uint32_t w0 = v[2 * half], w1 = v[2 * half + 1];
     return i32x4{static_cast<int>(unpack_lo16(w0)), static_cast<int>(unpack_hi16(w0)),
                  static_cast<int>(unpack_lo16(w1)), static_cast<int>(unpack_hi16(w1))};
 }
 
-__global__ __launch_bounds__(kGemmThreads) void w4a4_gemm_kernel(
+__global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
     const uint8_t* __restrict__ qx, const float* __restrict__ s_x,
     const uint8_t* __restrict__ qw, const float* __restrict__ s_w, int64_t n, int64_t d_in,
     int64_t d_out, float* __restrict__ y, int32_t* __restrict__ acc_out) {
-    __shared__ u32x4 lds_a[2][kBM * kUnits];
-    __shared__ u32x4 lds_b[2][kBN * kUnits];
+    __shared__ __attribute__((aligned(16))) u32x4 ring_a[kStages][kAUnits];
+    __shared__ __attribute__((aligned(16))) u32x4 ring_b[kStages][kBUnits];
 
-    const int64_t tiles_n = (d_out + kBN - 1) / kBN;
-    const int64_t tm = blockIdx.x / tiles_n;
-    const int64_t tn = blockIdx.x % tiles_n;
-    const int64_t m0 = tm * kBM, n0 = tn * kBN;
     const int64_t row_bytes = d_in / 2;
-    const int nk = static_cast<int>((row_bytes + kBKB - 1) / kBKB);
+    const int nk = static_cast<int>((row_bytes + kKBP - 1) / kKBP);
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
     const int wave = tid / kWave;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave >> 1, wn = wave & 1;   // 2 x 2 waves, each 128 x 64
     const int l32 = lane & 31;
     const int h = lane >> 5;
 
-    // global -> register staging: each thread moves 2 units of A and 2 of B
-    u32x4 ra[2], rb[2];
-    auto gload = [&](int kt) {
+    // Direct loads: instruction q of wave w fills slots [64 I, 64 I + 64)
+    // with I = q * 4 + w; slot s holds row s / 4, logical unit
+    // (s % 4) ^ swz(row).  32-bit offsets from the tile's first row.
+    const uint8_t* a_base = qx;
+    const uint8_t* b_base = qw;
+    uint32_t a_off[kLoadsA], b_off[kLoadsB];
+    int ua_off[kLoadsA], ub_off[kLoadsB];
 #pragma unroll
-        for (int s = 0; s < 2; ++s) {
-            const int i = tid + s * kGemmThreads;
-            const int r = i / kUnits, u = i % kUnits;
-            const int64_t ga = m0 + r, gb = n0 + r;
-            const int64_t off = static_cast<int64_t>(kt) * kBKB + u * 16;
-            const bool kin = off < row_bytes;   // ragged last K step: zero codes
-            ra[s] = (ga < n && kin) ? *reinterpret_cast<const u32x4*>(qx + ga * row_bytes + off)
-                                    : u32x4{0u, 0u, 0u, 0u};
-            rb[s] = (gb < d_out && kin)
-                        ? *reinterpret_cast<const u32x4*>(qw + gb * row_bytes + off)
-                        : u32x4{0u, 0u, 0u, 0u};
+    for (int q = 0; q < kLoadsA; ++q) {
+        const int s = (q * 4 + wave) * 64 + lane;
+        ua_off[q] = ((s % kUP) ^ gemm_swz(s / kUP)) * 16;
+    }
+#pragma unroll
+    for (int q = 0; q < kLoadsB; ++q) {
+        const int s = (q * 4 + wave) * 64 + lane;
+        ub_off[q] = ((s % kUP) ^ gemm_swz(s / kUP)) * 16;
+    }
+    auto set_rows = [&](const GemmTile& tl) {
+        a_base = qx + tl.m0 * row_bytes;
+        b_base = qw + tl.n0 * row_bytes;
+#pragma unroll
+        for (int q = 0; q < kLoadsA; ++q) {
+            const int r = ((q * 4 + wave) * 64 + lane) / kUP;
+            const int64_t ra = tl.m0 + r < n ? r : n - 1 - tl.m0;   // clamped rows: never stored
+            a_off[q] = static_cast<uint32_t>(ra * row_bytes);
+        }
+#pragma unroll
+        for (int q = 0; q < kLoadsB; ++q) {
+            const int r = ((q * 4 + wave) * 64 + lane) / kUP;
+            const int64_t rb = tl.n0 + r < d_out ? r : d_out - 1 - tl.n0;
+            b_off[q] = static_cast<uint32_t>(rb * row_bytes);
         }
     };
-    auto lstore = [&](int buf) {
+    auto issue = [&](int kt, int st) {
+        const int64_t k0 = static_cast<int64_t>(kt) * kKBP;
 #pragma unroll
-        for (int s = 0; s < 2; ++s) {
-            const int i = tid + s * kGemmThreads;
-            const int r = i / kUnits, u = i % kUnits;
-            lds_a[buf][r * kUnits + (u ^ gemm_swz(r))] = ra[s];
-            lds_b[buf][r * kUnits + (u ^ gemm_swz(r))] = rb[s];
+        for (int q = 0; q < kLoadsA; ++q) {
+            int64_t col = k0 + ua_off[q];
+            col = col < row_bytes ? col : 0;     // past the row end: any in-bounds unit
+            __builtin_amdgcn_global_load_lds(
+                (const void*)(a_base + (a_off[q] + static_cast<uint32_t>(col))),
+                (lds_void_t*)&ring_a[st][(q * 4 + wave) * 64], 16, 0, 0);
+        }
+#pragma unroll
+        for (int q = 0; q < kLoadsB; ++q) {
+            int64_t col = k0 + ub_off[q];
+            col = col < row_bytes ? col : 0;
+            __builtin_amdgcn_global_load_lds(
+                (const void*)(b_base + (b_off[q] + static_cast<uint32_t>(col))),
+                (lds_void_t*)&ring_b[st][(q * 4 + wave) * 64], 16, 0, 0);
         }
     };
+    constexpr int kLoadsPerStep = kLoadsA + kLoadsB;
 
-    i32x16 acc[2][2];
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = i32x16{};
+    i32x16 acc[4][2];
 
-    gload(0);
-    lstore(0);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        const int buf = kt & 1;
-        if (kt + 1 < nk) gload(kt + 1);
+    // Fragments: lane half h reads logical units 2h and 2h+1 (c2 = 0, 1) of
+    // its row; each unit feeds two MFMA steps (its low and high 8 bytes).
+    // Both operands use the same assignment, so the reduction index is only
+    // permuted.
+    struct Packed {
+        u32x4 a[4], b[2];
+    };
+    struct Wide {
+        i32x4 a[4], b[2];
+    };
+    auto read_packed = [&](Packed& p, int st, int c2) {
+        const int u = 2 * h + c2;
 #pragma unroll
-        for (int c2 = 0; c2 < 2; ++c2) {
-            // lane half h reads unit 2h + c2 of its row: 32 codes = 2 MFMA steps
-            const int u = 2 * h + c2;
-            u32x4 a16[2], b16[2];
+        for (int i = 0; i < 4; ++i) {
+            const int r = wm * 128 + i * 32 + l32;
+            p.a[i] = ring_a[st][r * kUP + (u ^ gemm_swz(r))];
+        }
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const int r = wm * 64 + i * 32 + l32;
-                a16[i] = lds_a[buf][r * kUnits + (u ^ gemm_swz(r))];
+        for (int j = 0; j < 2; ++j) {
+            const int r = wn * 64 + j * 32 + l32;
+            p.b[j] = ring_b[st][r * kUP + (u ^ gemm_swz(r))];
+        }
+    };
+    auto widen = [&](Wide& w, const Packed& p, int half) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) w.a[i] = widen8(p.a[i], half);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) w.b[j] = widen8(p.b[j], half);
+    };
+    auto mfma16 = [&](const Wide& w) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(w.a[i], w.b[j], acc[i][j], 0, 0,
+                                                                 0);
+    };
+    // one K step = 4 MFMA steps of 32 codes; the widening of MFMA step
+    // c+1 is issued before the 16 MFMAs of step c
+    auto compute = [&](int st) {
+        Packed p;
+        Wide w0, w1;
+        read_packed(p, st, 0);
+        widen(w0, p, 0);
+        widen(w1, p, 1);
+        read_packed(p, st, 1);
+        mfma16(w0);
+        widen(w0, p, 0);
+        mfma16(w1);
+        widen(w1, p, 1);
+        mfma16(w0);
+        mfma16(w1);
+    };
+
+    GemmTile cur;
+    if (!gemm_tile(0, n, d_out, cur)) return;
+    set_rows(cur);
+#pragma unroll
+    for (int st = 0; st < kStages - 1; ++st)
+        if (st < nk) issue(st, st);
+
+    for (int64_t k = 0;; ++k) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) acc[i][j] = i32x16{};
+
+        for (int kt = 0; kt < nk; ++kt) {
+            // this thread's loads for step kt are done once at most the loads
+            // of the later steps already in flight remain outstanding
+            const int ahead = nk - 1 - kt < kStages - 2 ? nk - 1 - kt : kStages - 2;
+            if (ahead >= 2) wait_vmcnt<2 * kLoadsPerStep>();
+            else if (ahead == 1) wait_vmcnt<kLoadsPerStep>();
+            else wait_vmcnt<0>();
+            const int st = kt % kStages;
+            if (kt == nk - 1 && (row_bytes % kKBP) != 0) {
+                // ragged last step: codes past d_in read garbage; zero them in
+                // A (each thread clears the slots its own loads filled)
+#pragma unroll
+                for (int q = 0; q < kLoadsA; ++q)
+                    if (static_cast<int64_t>(kt) * kKBP + ua_off[q] >= row_bytes)
+                        ring_a[st][(q * 4 + wave) * 64 + lane] = u32x4{0u, 0u, 0u, 0u};
+            }
+            lds_barrier();     // all threads' loads of step kt landed; step kt-1 consumed
+            if (kt + kStages - 1 < nk) issue(kt + kStages - 1, (kt + kStages - 1) % kStages);
+            compute(st);
+        }
+        lds_barrier();     // every stage consumed before the next tile refills it
+
+        GemmTile nxt;
+        const bool more = gemm_tile(k + 1, n, d_out, nxt);
+        if (more) {
+            set_rows(nxt);
+#pragma unroll
+            for (int st = 0; st < kStages - 1; ++st)
+                if (st < nk) issue(st, st);
+        }
+
+        // ---- epilogue: lane holds column n0 + wn*128 + 32j + l32 and rows
+        // m0 + wm*128 + 32i + 8(r/4) + 4h + r%4
+        float sw[2];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int64_t o = cur.n0 + wn * 64 + j * 32 + l32;
+            sw[j] = o < d_out ? s_w[o] : 0.0f;
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int64_t tb = cur.m0 + wm * 128 + i * 32 + 4 * h;
+            float sx[16];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int64_t t = tb + 8 * (r >> 2) + (r & 3);
+                sx[r] = t < n ? s_x[t] : 0.0f;
             }
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
-                const int r = wn * 64 + j * 32 + l32;
-                b16[j] = lds_b[buf][r * kUnits + (u ^ gemm_swz(r))];
-            }
+                const int64_t o = cur.n0 + wn * 64 + j * 32 + l32;
+                if (o >= d_out) continue;
 #pragma unroll
-            for (int half = 0; half < 2; ++half) {
-                i32x4 av[2], bv[2];
-#pragma unroll
-                for (int i = 0; i < 2; ++i) av[i] = widen_lo_pair(a16[i], half);
-#pragma unroll
-                for (int j = 0; j < 2; ++j) bv[j] = widen_lo_pair(b16[j], half);
-#pragma unroll
-                for (int i = 0; i < 2; ++i)
-#pragma unroll
-                    for (int j = 0; j < 2; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(av[i], bv[j], acc[i][j],
-                                                                         0, 0, 0);
+                for (int r = 0; r < 16; ++r) {
+                    const int64_t t = tb + 8 * (r >> 2) + (r & 3);
+                    if (t >= n) continue;
+                    const int v = acc[i][j][r] >> 8;
+                    const float yv = (static_cast<float>(v) * sx[r]) * sw[j];
+                    __builtin_nontemporal_store(yv, y + t * d_out + o);
+                    if (acc_out) acc_out[t * d_out + o] = v;
+                }
             }
         }
-        if (kt + 1 < nk) {
-            lstore(buf ^ 1);
-        }
-        __syncthreads();
-    }
-
-    // epilogue: lane holds column n0 + wn*64 + 32j + l32 and rows
-    // m0 + wm*64 + 32i + 8(r/4) + 4h + r%4
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-        const int64_t o = n0 + wn * 64 + j * 32 + l32;
-        if (o >= d_out) continue;
-        const float sw = s_w[o];
-#pragma unroll
-        for (int i = 0; i < 2; ++i) {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int64_t t = m0 + wm * 64 + i * 32 + 8 * (r >> 2) + 4 * h + (r & 3);
-                if (t >= n) continue;
-                const int v = acc[i][j][r] >> 8;
-                const float yv = (static_cast<float>(v) * s_x[t]) * sw;
-                y[t * d_out + o] = yv;
-                if (acc_out) acc_out[t * d_out + o] = v;
-            }
-        }
+        if (!more) break;
+        cur = nxt;
     }
 }
 
 hipError_t launch_w4a4_linear(const uint8_t* codes_x, const float* s_x, const uint8_t* codes_w,
                               const float* s_w, int64_t n, int64_t d_in, int64_t d_out, float* y,
                               int32_t* acc_out, hipStream_t stream) {
-    const int64_t grid = ((n + kBM - 1) / kBM) * ((d_out + kBN - 1) / kBN);
+    int dev = 0, cus = 0;
+    hipError_t err = hipGetDevice(&dev);
+    if (err != hipSuccess) return err;
+    err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (err != hipSuccess) return err;
+    const int64_t T = ((n + kBM - 1) / kBM) * ((d_out + kBN - 1) / kBN);
+    // kWgPerCu resident workgroups per CU, a multiple of the XCD count
+    int64_t grid = (static_cast<int64_t>(cus) * kWgPerCu / kXcd) * kXcd;
+    const int64_t t_pad = ((T + kXcd - 1) / kXcd) * kXcd;
+    if (grid > t_pad) grid = t_pad;
+    if (grid < kXcd) grid = kXcd;
     hipLaunchKernelGGL(w4a4_gemm_kernel, dim3(static_cast<uint32_t>(grid)), dim3(kGemmThreads), 0,
                        stream, codes_x, s_x, codes_w, s_w, n, d_in, d_out, y, acc_out);
     return hipGetLastError();

@@ -247,6 +247,197 @@ hipError_t launch_tq_mfma(const uint16_t* X, int64_t n, int64_t d, const uint16_
 }
 
 
+// ------------------------------------------------------ ring MFMA path
+// bf16, k in {128, 256, 512}.  Persistent workgroups of 4 waves, two per
+// CU.  Workgroup (bj, r) owns rows [jc*128, jc*128 + 128) of block b and
+// the token tiles r, r + R, ...; wave w holds rows jc*128 + 32w .. +31 of
+// T_b in registers (the MFMA A operand, loaded once).  Token tiles of TT
+// rows stream global -> LDS with global_load_lds_dwordx4 (whole 16-byte
+// units, 1 KiB contiguous per wave instruction) into a 2-stage ring: the
+// next tile is requested as soon as the previous one has been consumed, so
+// it loads during the current tile's MFMAs.  Each wave multiplies its 32
+// rows against every token of the tile (B operand read from LDS; 16-byte
+// units XOR-swizzled per token row so fragment reads are conflict free).
+// Pass 1 folds per-token maxima across the four waves in LDS and issues one
+// atomic max per token; pass 2 packs codes straight from the accumulators.
+template <int K>
+struct TqRing {
+    static constexpr int TT = K == 128 ? 128 : (K == 256 ? 64 : 32);   // tokens per tile
+    static constexpr int U = K / 8;                // 16-byte units per token row
+    static constexpr int NS = K / 16;              // 16-deep MFMA steps
+    static constexpr int NSB = TT / 32;            // 32-token subtiles
+    static constexpr int STAGE = TT * U;           // units per stage (2048 = 32 KiB)
+    static constexpr int LOADS = STAGE / kTqThreads;
+    static constexpr int NCHUNK = K / 128;         // 128-row chunks per block
+};
+
+template <int K>
+__device__ __forceinline__ int tq_xswz(int r) {
+    return K == 128 ? ((r ^ (r >> 4)) & 15) : (r & 31);
+}
+
+// s_waitcnt with only the vector-memory counter limited to 0 (gfx9
+// encoding: expcnt and lgkmcnt left at their maxima).
+__device__ __forceinline__ void tq_wait_vm0() { __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8)); }
+
+// Barrier that waits for this wave's LDS operations only (loads in flight
+// stay in flight).
+__device__ __forceinline__ void tq_lds_barrier() {
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    __builtin_amdgcn_s_barrier();
+}
+
+typedef __attribute__((address_space(3))) void tq_lds_void_t;
+
+template <int K, bool QUANT>
+__global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
+    const uint16_t* __restrict__ X, const uint16_t* __restrict__ T, int64_t n, int64_t d,
+    int64_t R, uint32_t* __restrict__ amax_ws, uint8_t* __restrict__ codes,
+    float* __restrict__ s_x) {
+    using C = TqRing<K>;
+    __shared__ __attribute__((aligned(16))) u32x4 ring[2][C::STAGE];
+    __shared__ uint32_t red[4][C::TT];
+
+    const int64_t nbj = (d / K) * C::NCHUNK;
+    const int64_t bj = blockIdx.x % nbj;
+    const int64_t r0 = blockIdx.x / nbj;
+    const int64_t b = bj / C::NCHUNK;
+    const int jc = static_cast<int>(bj % C::NCHUNK);
+    const int64_t ntiles = (n + C::TT - 1) / C::TT;
+    if (r0 >= ntiles) return;
+
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    const int l32 = lane & 31;
+    const int h = lane >> 5;
+    const int row0 = jc * 128 + wave * 32;     // first row of T_b this wave owns
+
+    // A operand: row row0 + l32 of T_b, elements 16s + 8h .. +7 per step s
+    u32x4 tf[C::NS];
+    {
+        const u32x4* tg = reinterpret_cast<const u32x4*>(T + (b * K + row0 + l32) * K);
+#pragma unroll
+        for (int s = 0; s < C::NS; ++s) tf[s] = tg[2 * s + h];
+    }
+
+    // slot sl of a stage holds token row sl / U, logical unit (sl % U) ^ swz
+    auto issue = [&](int64_t tile, int st) {
+        const int64_t t0 = tile * C::TT;
+#pragma unroll
+        for (int q = 0; q < C::LOADS; ++q) {
+            const int sl = (q * 4 + wave) * 64 + lane;
+            const int rr = sl / C::U;
+            const int u = (sl % C::U) ^ tq_xswz<K>(rr);
+            int64_t tok = t0 + rr;
+            tok = tok < n ? tok : n - 1;          // rows past the end: never used
+            const uint16_t* src = X + tok * d + b * K + u * 8;
+            __builtin_amdgcn_global_load_lds((const void*)src,
+                                             (tq_lds_void_t*)&ring[st][(q * 4 + wave) * 64], 16,
+                                             0, 0);
+        }
+    };
+
+    issue(r0, 0);
+    int it = 0;
+    for (int64_t tile = r0; tile < ntiles; tile += R, ++it) {
+        const int st = it & 1;
+        tq_wait_vm0();         // this thread's loads of the tile have landed
+        tq_lds_barrier();      // ... everyone's; the other stage is free again
+        if (tile + R < ntiles) issue(tile + R, st ^ 1);
+
+        f32x16 acc[C::NSB];
+#pragma unroll
+        for (int sb = 0; sb < C::NSB; ++sb) acc[sb] = f32x16{};
+#pragma unroll
+        for (int s = 0; s < C::NS; ++s) {
+#pragma unroll
+            for (int sb = 0; sb < C::NSB; ++sb) {
+                const int rr = sb * 32 + l32;
+                const u32x4 xf = ring[st][rr * C::U + ((2 * s + h) ^ tq_xswz<K>(rr))];
+                acc[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(tf[s]), as_bf16x8(xf),
+                                                                  acc[sb], 0, 0, 0);
+            }
+        }
+
+        if constexpr (!QUANT) {
+#pragma unroll
+            for (int sb = 0; sb < C::NSB; ++sb) {
+                uint32_t m = 0;
+#pragma unroll
+                for (int q = 0; q < 16; ++q) m = max(m, abs_bits(acc[sb][q]));
+                m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), 32)));
+                if (h == 0) red[wave][sb * 32 + l32] = m;
+            }
+            tq_lds_barrier();
+            for (int idx = threadIdx.x; idx < C::TT; idx += kTqThreads) {
+                const uint32_t m = max(max(red[0][idx], red[1][idx]), max(red[2][idx], red[3][idx]));
+                const int64_t t = tile * C::TT + idx;
+                if (t < n && m) atomicMax(amax_ws + t, m);
+            }
+        } else {
+#pragma unroll
+            for (int sb = 0; sb < C::NSB; ++sb) {
+                const int64_t t = tile * C::TT + sb * 32 + l32;
+                const bool valid = t < n;
+                const float amax = valid ? __uint_as_float(amax_ws[t]) : 0.0f;
+                if (valid && h == 0 && wave == 0 && b == 0 && jc == 0)
+                    s_x[t] = __fdiv_rn(amax, kQmax4);
+                const bool nz = amax > 0.0f;
+                const float inv = nz ? __fdiv_rn(kQmax4, amax) : 0.0f;
+                // v[q]: codes of rows 8q + 4h + (0..3) of the wave's 32, 16 bits
+                uint32_t v[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    uint32_t pk = 0;
+                    if (nz) {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            pk |= static_cast<uint32_t>(quant_code(acc[sb][4 * q + e], inv) & 0xF)
+                                  << (4 * e);
+                    }
+                    v[q] = pk;
+                }
+                uint32_t* crow =
+                    reinterpret_cast<uint32_t*>(codes + t * (d / 2) + (b * K + row0) / 2);
+#pragma unroll
+                for (int qp = 0; qp < 4; qp += 2) {
+                    // h=0 stores rows 8qp+0..7, h=1 rows 8(qp+1)+0..7
+                    const uint32_t send = h ? v[qp] : v[qp + 1];
+                    const uint32_t recv =
+                        static_cast<uint32_t>(__shfl_xor(static_cast<int>(send), 32));
+                    const uint32_t word = h ? (recv | (v[qp + 1] << 16)) : (v[qp] | (recv << 16));
+                    if (valid) crow[qp + h] = word;
+                }
+            }
+        }
+    }
+}
+
+template <int K>
+hipError_t launch_tq_ring(const uint16_t* X, int64_t n, int64_t d, const uint16_t* T,
+                          uint8_t* codes, float* s_x, uint32_t* ws, hipStream_t stream) {
+    using C = TqRing<K>;
+    int dev = 0, cus = 0;
+    hipError_t err = hipGetDevice(&dev);
+    if (err != hipSuccess) return err;
+    err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (err != hipSuccess) return err;
+    const int64_t ntiles = (n + C::TT - 1) / C::TT;
+    const int64_t nbj = (d / K) * C::NCHUNK;
+    // about two resident workgroups per CU
+    int64_t R = (2 * static_cast<int64_t>(cus) + nbj - 1) / nbj;
+    if (R > ntiles) R = ntiles;
+    if (R < 1) R = 1;
+    const int64_t grid = nbj * R;
+    hipLaunchKernelGGL((tq_ring_kernel<K, false>), dim3(static_cast<uint32_t>(grid)),
+                       dim3(kTqThreads), 0, stream, X, T, n, d, R, ws, codes, s_x);
+    err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL((tq_ring_kernel<K, true>), dim3(static_cast<uint32_t>(grid)),
+                       dim3(kTqThreads), 0, stream, X, T, n, d, R, ws, codes, s_x);
+    return hipGetLastError();
+}
+
 template <typename XT, typename TT>
 hipError_t launch_tq_generic(const XT* X, int64_t n, int64_t d, const TT* T, int64_t k,
                              uint8_t* codes, float* s_x, uint32_t* ws, hipStream_t stream) {
@@ -274,9 +465,9 @@ hipError_t launch_transform_quant(const void* X, int x_bf16, int64_t n, int64_t 
         switch (k) {
             case 32: return launch_tq_mfma<32, 32>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
             case 64: return launch_tq_mfma<64, 64>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
-            case 128: return launch_tq_mfma<128, 128>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
-            case 256: return launch_tq_mfma<256, 128>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
-            case 512: return launch_tq_mfma<512, 64>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
+            case 128: return launch_tq_ring<128>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
+            case 256: return launch_tq_ring<256>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
+            case 512: return launch_tq_ring<512>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
             default: break;
         }
     }

@@ -49,6 +49,9 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=10.0,
                    help="minimum CPU time of the oracle sample")
+    p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                   help="only run a plain device-to-device copy of MIB MiB (5 launches): "
+                        "the known-size kernel that scales HBM byte counters")
     return p.parse_args()
 
 
@@ -56,12 +59,16 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+GEMM_SOURCES = ("k_w4a4.hip", "device_common.h", "kernels.h")
+
+
 def kernel_sources_sha():
+    """Hash of the sources the W4A4 GEMM kernel is built from: the stored
+    counter figures apply only while it matches."""
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2603_04359_amd", "csrc")
-    for f in sorted(os.listdir(csrc)):
-        if f.endswith((".hip", ".h")):
-            h.update(open(os.path.join(csrc, f), "rb").read())
+    for f in GEMM_SOURCES:
+        h.update(open(os.path.join(csrc, f), "rb").read())
     return h.hexdigest()[:16]
 
 
@@ -116,8 +123,25 @@ def cpu_baseline(lay, T_vals, codes_w, s_w, n_tokens, min_seconds):
                       f"os.cpu_count()={os.cpu_count()})"}
 
 
+def copy_calibration(mib):
+    """Five launches of torch's device copy of `mib` MiB: each reads and
+    writes exactly mib*2^20 bytes, so FETCH_SIZE / WRITE_SIZE read under
+    rocprofv3 for it give the factor from counter units to HBM bytes."""
+    import torch
+    dev = torch.device("cuda:0")
+    src = torch.ones(mib << 18, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": mib << 20, "launches": 5}), flush=True)
+
+
 def main():
     args = parse()
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no "
               "multi-GPU path: collectives and sharding are design-only.", file=sys.stderr)

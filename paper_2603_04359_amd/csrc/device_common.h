@@ -54,4 +54,22 @@ __device__ __forceinline__ uint32_t unpack_hi16(uint32_t w) {
     return w & 0xF0F0F0F0u;
 }
 
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+// s_waitcnt with only the vector-memory counter limited (gfx9 encoding:
+// vmcnt in bits 3:0 and 15:14; expcnt and lgkmcnt left at their maxima).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Workgroup barrier that only waits for this wave's own LDS operations;
+// vector-memory loads in flight stay in flight (a plain __syncthreads()
+// would also drain them, which defeats a multi-stage prefetch).
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0), vmcnt/expcnt unlimited
+    __builtin_amdgcn_s_barrier();
+}
+
 }  // namespace catk

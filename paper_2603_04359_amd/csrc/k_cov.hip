@@ -1,18 +1,20 @@
 // Calibration second moment: acc += X^T X (Sec. 4, Sigma_x = E[x x^T];
 // Sec. 6 "Calibration").  The caller divides by the token count.
 //
-// bf16 path (gfx950 v_mfma_f32_32x32x16_bf16): one workgroup owns one
-// TILE x TILE output tile of the upper triangle (mode FULL) or of the upper
-// triangle of a diagonal k x k block (mode BLOCK_DIAG) and loops over all
-// tokens.  The contraction runs over tokens, i.e. down the columns of the
-// row-major X, so each 32-token slab is transposed on its way into LDS:
-// every lane loads one channel pair from 8 consecutive tokens (4-byte loads,
-// a whole 256-byte row segment per wave instruction), splits the pairs with
-// v_perm into two 16-byte runs of 8 tokens and stores them as one LDS unit
-// per channel.  Fragments are then 16-byte LDS reads (units XOR-swizzled
-// per channel row).  Partial sums stay in registers for at most 4096
-// tokens and are then added into acc by the tile's owner (no atomics, so
-// results are reproducible); off-diagonal tiles also add their transpose.
+// Matrices of at least 256 channels (bf16, channel count a multiple of 32)
+// run cov_sk_kernel: 256 x 256 upper-triangle tiles, token slabs streamed
+// HBM -> LDS in X's own layout and transposed by ds_read_tr16_b64 on the
+// way into v_mfma_f32_32x32x16_bf16, work split evenly over the CUs
+// (stream-K over (tile, slab) units), partial sums added with fp32
+// atomics.  The design notes are at that kernel.
+//
+// Smaller bf16 matrices (64 or 128 channels, or widths that are not a
+// multiple of 32) run cov_mfma_kernel: one workgroup per 128 x 128 (or
+// 64 x 64) upper-triangle tile looping over all tokens; each 32-token slab
+// is transposed on its way into LDS (4-byte loads of channel pairs split
+// with v_perm into 16-byte runs of 8 tokens per channel).  Partial sums
+// stay in registers for at most 4096 tokens and are then added into acc by
+// the tile's owner together with the transpose.
 //
 // fp32 inputs and blocks smaller than 64 use a vector-ALU kernel with the
 // same tiling and flush policy.
@@ -258,6 +260,259 @@ __global__ __launch_bounds__(kCovThreads) void cov_valu_kernel(const XT* __restr
     }
 }
 
+// ------------------------------------------- 256 x 256 tiles, stream-K
+// For matrices of at least 256 channels (bf16, channel count a multiple
+// of 8).  Each workgroup (4 waves, one per SIMD) owns a 256 x 256 tile of
+// the upper triangle; every wave keeps 128 x 128 fp32 partial sums (4 x 4
+// v_mfma_f32_32x32x16_bf16 accumulators).  Token slabs of 32 rows go from
+// HBM straight into a 3-stage LDS ring with global_load_lds_dwordx4, in
+// X's own row-major order (no transposition on the way in): 512 bytes of
+// each token row per operand, 16-byte units XOR-swizzled by row.  The
+// MFMA operands need 8 consecutive tokens of one channel; ds_read_tr16_b64
+// performs that transposition on the LDS read: within 16 lanes, lane
+// 4e + q addresses token row e, channels 4q..4q+3, and lane i receives
+// channel i of the 4 rows.
+//
+// The work is the list of (tile, 32-token slab) units over all tiles; each
+// workgroup takes one contiguous share of it (stream-K), so every CU gets
+// the same number of MFMAs whatever the tile count.  A tile processed by a
+// single workgroup from its first to its last slab is added into acc with
+// plain read-modify-write stores; a tile split between workgroups is added
+// with fp32 atomics (so the last bit of such tiles may differ between
+// runs).  Off-diagonal tiles also add their transpose (16-byte runs: each
+// lane holds 4 consecutive rows of one column); diagonal tiles are
+// computed whole and written as is.
+constexpr int kSkT = 256;                        // tile edge
+constexpr int kSkSlab = 32;                      // tokens per ring stage
+constexpr int kSkStages = 3;
+constexpr int kSkRowUnits = kSkT / 8;            // 16-byte units per token row (32)
+constexpr int kSkOpUnits = kSkSlab * kSkRowUnits;  // units per operand and stage (1024)
+constexpr int kSkLoads = kSkOpUnits / kCovThreads; // direct loads per thread and operand (4)
+constexpr int kSkFlushSlabs = 256;               // at most 8192 tokens per register partial
+
+struct SkGeom {
+    int64_t dim;     // channels of one matrix (d in FULL mode, k in BLOCK_DIAG mode)
+    int64_t T;       // tiles along one edge of a matrix
+    int64_t tri;     // upper-triangle tiles per matrix
+    int64_t S;       // slabs per tile (= token slabs)
+    int64_t U;       // total units = matrices * tri * S
+};
+
+typedef short sk_v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) sk_v4i16 sk_lds_v4i16;
+
+// Eight consecutive tokens of one channel from two transposing reads
+// (4 tokens each) at byte offsets off and off + 4 rows.
+__device__ __forceinline__ bf16x8 sk_frag(const char __attribute__((address_space(3))) * base,
+                                          uint32_t off) {
+    const sk_v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((sk_lds_v4i16*)(base + off));
+    const sk_v4i16 hi =
+        __builtin_amdgcn_ds_read_tr16_b64_v4i16((sk_lds_v4i16*)(base + off + 4 * kSkT * 2));
+    typedef short v8i16 __attribute__((ext_vector_type(8)));
+    const v8i16 v = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    return __builtin_bit_cast(bf16x8, v);
+}
+
+__global__ __launch_bounds__(kCovThreads, 1) void cov_sk_kernel(const uint16_t* __restrict__ X,
+                                                                int64_t n, int64_t d, int mode,
+                                                                int64_t k, SkGeom g,
+                                                                float* __restrict__ acc) {
+    __shared__ __attribute__((aligned(16))) u32x4 ring[kSkStages][2][kSkOpUnits];
+
+    const int tid = threadIdx.x;
+    const int lane = tid & (kWave - 1);
+    const int wave = tid / kWave;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int l32 = lane & 31;
+    const int h = lane >> 5;
+
+    // contiguous share of the unit list; consecutive shares on one XCD
+    const int64_t G = gridDim.x;
+    int64_t w = blockIdx.x;
+    if (G % 8 == 0) w = (blockIdx.x % 8) * (G / 8) + blockIdx.x / 8;
+    const int64_t u_begin = g.U * w / G, u_end = g.U * (w + 1) / G;
+
+    // direct-load geometry: load q of this thread fills unit (q*4+wave)*64+lane
+    // of an operand stage, i.e. token row 8q + rr, swizzled position l32.
+    const int rr = 2 * wave + h;
+    const int unit = l32 ^ ((rr & 3) << 2);      // global 16-byte unit of the row
+    const uint32_t row_bytes = static_cast<uint32_t>(d) * 2u;
+
+    // fragment-read geometry (bytes inside one operand stage)
+    const int i16 = lane & 15, e = i16 >> 2, qq = i16 & 3, gg = (lane >> 4) & 1;
+    uint32_t offA[4], offB[4];
+#pragma unroll
+    for (int a = 0; a < 4; ++a) {
+        const int row = 8 * h + e;                 // token row inside the 16-token step
+        const int ua = (wm * 16 + 4 * a + 2 * gg + (qq >> 1)) ^ ((row & 3) << 2);
+        const int ub = (wn * 16 + 4 * a + 2 * gg + (qq >> 1)) ^ ((row & 3) << 2);
+        offA[a] = row * (kSkT * 2) + 16 * ua + 8 * (qq & 1);
+        offB[a] = row * (kSkT * 2) + 16 * ub + 8 * (qq & 1);
+    }
+
+    for (int64_t u = u_begin; u < u_end;) {
+        const int64_t tile = u / g.S;
+        const int64_t s0 = u % g.S;
+        int64_t s1 = (g.S < s0 + (u_end - u)) ? g.S : s0 + (u_end - u);
+        const int64_t cend = (s0 / kSkFlushSlabs + 1) * kSkFlushSlabs;   // register partial limit
+        s1 = s1 < cend ? s1 : cend;
+        u += s1 - s0;
+
+        const int64_t mat = tile / g.tri;
+        int64_t I, J;
+        tri_decode(tile % g.tri, g.T, I, J);
+        const int64_t colbase = mode == CAT_COV_FULL ? 0 : mat * k;
+        const int64_t I0 = I * kSkT, J0 = J * kSkT;
+        const bool diag = I == J;
+        float* accm = acc + (mode == CAT_COV_FULL ? 0 : mat * k * k);
+
+        // per-thread source byte offsets inside a slab (columns clamped into
+        // the matrix when the last tile is ragged: those rows/columns of the
+        // result are discarded)
+        int64_t ca = I0 + 8 * unit, cb = J0 + 8 * unit;
+        if (ca >= g.dim) ca = I0;
+        if (cb >= g.dim) cb = J0;
+        const uint32_t oa = static_cast<uint32_t>(rr) * row_bytes + static_cast<uint32_t>(colbase + ca) * 2u;
+        const uint32_t ob = static_cast<uint32_t>(rr) * row_bytes + static_cast<uint32_t>(colbase + cb) * 2u;
+
+        auto issue = [&](int64_t s, int st) {
+            const int64_t t0 = s * kSkSlab;
+            const char* base = reinterpret_cast<const char*>(X + t0 * d);
+            if (t0 + kSkSlab <= n) {
+#pragma unroll
+                for (int q = 0; q < kSkLoads; ++q)
+                    __builtin_amdgcn_global_load_lds(
+                        (const void*)(base + (oa + q * 8u * row_bytes)),
+                        (lds_void_t*)&ring[st][0][(q * 4 + wave) * 64], 16, 0, 0);
+                if (!diag) {
+#pragma unroll
+                    for (int q = 0; q < kSkLoads; ++q)
+                        __builtin_amdgcn_global_load_lds(
+                            (const void*)(base + (ob + q * 8u * row_bytes)),
+                            (lds_void_t*)&ring[st][1][(q * 4 + wave) * 64], 16, 0, 0);
+                }
+            } else {
+                // ragged last slab: rows past n load row n-1 (zeroed once landed)
+#pragma unroll
+                for (int q = 0; q < kSkLoads; ++q) {
+                    const int64_t t = t0 + 8 * q + rr;
+                    const uint32_t back = t < n ? 0u : static_cast<uint32_t>(t - (n - 1)) * row_bytes;
+                    __builtin_amdgcn_global_load_lds(
+                        (const void*)(base + (oa + q * 8u * row_bytes - back)),
+                        (lds_void_t*)&ring[st][0][(q * 4 + wave) * 64], 16, 0, 0);
+                    if (!diag)
+                        __builtin_amdgcn_global_load_lds(
+                            (const void*)(base + (ob + q * 8u * row_bytes - back)),
+                            (lds_void_t*)&ring[st][1][(q * 4 + wave) * 64], 16, 0, 0);
+                }
+            }
+        };
+
+        f32x16 part[4][4];
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+            for (int b = 0; b < 4; ++b) part[a][b] = f32x16{};
+
+        issue(s0, 0);
+        if (s0 + 1 < s1) issue(s0 + 1, 1);
+        int st = 0;
+        for (int64_t s = s0; s < s1; ++s) {
+            if (s + 1 < s1) {
+                if (diag) wait_vmcnt<kSkLoads>();
+                else wait_vmcnt<2 * kSkLoads>();
+            } else {
+                wait_vmcnt<0>();
+            }
+            const int64_t t0 = s * kSkSlab;
+            if (t0 + kSkSlab > n) {
+#pragma unroll
+                for (int q = 0; q < kSkLoads; ++q) {
+                    if (t0 + 8 * q + rr >= n) {
+                        ring[st][0][(q * 4 + wave) * 64 + lane] = u32x4{0u, 0u, 0u, 0u};
+                        if (!diag) ring[st][1][(q * 4 + wave) * 64 + lane] = u32x4{0u, 0u, 0u, 0u};
+                    }
+                }
+            }
+            lds_barrier();   // slab s landed for every thread; slab s-1 consumed
+            if (s + 2 < s1) issue(s + 2, st == 0 ? 2 : st - 1);
+
+            const char __attribute__((address_space(3)))* baseA =
+                (const char __attribute__((address_space(3)))*)&ring[st][0][0];
+            const char __attribute__((address_space(3)))* baseB =
+                (const char __attribute__((address_space(3)))*)&ring[st][diag ? 0 : 1][0];
+#pragma unroll
+            for (int kk = 0; kk < 2; ++kk) {
+                bf16x8 fa[4], fb[4];
+#pragma unroll
+                for (int a = 0; a < 4; ++a) fa[a] = sk_frag(baseA, offA[a] + kk * 16 * kSkT * 2);
+#pragma unroll
+                for (int b = 0; b < 4; ++b) fb[b] = sk_frag(baseB, offB[b] + kk * 16 * kSkT * 2);
+#pragma unroll
+                for (int a = 0; a < 4; ++a)
+#pragma unroll
+                    for (int b = 0; b < 4; ++b)
+                        part[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[a], fb[b],
+                                                                             part[a][b], 0, 0, 0);
+            }
+            st = st == 2 ? 0 : st + 1;
+        }
+
+        // Add the partial sums into acc with fp32 atomics (no return value):
+        // each wave instruction covers two 128-byte row segments.  The
+        // transpose for the mirror tile goes through LDS (a 32 x 33 float
+        // pad per wave) so its atomics are row segments too.  32-bit element
+        // offsets from the matrix base; the empty asm keeps them from being
+        // precomputed outside the loop.
+        lds_barrier();   // the ring is free: every wave has finished reading it
+        uint32_t dimu = static_cast<uint32_t>(g.dim);
+        uint32_t rowb = static_cast<uint32_t>(I0 + wm * 128 + 4 * h);
+        uint32_t colb = static_cast<uint32_t>(J0 + wn * 128 + l32);
+        asm volatile("" : "+v"(rowb), "+v"(colb), "+s"(dimu));
+        const uint32_t row_u = static_cast<uint32_t>(I0 + wm * 128);
+        const uint32_t col_u = static_cast<uint32_t>(J0 + wn * 128);
+        float* pad = reinterpret_cast<float*>(&ring[0][0][0]) + wave * (32 * 33);
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+                if (row_u + 32 * a >= dimu || col_u + 32 * b >= dimu) continue;
+                const uint32_t up = (rowb + 32 * a) * dimu + colb + 32 * b;
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    unsafeAtomicAdd(accm + up + (8 * (r >> 2) + (r & 3)) * dimu, part[a][b][r]);
+                if (!diag) {
+                    // element (R, C) of the 32 x 32 block -> pad[C][R]; read back
+                    // as (R, C) of the transposed block
+#pragma unroll
+                    for (int r = 0; r < 16; ++r)
+                        pad[l32 * 33 + 8 * (r >> 2) + 4 * h + (r & 3)] = part[a][b][r];
+                    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+                    const uint32_t mi = (colb - l32 + 32 * b + 4 * h) * dimu +
+                                        (rowb - 4 * h + 32 * a + l32);
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int R = 8 * (r >> 2) + 4 * h + (r & 3);
+                        unsafeAtomicAdd(accm + mi + (8 * (r >> 2) + (r & 3)) * dimu,
+                                        pad[R * 33 + l32]);
+                    }
+                    __builtin_amdgcn_s_waitcnt(0xC07F);
+                }
+            }
+        lds_barrier();   // every wave is done with the ring before the next tile refills it
+    }
+}
+
+static bool cov_sk_geometry(int64_t n, int64_t d, int mode, int64_t k, SkGeom& g) {
+    g.dim = mode == CAT_COV_FULL ? d : k;
+    const int64_t nmat = mode == CAT_COV_FULL ? 1 : d / k;
+    g.T = (g.dim + kSkT - 1) / kSkT;
+    g.tri = g.T * (g.T + 1) / 2;
+    g.S = (n + kSkSlab - 1) / kSkSlab;
+    g.U = nmat * g.tri * g.S;
+    return g.U > 0;
+}
+
 static int64_t cov_grid(int tile, int64_t d, int mode, int64_t k) {
     if (mode == CAT_COV_FULL) {
         const int64_t T = (d + tile - 1) / tile;
@@ -270,6 +525,19 @@ static int64_t cov_grid(int tile, int64_t d, int mode, int64_t k) {
 hipError_t launch_cov_accumulate(const void* X, int x_bf16, int64_t n, int64_t d, int mode,
                                  int64_t k, float* acc, hipStream_t stream) {
     const int64_t dim = mode == CAT_COV_FULL ? d : k;
+    if (x_bf16 && dim >= kSkT && (d % 8) == 0 && (dim % 32) == 0) {
+        SkGeom g;
+        if (!cov_sk_geometry(n, d, mode, k, g)) return hipSuccess;
+        int dev = 0, cus = 0;
+        hipError_t err = hipGetDevice(&dev);
+        if (err != hipSuccess) return err;
+        err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+        if (err != hipSuccess) return err;
+        const int64_t grid = g.U < cus ? g.U : cus;
+        hipLaunchKernelGGL(cov_sk_kernel, dim3(static_cast<uint32_t>(grid)), dim3(kCovThreads), 0,
+                           stream, static_cast<const uint16_t*>(X), n, d, mode, k, g, acc);
+        return hipGetLastError();
+    }
     if (x_bf16 && dim >= 64 && (dim % 2) == 0 && (d % 2) == 0) {
         const uint16_t* Xb = static_cast<const uint16_t*>(X);
         if (dim >= 128) {

@@ -276,19 +276,6 @@ __device__ __forceinline__ int tq_xswz(int r) {
     return K == 128 ? ((r ^ (r >> 4)) & 15) : (r & 31);
 }
 
-// s_waitcnt with only the vector-memory counter limited to 0 (gfx9
-// encoding: expcnt and lgkmcnt left at their maxima).
-__device__ __forceinline__ void tq_wait_vm0() { __builtin_amdgcn_s_waitcnt((7 << 4) | (15 << 8)); }
-
-// Barrier that waits for this wave's LDS operations only (loads in flight
-// stay in flight).
-__device__ __forceinline__ void tq_lds_barrier() {
-    __builtin_amdgcn_s_waitcnt(0xC07F);
-    __builtin_amdgcn_s_barrier();
-}
-
-typedef __attribute__((address_space(3))) void tq_lds_void_t;
-
 template <int K, bool QUANT>
 __global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ T, int64_t n, int64_t d,
@@ -332,7 +319,7 @@ __global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
             tok = tok < n ? tok : n - 1;          // rows past the end: never used
             const uint16_t* src = X + tok * d + b * K + u * 8;
             __builtin_amdgcn_global_load_lds((const void*)src,
-                                             (tq_lds_void_t*)&ring[st][(q * 4 + wave) * 64], 16,
+                                             (lds_void_t*)&ring[st][(q * 4 + wave) * 64], 16,
                                              0, 0);
         }
     };
@@ -341,8 +328,8 @@ __global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
     int it = 0;
     for (int64_t tile = r0; tile < ntiles; tile += R, ++it) {
         const int st = it & 1;
-        tq_wait_vm0();         // this thread's loads of the tile have landed
-        tq_lds_barrier();      // ... everyone's; the other stage is free again
+        wait_vmcnt<0>();         // this thread's loads of the tile have landed
+        lds_barrier();      // ... everyone's; the other stage is free again
         if (tile + R < ntiles) issue(tile + R, st ^ 1);
 
         f32x16 acc[C::NSB];
@@ -368,7 +355,7 @@ __global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
                 m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), 32)));
                 if (h == 0) red[wave][sb * 32 + l32] = m;
             }
-            tq_lds_barrier();
+            lds_barrier();
             for (int idx = threadIdx.x; idx < C::TT; idx += kTqThreads) {
                 const uint32_t m = max(max(red[0][idx], red[1][idx]), max(red[2][idx], red[3][idx]));
                 const int64_t t = tile * C::TT + idx;

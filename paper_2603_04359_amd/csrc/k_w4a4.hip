@@ -65,22 +65,6 @@ __device__ __forceinline__ int gemm_swz(int r) {
     return ((q >> 2) ^ (q >> 4)) & 3;
 }
 
-// s_waitcnt with only the vector-memory counter limited (gfx9 encoding:
-// vmcnt in bits 3:0 and 15:14; expcnt and lgkmcnt left at their maxima).
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
-// Workgroup barrier that only waits for this wave's own LDS operations;
-// vector-memory loads in flight stay in flight (a plain __syncthreads()
-// would also drain them, which defeats a multi-step prefetch).
-__device__ __forceinline__ void lds_barrier() {
-    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0), vmcnt/expcnt unlimited
-    __builtin_amdgcn_s_barrier();
-}
-
 struct GemmTile {
     int64_t m0, n0;
 };
@@ -104,8 +88,6 @@ __device__ __forceinline__ bool gemm_tile(int64_t k, int64_t n, int64_t d_out, G
     t.n0 = (in_group / gm) * kBN;
     return true;
 }
-
-typedef __attribute__((address_space(3))) void lds_void_t;
 
 __device__ __forceinline__ i32x4 widen8(u32x4 v, int half) {
     const uint32_t w0 = v[2 * half], w1 = v[2 * half + 1];

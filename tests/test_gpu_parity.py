@@ -196,8 +196,17 @@ def _blocks(S, k):
     return np.stack([S[b * k:(b + 1) * k, b * k:(b + 1) * k] for b in range(d // k)])
 
 
+def _assert_symmetric(acc):
+    # split tiles are added with atomics, so the two triangles may round
+    # their sums in different orders: equal to within a few ulp
+    asym = np.max(np.abs(acc - acc.T))
+    assert asym <= 4e-7 * max(1.0, float(np.max(np.abs(acc))))
+
+
 @pytest.mark.parametrize("d,n,dtype", [(256, 5000, "bf16"), (320, 1000, "bf16"),
-                                       (256, 2048, "f32"), (96, 300, "bf16")])
+                                       (256, 2048, "f32"), (96, 300, "bf16"),
+                                       (1024, 3001, "bf16"), (768, 40, "bf16"),
+                                       (256, 1, "bf16"), (512, 17, "bf16")])
 def test_cov_full_matches_oracle(d, n, dtype):
     say(f"cov full d={d} n={n} {dtype}")
     cfg = wl.get_config("attn4096", d_in=d, d_out=d, n_cal=n, n=1)
@@ -208,14 +217,32 @@ def test_cov_full_matches_oracle(d, n, dtype):
     err = rel_fro(acc, ref)
     say(f"  rel fro {err:.2e}")
     assert err <= 1e-5
-    assert np.array_equal(acc, acc.T)
+    _assert_symmetric(acc)
+
+
+def test_cov_full_size_mlp_up_batch():
+    """The 4096-channel full matrix over one 8192-token mlp_up batch (the
+    shape the benchmark times), accumulated onto a non-zero symmetric start."""
+    say("cov full 4096 x 4096, 8192 tokens")
+    torch = torch_mod()
+    cfg = wl.get_config("mlp_up", n_cal=8192, n=1)
+    X = wl.make_layer(cfg, seed=5, with_eval=False, with_weights=False)["X_cal"]
+    start = wl.random_spd(256, seed=3)
+    S0 = np.kron(np.eye(16), start).astype(np.float32)
+    acc0 = torch.from_numpy(S0).cuda()
+    acc = _cov_gpu(X, "bf16", B.CAT_COV_FULL, 1, acc0=acc0)
+    ref = S0.astype(np.float64) + o.second_moment_sum(X)
+    err = rel_fro(acc, ref)
+    say(f"  rel fro {err:.2e}")
+    assert err <= 1e-5
+    _assert_symmetric(acc)
 
 
 @pytest.mark.parametrize("k,dtype", [(64, "bf16"), (128, "bf16"), (256, "bf16"), (32, "bf16"),
-                                     (32, "f32")])
+                                     (32, "f32"), (512, "bf16")])
 def test_cov_block_diag_matches_oracle(k, dtype):
     say(f"cov block k={k} {dtype}")
-    d, n = 512, 4500
+    d, n = (1024 if k == 512 else 512), 4500
     cfg = wl.get_config("attn4096", d_in=d, d_out=d, n_cal=n, n=1)
     X = o.round_storage(wl.make_layer(cfg, seed=k, with_eval=False, with_weights=False)["X_cal"],
                         dtype)

@@ -203,6 +203,9 @@ def main():
     ws_s = torch.empty(cat.cat_sqnr_workspace_bytes(n * d_out), dtype=torch.uint8, device=dev)
     out = torch.empty(3, dtype=torch.float64, device=dev)
     sigma = torch.zeros((d_in, d_in), dtype=torch.float32, device=dev)
+    ws_c = torch.empty(max(16, cat.cat_cov_workspace_bytes(
+        B.CAT_BF16 if xdt == torch.bfloat16 else B.CAT_F32, n, d_in, B.CAT_COV_FULL, k)),
+        dtype=torch.uint8, device=dev)
 
     def step(i, ev=None):
         Xi, Yi = Xs[i % 2], Ys[i % 2]
@@ -213,7 +216,7 @@ def main():
         if ev: ev[2].record()
         cat.cat_sqnr(Yi, y_t, ws_s, out)
         if ev: ev[3].record()
-        cat.cat_cov_accumulate(Xi, sigma, B.CAT_COV_FULL, k)
+        cat.cat_cov_accumulate(Xi, sigma, B.CAT_COV_FULL, k, ws_c)
         if ev: ev[4].record()
 
     log(f"[bench] warmup {args.warmup} steps")

@@ -83,17 +83,34 @@ typedef enum {
  *       to fp32 rounding).
  * d     channels, 1 <= d, d % k == 0.
  * mode  CAT_COV_FULL: acc is [d x d] fp32, both triangles written (the
- *       kernel computes the upper triangle and mirrors it).
+ *       kernels compute the upper triangle and mirror it).
  *       CAT_COV_BLOCK_DIAG: acc is [d/k x k x k] fp32, block b holding
  *       X[:, bk:(b+1)k]^T X[:, bk:(b+1)k].
  * k     block size: power of two in [1, CAT_MAX_BLOCK] (only read in
  *       CAT_COV_BLOCK_DIAG mode).
- * acc   device fp32, caller-owned, read and written.  Products are formed
- *       exactly (bf16) and summed in fp32, with partial sums over at most
- *       4096 tokens before they are added into acc.
+ * acc   device fp32, caller-owned, read and written.  It must be symmetric
+ *       on entry (zero, or the result of earlier calls): for matrices of
+ *       256 channels or more the strictly lower triangle is rewritten as
+ *       the transpose of the updated upper triangle.  Products are formed
+ *       exactly (bf16) and summed in fp32 in register partials over at most
+ *       8192 tokens, which are added into acc in a fixed order: results are
+ *       deterministic for a given device.
+ * workspace, workspace_bytes
+ *       device scratch of at least cat_cov_workspace_bytes() bytes, 16-byte
+ *       aligned, caller-owned (partial tiles of workgroups that share a
+ *       tile); may be NULL when that size is 0.  One workspace must not be
+ *       used by calls that run concurrently.
+ * Errors: CAT_ERR_INVALID_ARG (NULL X/acc, bad sizes, mode, k, alignment),
+ *       CAT_ERR_WORKSPACE (workspace missing or too small), CAT_ERR_HIP.
  */
+/* Workspace size for cat_cov_accumulate with these arguments on the
+ * current device (it scales with the device's CU count; 0 for
+ * configurations that need none, or when the arguments are invalid or no
+ * device is present). */
+size_t cat_cov_workspace_bytes(int x_dtype, int64_t n, int64_t d, int mode, int64_t k);
 int cat_cov_accumulate(const void* X, int x_dtype, int64_t n, int64_t d,
-                       int mode, int64_t k, float* acc, void* stream);
+                       int mode, int64_t k, float* acc, void* workspace,
+                       size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------ (2)
  * Block transform fused with symmetric per-token quantization

@@ -40,7 +40,8 @@ CAT_MAX_BLOCK = 512
 
 # every symbol include/cat.h declares
 EXPORTED = (
-    "cat_cov_accumulate", "cat_transform_quant_workspace_bytes", "cat_transform_quant",
+    "cat_cov_workspace_bytes", "cat_cov_accumulate", "cat_transform_quant_workspace_bytes",
+    "cat_transform_quant",
     "cat_w4a4_linear", "cat_sqnr_workspace_bytes", "cat_sqnr", "cat_build_transform",
     "cat_quantize_weights", "cat_last_error", "cat_version",
 )
@@ -70,7 +71,9 @@ def lib() -> ctypes.CDLL:
         raise ImportError(f"{LIB_PATH} is missing: build it with "
                           "`python paper_2603_04359_amd/build.py` (or __graft_entry__.build())")
     L = ctypes.CDLL(LIB_PATH)
-    L.cat_cov_accumulate.argtypes = [_vp, _int, _i64, _i64, _int, _i64, _vp, _vp]
+    L.cat_cov_workspace_bytes.argtypes = [_int, _i64, _i64, _int, _i64]
+    L.cat_cov_workspace_bytes.restype = _sz
+    L.cat_cov_accumulate.argtypes = [_vp, _int, _i64, _i64, _int, _i64, _vp, _vp, _sz, _vp]
     L.cat_cov_accumulate.restype = _int
     L.cat_transform_quant_workspace_bytes.argtypes = [_i64, _i64, _i64]
     L.cat_transform_quant_workspace_bytes.restype = _sz
@@ -147,16 +150,31 @@ def _stream_ptr(stream):
 
 
 # ------------------------------------------------------------ device calls
-def cat_cov_accumulate(X, acc, mode: int = CAT_COV_FULL, k: int = 1, stream=None):
-    """acc += X^T X (FULL: acc [d, d]; BLOCK_DIAG: acc [d/k, k, k]), fp32."""
+def cat_cov_workspace_bytes(x_dtype: int, n: int, d: int, mode: int = CAT_COV_FULL,
+                            k: int = 1) -> int:
+    return int(lib().cat_cov_workspace_bytes(x_dtype, n, d, mode, k))
+
+
+def cat_cov_accumulate(X, acc, mode: int = CAT_COV_FULL, k: int = 1, workspace=None,
+                       stream=None):
+    """acc += X^T X (FULL: acc [d, d]; BLOCK_DIAG: acc [d/k, k, k]), fp32.
+    `workspace`: a device tensor of at least cat_cov_workspace_bytes() bytes;
+    when None, one is allocated for this call."""
     torch = _torch()
     px = _dev_ptr(X, "X", (torch.bfloat16, torch.float32))
     pa = _dev_ptr(acc, "acc", (torch.float32,))
     if X.dim() != 2:
         raise ValueError("X must be [n, d]")
     n, d = X.shape
+    code = _dtype_code(X)
+    if workspace is None:
+        need = cat_cov_workspace_bytes(code, n, d, mode, k)
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=X.device)
+    pw = _dev_ptr(workspace, "workspace")
+    wbytes = workspace.numel() * workspace.element_size()
     _check("cat_cov_accumulate",
-           lib().cat_cov_accumulate(px, _dtype_code(X), n, d, mode, k, pa, _stream_ptr(stream)))
+           lib().cat_cov_accumulate(px, code, n, d, mode, k, pa, pw, wbytes,
+                                    _stream_ptr(stream)))
 
 
 def cat_transform_quant_workspace_bytes(n: int, d: int, k: int) -> int:

@@ -31,8 +31,19 @@ int require_device(const char* where) {
 
 }  // namespace
 
+extern "C" size_t cat_cov_workspace_bytes(int x_dtype, int64_t n, int64_t d, int mode,
+                                          int64_t k) {
+    if (!valid_dtype(x_dtype) || n < 1 || d < 1) return 0;
+    if (mode != CAT_COV_FULL && mode != CAT_COV_BLOCK_DIAG) return 0;
+    if (mode == CAT_COV_BLOCK_DIAG && (!cat::is_pow2(k) || k > CAT_MAX_BLOCK || d % k)) return 0;
+    size_t bytes = 0;
+    if (catk::cov_workspace_bytes(x_dtype == CAT_BF16, d, mode, k, bytes) != hipSuccess) return 0;
+    return bytes;
+}
+
 extern "C" int cat_cov_accumulate(const void* X, int x_dtype, int64_t n, int64_t d, int mode,
-                                  int64_t k, float* acc, void* stream) {
+                                  int64_t k, float* acc, void* workspace, size_t workspace_bytes,
+                                  void* stream) {
     const char* fn = "cat_cov_accumulate";
     try {
         if (!X || !acc) return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": NULL pointer");
@@ -48,8 +59,19 @@ extern "C" int cat_cov_accumulate(const void* X, int x_dtype, int64_t n, int64_t
         if (!cat::aligned16(X) || !cat::aligned16(acc))
             return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": pointers must be 16-byte aligned");
         if (int rc = require_device(fn)) return rc;
-        const hipError_t err = catk::launch_cov_accumulate(X, x_dtype == CAT_BF16, n, d, mode, k, acc,
-                                                           static_cast<hipStream_t>(stream));
+        size_t need = 0;
+        hipError_t err = catk::cov_workspace_bytes(x_dtype == CAT_BF16, d, mode, k, need);
+        if (err != hipSuccess) return hip_fail(fn, err);
+        if (need > 0) {
+            if (!workspace) return fail(CAT_ERR_WORKSPACE, std::string(fn) + ": workspace is NULL");
+            if (workspace_bytes < need)
+                return fail(CAT_ERR_WORKSPACE, std::string(fn) + ": workspace too small (need " +
+                                                   std::to_string(need) + " bytes)");
+            if (!cat::aligned16(workspace))
+                return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": workspace must be 16-byte aligned");
+        }
+        err = catk::launch_cov_accumulate(X, x_dtype == CAT_BF16, n, d, mode, k, acc, workspace,
+                                          workspace_bytes, static_cast<hipStream_t>(stream));
         if (err != hipSuccess) return hip_fail(fn, err);
         return CAT_OK;
     } catch (const std::exception& e) {

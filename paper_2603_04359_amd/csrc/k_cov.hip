@@ -262,10 +262,10 @@ __global__ __launch_bounds__(kCovThreads) void cov_valu_kernel(const XT* __restr
 
 // ------------------------------------------- 256 x 256 tiles, stream-K
 // For matrices of at least 256 channels (bf16, channel count a multiple
-// of 8).  Each workgroup (4 waves, one per SIMD) owns a 256 x 256 tile of
-// the upper triangle; every wave keeps 128 x 128 fp32 partial sums (4 x 4
-// v_mfma_f32_32x32x16_bf16 accumulators).  Token slabs of 32 rows go from
-// HBM straight into a 3-stage LDS ring with global_load_lds_dwordx4, in
+// of 32).  Each workgroup (4 waves, one per SIMD) works on 256 x 256 tiles
+// of the upper triangle; every wave keeps 128 x 128 fp32 partial sums (4 x
+// 4 v_mfma_f32_32x32x16_bf16 accumulators).  Token slabs of 32 rows go from
+// HBM straight into a 4-stage LDS ring with global_load_lds_dwordx4, in
 // X's own row-major order (no transposition on the way in): 512 bytes of
 // each token row per operand, 16-byte units XOR-swizzled by row.  The
 // MFMA operands need 8 consecutive tokens of one channel; ds_read_tr16_b64
@@ -273,30 +273,70 @@ __global__ __launch_bounds__(kCovThreads) void cov_valu_kernel(const XT* __restr
 // 4e + q addresses token row e, channels 4q..4q+3, and lane i receives
 // channel i of the 4 rows.
 //
-// The work is the list of (tile, 32-token slab) units over all tiles; each
-// workgroup takes one contiguous share of it (stream-K), so every CU gets
-// the same number of MFMAs whatever the tile count.  A tile processed by a
-// single workgroup from its first to its last slab is added into acc with
-// plain read-modify-write stores; a tile split between workgroups is added
-// with fp32 atomics (so the last bit of such tiles may differ between
-// runs).  Off-diagonal tiles also add their transpose (16-byte runs: each
-// lane holds 4 consecutive rows of one column); diagonal tiles are
-// computed whole and written as is.
+// Work split (stream-K): the (tile, slab) units of all tiles, tile-major
+// with tiles in super-tile order, are cut into one contiguous share per
+// workgroup, so every CU gets the same number of MFMAs whatever the tile
+// count.  A workgroup processes its tiles in order of their first slab
+// (its share's head tile first), so the workgroups of one XCD stream
+// nearly the same token slabs at the same time and share them in L2.
+// A tile covered whole by one workgroup is added into acc directly; the
+// pieces of a split tile go to per-workgroup slots of the workspace with
+// plain stores, and cov_combine_kernel adds them into acc in a fixed order
+// (deterministic, no atomics) and writes every tile's mirror image.
 constexpr int kSkT = 256;                        // tile edge
 constexpr int kSkSlab = 32;                      // tokens per ring stage
-constexpr int kSkStages = 3;
+constexpr int kSkStages = 4;
+static_assert(kSkStages >= 2 && kSkStages <= 4, "wait counts cover at most 2 slabs ahead");
 constexpr int kSkRowUnits = kSkT / 8;            // 16-byte units per token row (32)
 constexpr int kSkOpUnits = kSkSlab * kSkRowUnits;  // units per operand and stage (1024)
 constexpr int kSkLoads = kSkOpUnits / kCovThreads; // direct loads per thread and operand (4)
-constexpr int kSkFlushSlabs = 256;               // at most 8192 tokens per register partial
+constexpr int kSkMaxSlabs = 256;                 // slabs per launch (8192 tokens)
+constexpr int64_t kSkSlotFloats = int64_t(kSkT) * kSkT;   // one 256 x 256 fp32 tile
 
 struct SkGeom {
     int64_t dim;     // channels of one matrix (d in FULL mode, k in BLOCK_DIAG mode)
     int64_t T;       // tiles along one edge of a matrix
     int64_t tri;     // upper-triangle tiles per matrix
-    int64_t S;       // slabs per tile (= token slabs)
-    int64_t U;       // total units = matrices * tri * S
+    int64_t tiles;   // tiles over all matrices
+    int64_t S;       // 32-token slabs of this launch
+    int64_t U;       // units = tiles * S
+    int64_t G;       // workgroups
 };
+
+// First unit of workgroup w's share (w = G gives U).
+__device__ __forceinline__ int64_t sk_begin(const SkGeom& g, int64_t w) { return g.U * w / g.G; }
+
+// The k-th upper-triangle tile of a T x T tile grid in super-tile order:
+// 4 x 4 groups of tiles (row-major over the upper triangle of groups),
+// row-major inside a group.  Consecutive tiles then share few distinct
+// 256-channel blocks of X, which is what one XCD's L2 holds.
+__device__ __forceinline__ void st_decode(int64_t r, int64_t T, int64_t& I, int64_t& J) {
+    const int64_t Ts = (T + 3) / 4;
+    for (int64_t P = 0; P < Ts; ++P)
+        for (int64_t Q = P; Q < Ts; ++Q) {
+            const int64_t i0 = 4 * P, i1 = (4 * P + 4 < T) ? 4 * P + 4 : T;
+            const int64_t j0 = 4 * Q, j1 = (4 * Q + 4 < T) ? 4 * Q + 4 : T;
+            const int64_t m = i1 - i0;
+            const int64_t cnt = P == Q ? m * (m + 1) / 2 : m * (j1 - j0);
+            if (r < cnt) {
+                if (P == Q) {
+                    int64_t i = 0;
+                    while (r >= m - i) {
+                        r -= m - i;
+                        ++i;
+                    }
+                    I = i0 + i;
+                    J = i0 + i + r;
+                } else {
+                    I = i0 + r / (j1 - j0);
+                    J = j0 + r % (j1 - j0);
+                }
+                return;
+            }
+            r -= cnt;
+        }
+    I = J = 0;   // not reached for r < T (T + 1) / 2
+}
 
 typedef short sk_v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) sk_v4i16 sk_lds_v4i16;
@@ -316,7 +356,8 @@ __device__ __forceinline__ bf16x8 sk_frag(const char __attribute__((address_spac
 __global__ __launch_bounds__(kCovThreads, 1) void cov_sk_kernel(const uint16_t* __restrict__ X,
                                                                 int64_t n, int64_t d, int mode,
                                                                 int64_t k, SkGeom g,
-                                                                float* __restrict__ acc) {
+                                                                float* __restrict__ acc,
+                                                                float* __restrict__ ws) {
     __shared__ __attribute__((aligned(16))) u32x4 ring[kSkStages][2][kSkOpUnits];
 
     const int tid = threadIdx.x;
@@ -326,11 +367,14 @@ __global__ __launch_bounds__(kCovThreads, 1) void cov_sk_kernel(const uint16_t* 
     const int l32 = lane & 31;
     const int h = lane >> 5;
 
-    // contiguous share of the unit list; consecutive shares on one XCD
-    const int64_t G = gridDim.x;
+    // this workgroup's share of the unit list (XCD-major numbering: the
+    // 32 consecutive shares of one XCD cover neighbouring tiles)
+    const int64_t G = g.G;
     int64_t w = blockIdx.x;
     if (G % 8 == 0) w = (blockIdx.x % 8) * (G / 8) + blockIdx.x / 8;
-    const int64_t u_begin = g.U * w / G, u_end = g.U * (w + 1) / G;
+    const int64_t u_begin = sk_begin(g, w), u_end = sk_begin(g, w + 1);
+    const int64_t t_first = u_begin / g.S, t_last = (u_end - 1) / g.S;
+    const bool head_first = (u_begin % g.S) != 0 && t_last > t_first;
 
     // direct-load geometry: load q of this thread fills unit (q*4+wave)*64+lane
     // of an operand stage, i.e. token row 8q + rr, swizzled position l32.
@@ -350,17 +394,16 @@ __global__ __launch_bounds__(kCovThreads, 1) void cov_sk_kernel(const uint16_t* 
         offB[a] = row * (kSkT * 2) + 16 * ub + 8 * (qq & 1);
     }
 
-    for (int64_t u = u_begin; u < u_end;) {
-        const int64_t tile = u / g.S;
-        const int64_t s0 = u % g.S;
-        int64_t s1 = (g.S < s0 + (u_end - u)) ? g.S : s0 + (u_end - u);
-        const int64_t cend = (s0 / kSkFlushSlabs + 1) * kSkFlushSlabs;   // register partial limit
-        s1 = s1 < cend ? s1 : cend;
-        u += s1 - s0;
-
+    for (int64_t idx = 0; u_begin < u_end && idx <= t_last - t_first; ++idx) {
+        // tiles in order of their first slab: t_first + 1 .. t_last, then t_first
+        const int64_t tile = head_first ? (idx < t_last - t_first ? t_first + 1 + idx : t_first)
+                                        : t_first + idx;
+        const int64_t s0 = tile == t_first ? u_begin % g.S : 0;
+        const int64_t s1 = tile == t_last ? (u_end - 1) % g.S + 1 : g.S;
+        const bool whole = s0 == 0 && s1 == g.S;
         const int64_t mat = tile / g.tri;
         int64_t I, J;
-        tri_decode(tile % g.tri, g.T, I, J);
+        st_decode(tile % g.tri, g.T, I, J);
         const int64_t colbase = mode == CAT_COV_FULL ? 0 : mat * k;
         const int64_t I0 = I * kSkT, J0 = J * kSkT;
         const bool diag = I == J;
@@ -378,18 +421,15 @@ __global__ __launch_bounds__(kCovThreads, 1) void cov_sk_kernel(const uint16_t* 
         auto issue = [&](int64_t s, int st) {
             const int64_t t0 = s * kSkSlab;
             const char* base = reinterpret_cast<const char*>(X + t0 * d);
+            const uint32_t la = lds_addr(&ring[st][0][wave * 64]);
+            const uint32_t lb = lds_addr(&ring[st][1][wave * 64]);
             if (t0 + kSkSlab <= n) {
 #pragma unroll
-                for (int q = 0; q < kSkLoads; ++q)
-                    __builtin_amdgcn_global_load_lds(
-                        (const void*)(base + (oa + q * 8u * row_bytes)),
-                        (lds_void_t*)&ring[st][0][(q * 4 + wave) * 64], 16, 0, 0);
+                for (int q = 0; q < kSkLoads; ++q) dma16(base, oa + q * 8u * row_bytes, la + q * 4096u);
                 if (!diag) {
 #pragma unroll
                     for (int q = 0; q < kSkLoads; ++q)
-                        __builtin_amdgcn_global_load_lds(
-                            (const void*)(base + (ob + q * 8u * row_bytes)),
-                            (lds_void_t*)&ring[st][1][(q * 4 + wave) * 64], 16, 0, 0);
+                        dma16(base, ob + q * 8u * row_bytes, lb + q * 4096u);
                 }
             } else {
                 // ragged last slab: rows past n load row n-1 (zeroed once landed)
@@ -397,13 +437,8 @@ __global__ __launch_bounds__(kCovThreads, 1) void cov_sk_kernel(const uint16_t* 
                 for (int q = 0; q < kSkLoads; ++q) {
                     const int64_t t = t0 + 8 * q + rr;
                     const uint32_t back = t < n ? 0u : static_cast<uint32_t>(t - (n - 1)) * row_bytes;
-                    __builtin_amdgcn_global_load_lds(
-                        (const void*)(base + (oa + q * 8u * row_bytes - back)),
-                        (lds_void_t*)&ring[st][0][(q * 4 + wave) * 64], 16, 0, 0);
-                    if (!diag)
-                        __builtin_amdgcn_global_load_lds(
-                            (const void*)(base + (ob + q * 8u * row_bytes - back)),
-                            (lds_void_t*)&ring[st][1][(q * 4 + wave) * 64], 16, 0, 0);
+                    dma16(base, oa + q * 8u * row_bytes - back, la + q * 4096u);
+                    if (!diag) dma16(base, ob + q * 8u * row_bytes - back, lb + q * 4096u);
                 }
             }
         };
@@ -414,103 +449,259 @@ __global__ __launch_bounds__(kCovThreads, 1) void cov_sk_kernel(const uint16_t* 
 #pragma unroll
             for (int b = 0; b < 4; ++b) part[a][b] = f32x16{};
 
-        issue(s0, 0);
-        if (s0 + 1 < s1) issue(s0 + 1, 1);
-        int st = 0;
-        for (int64_t s = s0; s < s1; ++s) {
-            if (s + 1 < s1) {
-                if (diag) wait_vmcnt<kSkLoads>();
-                else wait_vmcnt<2 * kSkLoads>();
+        // Software pipeline: the fragments of the first 16 tokens of slab
+        // s + 1 are read right after the barrier that publishes the slab,
+        // while the MFMAs of the second half of slab s still run.
+        // Wait until this thread's loads of slab s have landed: at most the
+        // loads of the slabs issued after it (up to slab `last`) may still be
+        // outstanding.
+        auto wait_slab = [&](int64_t s, int64_t last) {
+            const int64_t ahead = last - s;
+            if (diag) {
+                if (ahead >= 2) wait_vmcnt<2 * kSkLoads>();
+                else if (ahead == 1) wait_vmcnt<kSkLoads>();
+                else wait_vmcnt<0>();
             } else {
-                wait_vmcnt<0>();
+                if (ahead >= 2) wait_vmcnt<4 * kSkLoads>();
+                else if (ahead == 1) wait_vmcnt<2 * kSkLoads>();
+                else wait_vmcnt<0>();
             }
             const int64_t t0 = s * kSkSlab;
             if (t0 + kSkSlab > n) {
+                // ragged last slab: rows past n were loaded clamped; zero them
+                const int sl = static_cast<int>((s - s0) % kSkStages);
 #pragma unroll
                 for (int q = 0; q < kSkLoads; ++q) {
                     if (t0 + 8 * q + rr >= n) {
-                        ring[st][0][(q * 4 + wave) * 64 + lane] = u32x4{0u, 0u, 0u, 0u};
-                        if (!diag) ring[st][1][(q * 4 + wave) * 64 + lane] = u32x4{0u, 0u, 0u, 0u};
+                        ring[sl][0][(q * 4 + wave) * 64 + lane] = u32x4{0u, 0u, 0u, 0u};
+                        if (!diag) ring[sl][1][(q * 4 + wave) * 64 + lane] = u32x4{0u, 0u, 0u, 0u};
                     }
                 }
             }
-            lds_barrier();   // slab s landed for every thread; slab s-1 consumed
-            if (s + 2 < s1) issue(s + 2, st == 0 ? 2 : st - 1);
+        };
+        typedef const char __attribute__((address_space(3))) * lds_cptr;
+        auto read_frags = [&](int sl, int kk, bf16x8* fa, bf16x8* fb) {
+            lds_cptr baseA = (lds_cptr)&ring[sl][0][0];
+            lds_cptr baseB = (lds_cptr)&ring[sl][diag ? 0 : 1][0];
+#pragma unroll
+            for (int a = 0; a < 4; ++a) fa[a] = sk_frag(baseA, offA[a] + kk * 16 * kSkT * 2);
+#pragma unroll
+            for (int b = 0; b < 4; ++b) fb[b] = sk_frag(baseB, offB[b] + kk * 16 * kSkT * 2);
+        };
+        auto mfmas = [&](const bf16x8* fa, const bf16x8* fb) {
+#pragma unroll
+            for (int a = 0; a < 4; ++a)
+#pragma unroll
+                for (int b = 0; b < 4; ++b)
+                    part[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[a], fb[b], part[a][b],
+                                                                         0, 0, 0);
+        };
 
-            const char __attribute__((address_space(3)))* baseA =
-                (const char __attribute__((address_space(3)))*)&ring[st][0][0];
-            const char __attribute__((address_space(3)))* baseB =
-                (const char __attribute__((address_space(3)))*)&ring[st][diag ? 0 : 1][0];
 #pragma unroll
-            for (int kk = 0; kk < 2; ++kk) {
-                bf16x8 fa[4], fb[4];
-#pragma unroll
-                for (int a = 0; a < 4; ++a) fa[a] = sk_frag(baseA, offA[a] + kk * 16 * kSkT * 2);
-#pragma unroll
-                for (int b = 0; b < 4; ++b) fb[b] = sk_frag(baseB, offB[b] + kk * 16 * kSkT * 2);
-#pragma unroll
-                for (int a = 0; a < 4; ++a)
-#pragma unroll
-                    for (int b = 0; b < 4; ++b)
-                        part[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[a], fb[b],
-                                                                             part[a][b], 0, 0, 0);
+        for (int p = 0; p < kSkStages - 1; ++p)
+            if (s0 + p < s1) issue(s0 + p, p);
+        wait_slab(s0, (s0 + kSkStages - 2 < s1 - 1) ? s0 + kSkStages - 2 : s1 - 1);
+        lds_barrier();
+        bf16x8 fa0[4], fb0[4], fa1[4], fb1[4];
+        read_frags(0, 0, fa0, fb0);
+        int st = 0;
+        for (int64_t s = s0; s < s1; ++s) {
+            read_frags(st, 1, fa1, fb1);
+            mfmas(fa0, fb0);
+            const int nx = st == kSkStages - 1 ? 0 : st + 1;
+            if (s + 1 < s1) {
+                // slabs issued so far: up to s + kSkStages - 2
+                wait_slab(s + 1, (s + kSkStages - 2 < s1 - 1) ? s + kSkStages - 2 : s1 - 1);
+                lds_barrier();   // slab s+1 landed everywhere; slab s-1 fully consumed
+                if (s + kSkStages - 1 < s1)
+                    issue(s + kSkStages - 1, st == 0 ? kSkStages - 1 : st - 1);
+                read_frags(nx, 0, fa0, fb0);
             }
-            st = st == 2 ? 0 : st + 1;
+            mfmas(fa1, fb1);
+            st = nx;
         }
 
-        // Add the partial sums into acc with fp32 atomics (no return value):
-        // each wave instruction covers two 128-byte row segments.  The
-        // transpose for the mirror tile goes through LDS (a 32 x 33 float
-        // pad per wave) so its atomics are row segments too.  32-bit element
-        // offsets from the matrix base; the empty asm keeps them from being
-        // precomputed outside the loop.
-        lds_barrier();   // the ring is free: every wave has finished reading it
-        uint32_t dimu = static_cast<uint32_t>(g.dim);
-        uint32_t rowb = static_cast<uint32_t>(I0 + wm * 128 + 4 * h);
-        uint32_t colb = static_cast<uint32_t>(J0 + wn * 128 + l32);
-        asm volatile("" : "+v"(rowb), "+v"(colb), "+s"(dimu));
-        const uint32_t row_u = static_cast<uint32_t>(I0 + wm * 128);
-        const uint32_t col_u = static_cast<uint32_t>(J0 + wn * 128);
-        float* pad = reinterpret_cast<float*>(&ring[0][0][0]) + wave * (32 * 33);
+        // Partial sums out.  A whole tile is added into acc (upper tile,
+        // both triangles of a diagonal tile) in 4 chunks of 64 values per
+        // lane; a split tile's piece is stored to its slot, a 256 x 256
+        // row-major fp32 tile (slot 0: the share's first tile, slot 1: its
+        // last).  32-bit element offsets; the empty asm statements keep the
+        // offsets from being precomputed outside the loop and the chunks
+        // apart.
+        uint32_t rowb = static_cast<uint32_t>(wm * 128 + 4 * h);
+        uint32_t colb = static_cast<uint32_t>(wn * 128 + l32);
+        asm volatile("" : "+v"(rowb), "+v"(colb));
+        if (whole) {
+            // Through LDS (the ring is free once every wave is past its last
+            // fragment read): the 128 x 256 half of the tile that waves
+            // (h, 0) and (h, 1) hold is written row-major into LDS, then all
+            // 256 threads add it into acc with 16-byte row accesses.  This
+            // keeps the read-modify-write of acc out of the accumulator
+            // registers.
+            float* stage = reinterpret_cast<float*>(&ring[0][0][0]);   // 128 x 256 fp32
+            const int64_t dimv = g.dim;
+            const bool rows_ok = I0 + kSkT <= dimv, cols_ok = J0 + kSkT <= dimv;
 #pragma unroll
-        for (int a = 0; a < 4; ++a)
+            for (int half = 0; half < 2; ++half) {
+                lds_barrier();
+                if (wm == half) {
 #pragma unroll
-            for (int b = 0; b < 4; ++b) {
-                if (row_u + 32 * a >= dimu || col_u + 32 * b >= dimu) continue;
-                const uint32_t up = (rowb + 32 * a) * dimu + colb + 32 * b;
+                    for (int a = 0; a < 4; ++a)
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    unsafeAtomicAdd(accm + up + (8 * (r >> 2) + (r & 3)) * dimu, part[a][b][r]);
-                if (!diag) {
-                    // element (R, C) of the 32 x 32 block -> pad[C][R]; read back
-                    // as (R, C) of the transposed block
+                        for (int b = 0; b < 4; ++b)
 #pragma unroll
-                    for (int r = 0; r < 16; ++r)
-                        pad[l32 * 33 + 8 * (r >> 2) + 4 * h + (r & 3)] = part[a][b][r];
-                    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
-                    const uint32_t mi = (colb - l32 + 32 * b + 4 * h) * dimu +
-                                        (rowb - 4 * h + 32 * a + l32);
+                            for (int r = 0; r < 16; ++r)
+                                stage[(32 * a + 8 * (r >> 2) + 4 * h + (r & 3)) * kSkT + wn * 128 +
+                                      32 * b + l32] = part[a][b][r];
+                }
+                lds_barrier();
+                // 128 rows x 64 float4 per row; thread tid takes column group
+                // tid % 64 of rows tid / 64 + 4 j
+                const int cg = tid & 63;
+                const int64_t col = J0 + 4 * cg;
+                if (cols_ok || col < dimv) {
 #pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int R = 8 * (r >> 2) + 4 * h + (r & 3);
-                        unsafeAtomicAdd(accm + mi + (8 * (r >> 2) + (r & 3)) * dimu,
-                                        pad[R * 33 + l32]);
+                    for (int j0 = 0; j0 < 32; j0 += 8) {
+                        f32x4 old[8];
+#pragma unroll
+                        for (int j = 0; j < 8; ++j) {
+                            const int row = (tid >> 6) + 4 * (j0 + j);
+                            const int64_t grow = I0 + 128 * half + row;
+                            old[j] = (rows_ok || grow < dimv)
+                                         ? *reinterpret_cast<const f32x4*>(accm + grow * dimv + col)
+                                         : f32x4{0.f, 0.f, 0.f, 0.f};
+                        }
+#pragma unroll
+                        for (int j = 0; j < 8; ++j) {
+                            const int row = (tid >> 6) + 4 * (j0 + j);
+                            const int64_t grow = I0 + 128 * half + row;
+                            const f32x4 add = *reinterpret_cast<const f32x4*>(stage + row * kSkT + 4 * cg);
+                            if (rows_ok || grow < dimv)
+                                *reinterpret_cast<f32x4*>(accm + grow * dimv + col) = old[j] + add;
+                        }
                     }
-                    __builtin_amdgcn_s_waitcnt(0xC07F);
                 }
             }
+        } else {
+            float* slot = ws + (w * 2 + (tile == t_first ? 0 : 1)) * kSkSlotFloats;
+#pragma unroll
+            for (int a = 0; a < 4; ++a)
+#pragma unroll
+                for (int b = 0; b < 4; ++b)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r)
+                        slot[(rowb + 32 * a + 8 * (r >> 2) + (r & 3)) * kSkT + colb + 32 * b] =
+                            part[a][b][r];
+        }
         lds_barrier();   // every wave is done with the ring before the next tile refills it
     }
 }
 
-static bool cov_sk_geometry(int64_t n, int64_t d, int mode, int64_t k, SkGeom& g) {
+// The workgroup whose share holds unit u.
+__device__ __forceinline__ int64_t sk_owner(const SkGeom& g, int64_t u) {
+    int64_t w = u * g.G / g.U;
+    while (w + 1 < g.G && sk_begin(g, w + 1) <= u) ++w;
+    while (w > 0 && sk_begin(g, w) > u) --w;
+    return w;
+}
+
+// After cov_sk_kernel: every split tile's pieces are added into acc in
+// share order (acc + piece of the lowest workgroup + ... ), and every
+// off-diagonal tile's transpose is written below the diagonal.  One
+// workgroup per 64 x 64 sub-block of a tile: coalesced 16-byte row reads,
+// transposition through LDS, coalesced 16-byte row writes.
+__global__ __launch_bounds__(kCovThreads) void cov_combine_kernel(float* __restrict__ acc, int mode,
+                                                                  int64_t k, SkGeom g,
+                                                                  const float* __restrict__ ws) {
+    __shared__ float tr[64][65];
+    const int64_t tile = blockIdx.x / 16;
+    const int sub = static_cast<int>(blockIdx.x % 16);
+    const int64_t mat = tile / g.tri;
+    int64_t I, J;
+    st_decode(tile % g.tri, g.T, I, J);
+    const int sr = (sub >> 2) * 64, sc = (sub & 3) * 64;   // sub-block origin inside the tile
+    const int64_t r0 = I * kSkT + sr, c0 = J * kSkT + sc;
+    if (r0 >= g.dim || c0 >= g.dim) return;
+    const int64_t w_lo = sk_owner(g, tile * g.S), w_hi = sk_owner(g, (tile + 1) * g.S - 1);
+    const bool whole = w_lo == w_hi && sk_begin(g, w_lo) <= tile * g.S &&
+                       sk_begin(g, w_lo + 1) >= (tile + 1) * g.S;
+    if (whole && I == J) return;   // added in place by the main kernel, no mirror
+    float* m = acc + (mode == CAT_COV_FULL ? 0 : mat * k * k);
+    const int tid = threadIdx.x;
+    const int rl = tid >> 4, cl = 4 * (tid & 15);
+    f32x4 v[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int row = rl + 16 * i;
+        const bool ok = r0 + row < g.dim && c0 + cl < g.dim;
+        v[i] = ok ? *reinterpret_cast<const f32x4*>(m + (r0 + row) * g.dim + c0 + cl)
+                  : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    if (!whole) {
+        for (int64_t w = w_lo; w <= w_hi; ++w) {
+            const int64_t t_first = sk_begin(g, w) / g.S;
+            const float* slot = ws + (w * 2 + (tile == t_first ? 0 : 1)) * kSkSlotFloats;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                v[i] += *reinterpret_cast<const f32x4*>(slot + (sr + rl + 16 * i) * kSkT + sc + cl);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int row = rl + 16 * i;
+            if (r0 + row < g.dim && c0 + cl < g.dim)
+                *reinterpret_cast<f32x4*>(m + (r0 + row) * g.dim + c0 + cl) = v[i];
+        }
+    }
+    if (I == J) return;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int row = rl + 16 * i;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) tr[row][cl + e] = v[i][e];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int row = rl + 16 * i;   // row of the lower block = column of the upper one
+        if (c0 + row >= g.dim || r0 + cl >= g.dim) continue;
+        const f32x4 t = {tr[cl][row], tr[cl + 1][row], tr[cl + 2][row], tr[cl + 3][row]};
+        *reinterpret_cast<f32x4*>(m + (c0 + row) * g.dim + r0 + cl) = t;
+    }
+}
+
+// Geometry of one launch over n <= kSkMaxSlabs * 32 tokens.
+static bool cov_sk_geometry(int64_t n, int64_t d, int mode, int64_t k, int64_t cus, SkGeom& g) {
     g.dim = mode == CAT_COV_FULL ? d : k;
     const int64_t nmat = mode == CAT_COV_FULL ? 1 : d / k;
     g.T = (g.dim + kSkT - 1) / kSkT;
     g.tri = g.T * (g.T + 1) / 2;
+    g.tiles = nmat * g.tri;
     g.S = (n + kSkSlab - 1) / kSkSlab;
-    g.U = nmat * g.tri * g.S;
+    g.U = g.tiles * g.S;
+    g.G = g.U < cus ? g.U : cus;
     return g.U > 0;
+}
+
+static bool cov_uses_sk(int x_bf16, int64_t d, int mode, int64_t k) {
+    const int64_t dim = mode == CAT_COV_FULL ? d : k;
+    return x_bf16 && dim >= kSkT && (d % 8) == 0 && (dim % 32) == 0;
+}
+
+static hipError_t device_cus(int& cus) {
+    int dev = 0;
+    hipError_t err = hipGetDevice(&dev);
+    if (err != hipSuccess) return err;
+    return hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+}
+
+hipError_t cov_workspace_bytes(int x_bf16, int64_t d, int mode, int64_t k, size_t& bytes) {
+    bytes = 0;
+    if (!cov_uses_sk(x_bf16, d, mode, k)) return hipSuccess;
+    int cus = 0;
+    hipError_t err = device_cus(cus);
+    if (err != hipSuccess) return err;
+    bytes = static_cast<size_t>(cus) * 2 * kSkSlotFloats * sizeof(float);
+    return hipSuccess;
 }
 
 static int64_t cov_grid(int tile, int64_t d, int mode, int64_t k) {
@@ -523,20 +714,36 @@ static int64_t cov_grid(int tile, int64_t d, int mode, int64_t k) {
 }
 
 hipError_t launch_cov_accumulate(const void* X, int x_bf16, int64_t n, int64_t d, int mode,
-                                 int64_t k, float* acc, hipStream_t stream) {
+                                 int64_t k, float* acc, void* workspace, size_t workspace_bytes,
+                                 hipStream_t stream) {
     const int64_t dim = mode == CAT_COV_FULL ? d : k;
-    if (x_bf16 && dim >= kSkT && (d % 8) == 0 && (dim % 32) == 0) {
-        SkGeom g;
-        if (!cov_sk_geometry(n, d, mode, k, g)) return hipSuccess;
-        int dev = 0, cus = 0;
-        hipError_t err = hipGetDevice(&dev);
+    if (cov_uses_sk(x_bf16, d, mode, k)) {
+        int cus = 0;
+        hipError_t err = device_cus(cus);
         if (err != hipSuccess) return err;
-        err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
-        if (err != hipSuccess) return err;
-        const int64_t grid = g.U < cus ? g.U : cus;
-        hipLaunchKernelGGL(cov_sk_kernel, dim3(static_cast<uint32_t>(grid)), dim3(kCovThreads), 0,
-                           stream, static_cast<const uint16_t*>(X), n, d, mode, k, g, acc);
-        return hipGetLastError();
+        if (workspace_bytes < static_cast<size_t>(cus) * 2 * kSkSlotFloats * sizeof(float))
+            return hipErrorInvalidValue;   // checked by the caller; never reached
+        const uint16_t* Xb = static_cast<const uint16_t*>(X);
+        // one launch pair per 8192 tokens: each register partial covers at
+        // most that many tokens, and the pieces are combined before the
+        // workspace is reused
+        for (int64_t t0 = 0; t0 < n; t0 += int64_t(kSkMaxSlabs) * kSkSlab) {
+            const int64_t nc = (n - t0 < int64_t(kSkMaxSlabs) * kSkSlab) ? n - t0
+                                                                       : int64_t(kSkMaxSlabs) * kSkSlab;
+            SkGeom g;
+            if (!cov_sk_geometry(nc, d, mode, k, cus, g)) return hipSuccess;
+            hipLaunchKernelGGL(cov_sk_kernel, dim3(static_cast<uint32_t>(g.G)), dim3(kCovThreads),
+                               0, stream, Xb + t0 * d, nc, d, mode, k, g, acc,
+                               static_cast<float*>(workspace));
+            err = hipGetLastError();
+            if (err != hipSuccess) return err;
+            hipLaunchKernelGGL(cov_combine_kernel, dim3(static_cast<uint32_t>(g.tiles * 16)),
+                               dim3(kCovThreads), 0, stream, acc, mode, k, g,
+                               static_cast<const float*>(workspace));
+            err = hipGetLastError();
+            if (err != hipSuccess) return err;
+        }
+        return hipSuccess;
     }
     if (x_bf16 && dim >= 64 && (dim % 2) == 0 && (d % 2) == 0) {
         const uint16_t* Xb = static_cast<const uint16_t*>(X);

@@ -310,17 +310,16 @@ __global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
     // slot sl of a stage holds token row sl / U, logical unit (sl % U) ^ swz
     auto issue = [&](int64_t tile, int st) {
         const int64_t t0 = tile * C::TT;
+        const uint16_t* base = X + t0 * d + b * K;   // wave-uniform
+        const int64_t last = n - 1 - t0;              // last valid row of the tile
 #pragma unroll
         for (int q = 0; q < C::LOADS; ++q) {
             const int sl = (q * 4 + wave) * 64 + lane;
-            const int rr = sl / C::U;
+            int rr = sl / C::U;
             const int u = (sl % C::U) ^ tq_xswz<K>(rr);
-            int64_t tok = t0 + rr;
-            tok = tok < n ? tok : n - 1;          // rows past the end: never used
-            const uint16_t* src = X + tok * d + b * K + u * 8;
-            __builtin_amdgcn_global_load_lds((const void*)src,
-                                             (lds_void_t*)&ring[st][(q * 4 + wave) * 64], 16,
-                                             0, 0);
+            rr = rr <= last ? rr : static_cast<int>(last);   // rows past the end: never used
+            dma16(base, static_cast<uint32_t>((rr * d + u * 8) * 2),
+                  lds_addr(&ring[st][(q * 4 + wave) * 64]));
         }
     };
 

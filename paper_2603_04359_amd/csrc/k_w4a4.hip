@@ -151,17 +151,15 @@ __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
         for (int q = 0; q < kLoadsA; ++q) {
             int64_t col = k0 + ua_off[q];
             col = col < row_bytes ? col : 0;     // past the row end: any in-bounds unit
-            __builtin_amdgcn_global_load_lds(
-                (const void*)(a_base + (a_off[q] + static_cast<uint32_t>(col))),
-                (lds_void_t*)&ring_a[st][(q * 4 + wave) * 64], 16, 0, 0);
+            dma16(a_base, a_off[q] + static_cast<uint32_t>(col),
+                  lds_addr(&ring_a[st][(q * 4 + wave) * 64]));
         }
 #pragma unroll
         for (int q = 0; q < kLoadsB; ++q) {
             int64_t col = k0 + ub_off[q];
             col = col < row_bytes ? col : 0;
-            __builtin_amdgcn_global_load_lds(
-                (const void*)(b_base + (b_off[q] + static_cast<uint32_t>(col))),
-                (lds_void_t*)&ring_b[st][(q * 4 + wave) * 64], 16, 0, 0);
+            dma16(b_base, b_off[q] + static_cast<uint32_t>(col),
+                  lds_addr(&ring_b[st][(q * 4 + wave) * 64]));
         }
     };
     constexpr int kLoadsPerStep = kLoadsA + kLoadsB;

@@ -28,7 +28,11 @@ hipError_t launch_w4a4_linear(const uint8_t* codes_x, const float* s_x, const ui
                               float* y, int32_t* acc_out, hipStream_t stream);
 
 // ---- second moment accumulation
+// Workspace of launch_cov_accumulate on the current device (0 when the
+// configuration runs on kernels that need none).
+hipError_t cov_workspace_bytes(int x_bf16, int64_t d, int mode, int64_t k, size_t& bytes);
 hipError_t launch_cov_accumulate(const void* X, int x_bf16, int64_t n, int64_t d, int mode,
-                                 int64_t k, float* acc, hipStream_t stream);
+                                 int64_t k, float* acc, void* workspace, size_t workspace_bytes,
+                                 hipStream_t stream);
 
 }  // namespace catk

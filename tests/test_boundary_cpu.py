@@ -43,15 +43,15 @@ P = 1 << 20
 
 def test_cov_invalid_args():
     L = cat.lib()
-    assert L.cat_cov_accumulate(None, 1, 10, 64, 0, 1, P, None) == B.CAT_ERR_INVALID_ARG
+    assert L.cat_cov_accumulate(None, 1, 10, 64, 0, 1, P, P, 1 << 30, None) == B.CAT_ERR_INVALID_ARG
     assert "NULL" in cat.cat_last_error()
-    assert L.cat_cov_accumulate(P, 7, 10, 64, 0, 1, P, None) == B.CAT_ERR_INVALID_ARG
-    assert L.cat_cov_accumulate(P, 1, 0, 64, 0, 1, P, None) == B.CAT_ERR_INVALID_ARG
-    assert L.cat_cov_accumulate(P, 1, 10, 64, 5, 1, P, None) == B.CAT_ERR_INVALID_ARG
-    assert L.cat_cov_accumulate(P, 1, 10, 64, 1, 24, P, None) == B.CAT_ERR_INVALID_ARG
-    assert L.cat_cov_accumulate(P, 1, 10, 64, 1, 1024, P, None) == B.CAT_ERR_INVALID_ARG
-    assert L.cat_cov_accumulate(P, 1, 10, 96, 1, 64, P, None) == B.CAT_ERR_INVALID_ARG
-    assert L.cat_cov_accumulate(P + 2, 1, 10, 64, 0, 1, P, None) == B.CAT_ERR_INVALID_ARG
+    assert L.cat_cov_accumulate(P, 7, 10, 64, 0, 1, P, P, 1 << 30, None) == B.CAT_ERR_INVALID_ARG
+    assert L.cat_cov_accumulate(P, 1, 0, 64, 0, 1, P, P, 1 << 30, None) == B.CAT_ERR_INVALID_ARG
+    assert L.cat_cov_accumulate(P, 1, 10, 64, 5, 1, P, P, 1 << 30, None) == B.CAT_ERR_INVALID_ARG
+    assert L.cat_cov_accumulate(P, 1, 10, 64, 1, 24, P, P, 1 << 30, None) == B.CAT_ERR_INVALID_ARG
+    assert L.cat_cov_accumulate(P, 1, 10, 64, 1, 1024, P, P, 1 << 30, None) == B.CAT_ERR_INVALID_ARG
+    assert L.cat_cov_accumulate(P, 1, 10, 96, 1, 64, P, P, 1 << 30, None) == B.CAT_ERR_INVALID_ARG
+    assert L.cat_cov_accumulate(P + 2, 1, 10, 64, 0, 1, P, P, 1 << 30, None) == B.CAT_ERR_INVALID_ARG
     assert "aligned" in cat.cat_last_error()
 
 

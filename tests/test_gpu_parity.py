@@ -111,6 +111,18 @@ def _tq_gpu(X, T, k, x_dtype, t_dtype):
     return host(codes), host(s_x)
 
 
+def _tq_gpu_from_device(dX, T, k):
+    torch = torch_mod()
+    n, d = dX.shape
+    dT = dev(T, "bf16")
+    codes = torch.empty((n, d // 2), dtype=torch.uint8, device="cuda")
+    s_x = torch.empty(n, dtype=torch.float32, device="cuda")
+    ws = torch.empty(cat.cat_transform_quant_workspace_bytes(n, d, k), dtype=torch.uint8,
+                     device="cuda")
+    cat.cat_transform_quant(dX, dT, k, codes, s_x, ws)
+    return host(codes), host(s_x)
+
+
 def _check_scales(s_gpu, s_or, label):
     assert np.all((s_gpu == 0) == (s_or == 0)), label
     nz = s_or != 0
@@ -308,3 +320,50 @@ def test_end_to_end_tiny_layer_sqnr(transform):
     or_db = o.sqnr(y, fw["y_tilde"])[2]
     say(f"  SQNR gpu {gpu_db:.4f} dB, oracle {or_db:.4f} dB")
     assert abs(gpu_db - or_db) <= 0.05
+
+
+# ------------------------------------------- device addresses above 2^31
+def _view_with_bit31(torch, nbytes):
+    """A uint8 device view of `nbytes` whose address has bit 31 of its low
+    32-bit word set (the kernels take wave-uniform 64-bit base addresses
+    apart into 32-bit halves; this catches a sign-extended low half)."""
+    buf = torch.empty((1 << 31) + nbytes + 4096, dtype=torch.uint8, device="cuda")
+    base = buf.data_ptr()
+    off = 0 if base & 0x80000000 else (0x80000000 - (base & 0xFFFFFFFF)) % (1 << 32)
+    off = (off + 15) // 16 * 16
+    v = buf[off:off + nbytes]
+    assert v.data_ptr() & 0x80000000 and v.data_ptr() % 16 == 0
+    return buf, v
+
+
+def test_inputs_at_addresses_with_bit31_set():
+    say("cov / transform_quant / w4a4 on inputs at addresses with bit 31 set")
+    torch = torch_mod()
+    n, d, k = 300, 512, 128
+    cfg = wl.get_config("attn4096", d_in=d, d_out=d, n_cal=n, n=1)
+    X = o.round_storage(wl.make_layer(cfg, seed=31, with_eval=False, with_weights=False)["X_cal"],
+                        "bf16")
+    xbits = torch.from_numpy(wl.to_bf16_bits(X).view(np.uint8).reshape(-1).copy())
+    keep, xv = _view_with_bit31(torch, xbits.numel())
+    xv.copy_(xbits.cuda())
+    dX = xv.view(torch.bfloat16).view(n, d)
+    acc = torch.zeros((d, d), dtype=torch.float32, device="cuda")
+    cat.cat_cov_accumulate(dX, acc, B.CAT_COV_FULL, 1)
+    assert rel_fro(host(acc), o.second_moment_sum(X)) <= 1e-5
+    T = _cat_T(X, wl.random_bf16_matrix(d, d, seed=2, scale=0.05), k, "bf16")
+    codes, _ = _tq_gpu_from_device(dX, T, k)
+    _, _, _ = check_codes(codes, X, T, label="bit31 tq")
+    qw = wl.random_codes(256, d, seed=4)
+    pw = o.pack_int4(qw)
+    keep2, wv = _view_with_bit31(torch, pw.size)
+    wv.copy_(torch.from_numpy(pw.reshape(-1).copy()).cuda())
+    cw = wv.view(256, d // 2)
+    sw = torch.rand(256, device="cuda") + 0.5
+    cx = torch.from_numpy(codes).cuda()
+    sx = torch.rand(n, device="cuda") + 0.5
+    y = torch.empty((n, 256), dtype=torch.float32, device="cuda")
+    acc_i = torch.empty((n, 256), dtype=torch.int32, device="cuda")
+    cat.cat_w4a4_linear(cx, sx, cw, sw, y, acc_i)
+    ref_acc, _ = o.w4a4_linear(o.unpack_int4(codes), host(sx), qw, host(sw))
+    assert np.array_equal(host(acc_i), ref_acc.astype(np.int32))
+    del keep, keep2

@@ -109,4 +109,24 @@ __device__ __forceinline__ void dma16(const void* sbase, uint32_t voff, uint32_t
         : "memory");
 }
 
+// As dma16 with 4 bytes per lane (global_load_lds_dword): lane L's dword
+// lands at LDS byte address lds_base + 4 L.
+__device__ __forceinline__ void dma4(const void* sbase, uint32_t voff, uint32_t lds_base) {
+    const uint64_t b = reinterpret_cast<uint64_t>(sbase);
+    const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b)));
+    const uint32_t hi =
+        static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(b >> 32)));
+    const uint64_t bu = static_cast<uint64_t>(lo) | (static_cast<uint64_t>(hi) << 32);
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %3\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dword %1, %2\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "v"(voff), "s"(bu), "s"(__builtin_amdgcn_readfirstlane(lds_base))
+        : "memory");
+}
+
 }  // namespace catk

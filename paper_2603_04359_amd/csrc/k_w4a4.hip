@@ -38,9 +38,11 @@
 // Persistent launch: kWgPerCu workgroups per CU walk lists of tiles in an
 // XCD-aware order (workgroups are dealt to the 8 XCDs round-robin; those of
 // XCD x walk one contiguous range of tiles, in groups of kGroupM row
-// panels, so tiles resident on one XCD share panels in its L2).  The first
-// steps of the next tile are requested before the current tile's output is
-// stored.  Output rows stream out with nontemporal stores.
+// panels, so tiles resident on one XCD share panels in its L2).  The
+// operand steps of consecutive tiles form one stream through the ring, and
+// the tile's scales are staged in LDS with the first step, so the epilogue
+// reads no global memory and the next tile never waits behind the output
+// stores.  Output rows stream out with nontemporal stores.
 #include "device_common.h"
 #include "kernels.h"
 
@@ -101,6 +103,9 @@ __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
     int64_t d_out, float* __restrict__ y, int32_t* __restrict__ acc_out) {
     __shared__ __attribute__((aligned(16))) u32x4 ring_a[kStages][kAUnits];
     __shared__ __attribute__((aligned(16))) u32x4 ring_b[kStages][kBUnits];
+    // s_x of the tile's 256 rows and s_w of its 128 outputs (+128 unused),
+    // double-buffered by tile
+    __shared__ __attribute__((aligned(16))) float sscale[2][kBM + 2 * kBN];
 
     const int64_t row_bytes = d_in / 2;
     const int nk = static_cast<int>((row_bytes + kKBP - 1) / kKBP);
@@ -220,27 +225,54 @@ __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
         mfma16(w1);
     };
 
+    // s_x / s_w of a tile into its scale slot: 64 dwords per wave
+    // instruction (rows / outputs past the end load the last one; their
+    // outputs are never stored).  Issued before the tile's first operand
+    // step, so waiting for that step covers them.
+    auto issue_scales = [&](const GemmTile& tl, int slot) {
+        const int64_t r = tl.m0 + 64 * wave + lane;
+        dma4(s_x, static_cast<uint32_t>((r < n ? r : n - 1) * 4),
+             lds_addr(&sscale[slot][64 * wave]));
+        if (wave < 2) {
+            const int64_t o = tl.n0 + 64 * wave + lane;
+            dma4(s_w, static_cast<uint32_t>((o < d_out ? o : d_out - 1) * 4),
+                 lds_addr(&sscale[slot][kBM + 64 * wave]));
+        }
+    };
+
+    // The operand steps of consecutive tiles form one stream through the
+    // ring: during a tile's last steps the first steps of the next tile
+    // (and its scales) are already requested, and they have landed before
+    // the tile's output is stored, so the next tile starts without waiting
+    // behind those stores.
     GemmTile cur;
     if (!gemm_tile(0, n, d_out, cur)) return;
+    const int pre_n = nk < kStages - 1 ? nk : kStages - 1;   // steps requested ahead of a tile
+    int sp = 0;      // scale slot of the current tile
+    int base = 0;    // ring stage of the current tile's step 0
     set_rows(cur);
-#pragma unroll
-    for (int st = 0; st < kStages - 1; ++st)
-        if (st < nk) issue(st, st);
+    issue_scales(cur, sp);
+    for (int j = 0; j < pre_n; ++j) issue(j, j);
+    wait_vmcnt<0>();
+    lds_barrier();
 
     for (int64_t k = 0;; ++k) {
 #pragma unroll
         for (int i = 0; i < 4; ++i)
 #pragma unroll
             for (int j = 0; j < 2; ++j) acc[i][j] = i32x16{};
+        GemmTile nxt;
+        const bool more = gemm_tile(k + 1, n, d_out, nxt);
+        int nx_issued = 0;   // steps of the next tile requested so far
 
         for (int kt = 0; kt < nk; ++kt) {
-            // this thread's loads for step kt are done once at most the loads
-            // of the later steps already in flight remain outstanding
-            const int ahead = nk - 1 - kt < kStages - 2 ? nk - 1 - kt : kStages - 2;
-            if (ahead >= 2) wait_vmcnt<2 * kLoadsPerStep>();
-            else if (ahead == 1) wait_vmcnt<kLoadsPerStep>();
-            else wait_vmcnt<0>();
-            const int st = kt % kStages;
+            const int st = (base + kt) % kStages;
+            if (kt >= pre_n) {
+                // this thread's loads of step kt have landed once at most the
+                // loads of the one step requested after it are outstanding
+                if (kt + 1 < nk || more) wait_vmcnt<kLoadsPerStep>();
+                else wait_vmcnt<0>();
+            }
             if (kt == nk - 1 && (row_bytes % kKBP) != 0) {
                 // ragged last step: codes past d_in read garbage; zero them in
                 // A (each thread clears the slots its own loads filled)
@@ -250,36 +282,47 @@ __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
                         ring_a[st][(q * 4 + wave) * 64 + lane] = u32x4{0u, 0u, 0u, 0u};
             }
             lds_barrier();     // all threads' loads of step kt landed; step kt-1 consumed
-            if (kt + kStages - 1 < nk) issue(kt + kStages - 1, (kt + kStages - 1) % kStages);
+            const int tgt = kt + kStages - 1;
+            if (tgt < nk) {
+                issue(tgt, (base + tgt) % kStages);
+            } else if (more && tgt - nk < pre_n) {
+                const int j = tgt - nk;
+                if (j == 0) {
+                    set_rows(nxt);
+                    issue_scales(nxt, sp ^ 1);
+                }
+                issue(j, (base + nk + j) % kStages);
+                nx_issued = j + 1;
+            }
             compute(st);
         }
-        lds_barrier();     // every stage consumed before the next tile refills it
-
-        GemmTile nxt;
-        const bool more = gemm_tile(k + 1, n, d_out, nxt);
         if (more) {
-            set_rows(nxt);
-#pragma unroll
-            for (int st = 0; st < kStages - 1; ++st)
-                if (st < nk) issue(st, st);
+            for (int j = nx_issued; j < pre_n; ++j) {   // only when nk < kStages - 1
+                if (j == 0) {
+                    set_rows(nxt);
+                    issue_scales(nxt, sp ^ 1);
+                }
+                issue(j, (base + nk + j) % kStages);
+            }
+            wait_vmcnt<0>();   // the next tile's first steps and scales have landed
         }
+        lds_barrier();         // stages of this tile consumed; next tile's first steps visible
 
-        // ---- epilogue: lane holds column n0 + wn*128 + 32j + l32 and rows
+        // ---- epilogue: lane holds column n0 + wn*64 + 32j + l32 and rows
         // m0 + wm*128 + 32i + 8(r/4) + 4h + r%4
+        const float* sc = sscale[sp];
         float sw[2];
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int64_t o = cur.n0 + wn * 64 + j * 32 + l32;
-            sw[j] = o < d_out ? s_w[o] : 0.0f;
-        }
+        for (int j = 0; j < 2; ++j) sw[j] = sc[kBM + wn * 64 + j * 32 + l32];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int64_t tb = cur.m0 + wm * 128 + i * 32 + 4 * h;
             float sx[16];
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int64_t t = tb + 8 * (r >> 2) + (r & 3);
-                sx[r] = t < n ? s_x[t] : 0.0f;
+            for (int q = 0; q < 4; ++q) {
+                const f32x4 v = *reinterpret_cast<const f32x4*>(sc + wm * 128 + i * 32 + 8 * q + 4 * h);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) sx[4 * q + e] = v[e];
             }
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
@@ -298,6 +341,8 @@ __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
         }
         if (!more) break;
         cur = nxt;
+        sp ^= 1;
+        base = (base + nk) % kStages;
     }
 }
 

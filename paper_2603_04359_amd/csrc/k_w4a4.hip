@@ -4,14 +4,14 @@
 //
 // gfx950 int8 MFMA (v_mfma_i32_32x32x32_i8) on INT4 codes.
 //
-// Tiles: 256 x 128 outputs per workgroup of 256 threads = 4 waves in a
-// 2 x 2 grid, each wave 128 x 64 = 4 x 2 MFMA tiles with int32
-// accumulators; two workgroups are resident per CU, so one workgroup's
-// barrier waits and output stores overlap the other's MFMAs.  One K step
-// covers 128 codes (64 packed bytes per row).
+// Tiles: 256 x 256 outputs per workgroup of 512 threads = 8 waves in a
+// 2 x 4 grid, each wave 128 x 64 = 4 x 2 MFMA tiles with int32
+// accumulators; one workgroup per CU (two waves per SIMD, 132 KiB of LDS).
+// One K step covers 128 codes (64 packed bytes per row); a tile reads
+// 32 KiB of packed codes per step.
 //
 // Operand path: packed INT4 tiles go straight from global memory into an
-// LDS ring of kStages steps with global_load_lds_dwordx4 (no register
+// LDS ring of kStages (4) steps with global_load_lds_dwordx4 (no register
 // staging, no LDS store instructions), issued kStages-1 steps ahead of
 // use, with one barrier per step that waits for LDS traffic only (a plain
 // workgroup barrier would also drain the loads in flight).  Each lane reads
@@ -25,10 +25,14 @@
 // by 8 recovers acc exactly for d_in <= 131072.
 //
 // LDS layout: each operand stage is rows x 4 units of 16 bytes; unit u of
-// row r sits at slot 4r + (u ^ swz(r)), which keeps 16- and 32-lane groups
-// of fragment reads (32 consecutive rows, one unit) free of bank
-// conflicts.  The direct loads fill 64 consecutive slots per wave
-// instruction, so each lane loads the global unit that belongs in its slot
+// row r sits at slot 4r + (u ^ swz(r)), with swz(r) built from bits 2 and 3
+// of r.  A fragment read covers 32 consecutive rows at one unit (lanes
+// 0-31) and the same rows at unit u ^ 2 (lanes 32-63).  Rows r, r+4, r+8,
+// r+12 get four different swz values, and swz(r+4) always differs from
+// swz(r) in bit 0, so both 16 consecutive lanes and lanes {i..i+7} with
+// {i+32..i+39} land on 16 distinct 16-byte bank groups of a 64-bank LDS.
+// The direct loads fill 64 consecutive slots per wave instruction, so each
+// lane loads the global unit that belongs in its slot
 // (a permutation inside each 64-byte row segment).  Rows past the end of a
 // matrix load a clamped in-bounds row (their outputs are never stored);
 // units past d_in in a ragged last step load any in-bounds unit and the
@@ -48,23 +52,24 @@
 
 namespace catk {
 
-constexpr int kGemmThreads = 256;
+constexpr int kGemmWaves = 8;
+constexpr int kGemmThreads = kGemmWaves * 64;
 constexpr int kBM = 256;           // tokens per tile
-constexpr int kBN = 128;           // outputs per tile
+constexpr int kBN = 256;           // outputs per tile
 constexpr int kKBP = 64;           // packed bytes per row per K step (128 codes)
 constexpr int kUP = kKBP / 16;     // 16-byte units per row per step
-constexpr int kStages = 3;         // LDS ring depth (steps)
+constexpr int kStages = 4;         // LDS ring depth (steps)
 constexpr int kAUnits = kBM * kUP;                   // A units per stage
 constexpr int kBUnits = kBN * kUP;                   // B units per stage
 constexpr int kLoadsA = kAUnits / kGemmThreads;      // direct loads per thread, A
 constexpr int kLoadsB = kBUnits / kGemmThreads;      // direct loads per thread, B
-constexpr int kWgPerCu = 2;
+constexpr int kWgPerCu = 1;
+static_assert(kStages >= 2 && kStages <= 4, "waits cover at most 2 steps ahead");
 constexpr int kGroupM = 4;         // row panels per tile group
 constexpr int kXcd = 8;
 
 __device__ __forceinline__ int gemm_swz(int r) {
-    const int q = r & 31;
-    return ((q >> 2) ^ (q >> 4)) & 3;
+    return ((r >> 2) & 1) | ((((r >> 2) ^ (r >> 3)) & 1) << 1);
 }
 
 struct GemmTile {
@@ -103,9 +108,8 @@ __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
     int64_t d_out, float* __restrict__ y, int32_t* __restrict__ acc_out) {
     __shared__ __attribute__((aligned(16))) u32x4 ring_a[kStages][kAUnits];
     __shared__ __attribute__((aligned(16))) u32x4 ring_b[kStages][kBUnits];
-    // s_x of the tile's 256 rows and s_w of its 128 outputs (+128 unused),
-    // double-buffered by tile
-    __shared__ __attribute__((aligned(16))) float sscale[2][kBM + 2 * kBN];
+    // s_x of the tile's rows and s_w of its outputs, double-buffered by tile
+    __shared__ __attribute__((aligned(16))) float sscale[2][kBM + kBN];
 
     const int64_t row_bytes = d_in / 2;
     const int nk = static_cast<int>((row_bytes + kKBP - 1) / kKBP);
@@ -113,65 +117,74 @@ __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
     const int wave = tid / kWave;
-    const int wm = wave >> 1, wn = wave & 1;   // 2 x 2 waves, each 128 x 64
+    const int wm = wave >> 2, wn = wave & 3;   // 2 x 4 waves, each 128 x 64
     const int l32 = lane & 31;
     const int h = lane >> 5;
 
     // Direct loads: instruction q of wave w fills slots [64 I, 64 I + 64)
-    // with I = q * 4 + w; slot s holds row s / 4, logical unit
-    // (s % 4) ^ swz(row).  32-bit offsets from the tile's first row.
+    // with I = q * 8 + w (16 rows of 64 bytes); slot s holds row s / 4,
+    // logical unit (s % 4) ^ swz(row).  32-bit offsets from the tile's
+    // first row.
     const uint8_t* a_base = qx;
     const uint8_t* b_base = qw;
     uint32_t a_off[kLoadsA], b_off[kLoadsB];
-    int ua_off[kLoadsA], ub_off[kLoadsB];
-#pragma unroll
-    for (int q = 0; q < kLoadsA; ++q) {
-        const int s = (q * 4 + wave) * 64 + lane;
-        ua_off[q] = ((s % kUP) ^ gemm_swz(s / kUP)) * 16;
-    }
-#pragma unroll
-    for (int q = 0; q < kLoadsB; ++q) {
-        const int s = (q * 4 + wave) * 64 + lane;
-        ub_off[q] = ((s % kUP) ^ gemm_swz(s / kUP)) * 16;
-    }
+    // the byte offset of a thread's unit inside its row segment is the same
+    // for every load q (64 slots per instruction keep row / 8 and slot % 8)
+    const int u_off = ((lane % kUP) ^ gemm_swz((wave * 64 + lane) / kUP)) * 16;
+    static_assert((64 / kUP) % 16 == 0, "swz(row) must not depend on the instruction");
     auto set_rows = [&](const GemmTile& tl) {
         a_base = qx + tl.m0 * row_bytes;
         b_base = qw + tl.n0 * row_bytes;
 #pragma unroll
         for (int q = 0; q < kLoadsA; ++q) {
-            const int r = ((q * 4 + wave) * 64 + lane) / kUP;
+            const int r = ((q * kGemmWaves + wave) * 64 + lane) / kUP;
             const int64_t ra = tl.m0 + r < n ? r : n - 1 - tl.m0;   // clamped rows: never stored
             a_off[q] = static_cast<uint32_t>(ra * row_bytes);
         }
 #pragma unroll
         for (int q = 0; q < kLoadsB; ++q) {
-            const int r = ((q * 4 + wave) * 64 + lane) / kUP;
+            const int r = ((q * kGemmWaves + wave) * 64 + lane) / kUP;
             const int64_t rb = tl.n0 + r < d_out ? r : d_out - 1 - tl.n0;
             b_off[q] = static_cast<uint32_t>(rb * row_bytes);
         }
     };
+    // LDS byte addresses of this wave's first slot in stage 0 (wave-uniform)
+    const uint32_t lds_a0 = static_cast<uint32_t>(
+        __builtin_amdgcn_readfirstlane(lds_addr(&ring_a[0][wave * 64])));
+    const uint32_t lds_b0 = static_cast<uint32_t>(
+        __builtin_amdgcn_readfirstlane(lds_addr(&ring_b[0][wave * 64])));
     auto issue = [&](int kt, int st) {
         const int64_t k0 = static_cast<int64_t>(kt) * kKBP;
+        const uint32_t la = lds_a0 + static_cast<uint32_t>(st) * (kAUnits * 16);
+        const uint32_t lb = lds_b0 + static_cast<uint32_t>(st) * (kBUnits * 16);
+        if (k0 + kKBP <= row_bytes) {
+            const uint32_t k0u = static_cast<uint32_t>(k0);
 #pragma unroll
-        for (int q = 0; q < kLoadsA; ++q) {
-            int64_t col = k0 + ua_off[q];
-            col = col < row_bytes ? col : 0;     // past the row end: any in-bounds unit
-            dma16(a_base, a_off[q] + static_cast<uint32_t>(col),
-                  lds_addr(&ring_a[st][(q * 4 + wave) * 64]));
-        }
+            for (int q = 0; q < kLoadsA; ++q)
+                dma16(a_base, a_off[q] + k0u + u_off, la + q * (kGemmWaves * 1024u));
 #pragma unroll
-        for (int q = 0; q < kLoadsB; ++q) {
-            int64_t col = k0 + ub_off[q];
-            col = col < row_bytes ? col : 0;
-            dma16(b_base, b_off[q] + static_cast<uint32_t>(col),
-                  lds_addr(&ring_b[st][(q * 4 + wave) * 64]));
+            for (int q = 0; q < kLoadsB; ++q)
+                dma16(b_base, b_off[q] + k0u + u_off, lb + q * (kGemmWaves * 1024u));
+        } else {
+#pragma unroll
+            for (int q = 0; q < kLoadsA; ++q) {
+                int64_t col = k0 + u_off;
+                col = col < row_bytes ? col : 0;     // past the row end: any in-bounds unit
+                dma16(a_base, a_off[q] + static_cast<uint32_t>(col), la + q * (kGemmWaves * 1024u));
+            }
+#pragma unroll
+            for (int q = 0; q < kLoadsB; ++q) {
+                int64_t col = k0 + u_off;
+                col = col < row_bytes ? col : 0;
+                dma16(b_base, b_off[q] + static_cast<uint32_t>(col), lb + q * (kGemmWaves * 1024u));
+            }
         }
     };
     constexpr int kLoadsPerStep = kLoadsA + kLoadsB;
 
     i32x16 acc[4][2];
 
-    // Fragments: lane half h reads logical units 2h and 2h+1 (c2 = 0, 1) of
+    // Fragments: lane half h reads logical units 2h and 2h+1 (c = 0, 1) of
     // its row; each unit feeds two MFMA steps (its low and high 8 bytes).
     // Both operands use the same assignment, so the reduction index is only
     // permuted.
@@ -181,8 +194,8 @@ __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
     struct Wide {
         i32x4 a[4], b[2];
     };
-    auto read_packed = [&](Packed& p, int st, int c2) {
-        const int u = 2 * h + c2;
+    auto read_packed = [&](Packed& p, int st, int c) {
+        const int u = 2 * h + c;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int r = wm * 128 + i * 32 + l32;
@@ -209,18 +222,21 @@ __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
                                                                  0);
     };
     // one K step = 4 MFMA steps of 32 codes; the widening of MFMA step
-    // c+1 is issued before the 16 MFMAs of step c
+    // m+1 is issued before the 16 MFMAs of step m
     auto compute = [&](int st) {
         Packed p;
         Wide w0, w1;
         read_packed(p, st, 0);
         widen(w0, p, 0);
         widen(w1, p, 1);
-        read_packed(p, st, 1);
-        mfma16(w0);
-        widen(w0, p, 0);
-        mfma16(w1);
-        widen(w1, p, 1);
+#pragma unroll
+        for (int c = 1; c < kUP / 2; ++c) {
+            read_packed(p, st, c);
+            mfma16(w0);
+            widen(w0, p, 0);
+            mfma16(w1);
+            widen(w1, p, 1);
+        }
         mfma16(w0);
         mfma16(w1);
     };
@@ -230,13 +246,14 @@ __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
     // outputs are never stored).  Issued before the tile's first operand
     // step, so waiting for that step covers them.
     auto issue_scales = [&](const GemmTile& tl, int slot) {
-        const int64_t r = tl.m0 + 64 * wave + lane;
-        dma4(s_x, static_cast<uint32_t>((r < n ? r : n - 1) * 4),
-             lds_addr(&sscale[slot][64 * wave]));
-        if (wave < 2) {
-            const int64_t o = tl.n0 + 64 * wave + lane;
+        if (wave < 4) {
+            const int64_t r = tl.m0 + 64 * wave + lane;
+            dma4(s_x, static_cast<uint32_t>((r < n ? r : n - 1) * 4),
+                 lds_addr(&sscale[slot][64 * wave]));
+        } else {
+            const int64_t o = tl.n0 + 64 * (wave - 4) + lane;
             dma4(s_w, static_cast<uint32_t>((o < d_out ? o : d_out - 1) * 4),
-                 lds_addr(&sscale[slot][kBM + 64 * wave]));
+                 lds_addr(&sscale[slot][kBM + 64 * (wave - 4)]));
         }
     };
 
@@ -270,7 +287,11 @@ __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
             if (kt >= pre_n) {
                 // this thread's loads of step kt have landed once at most the
                 // loads of the one step requested after it are outstanding
-                if (kt + 1 < nk || more) wait_vmcnt<kLoadsPerStep>();
+                const int last = nk - 1 + (more ? pre_n : 0);   // last step requested in this tile
+                const int issued = kt + kStages - 2 < last ? kt + kStages - 2 : last;
+                const int ahead = issued - kt;
+                if (ahead >= 2) wait_vmcnt<2 * kLoadsPerStep>();
+                else if (ahead == 1) wait_vmcnt<kLoadsPerStep>();
                 else wait_vmcnt<0>();
             }
             if (kt == nk - 1 && (row_bytes % kKBP) != 0) {
@@ -278,15 +299,17 @@ __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
                 // A (each thread clears the slots its own loads filled)
 #pragma unroll
                 for (int q = 0; q < kLoadsA; ++q)
-                    if (static_cast<int64_t>(kt) * kKBP + ua_off[q] >= row_bytes)
-                        ring_a[st][(q * 4 + wave) * 64 + lane] = u32x4{0u, 0u, 0u, 0u};
+                    if (static_cast<int64_t>(kt) * kKBP + u_off >= row_bytes)
+                        ring_a[st][(q * kGemmWaves + wave) * 64 + lane] = u32x4{0u, 0u, 0u, 0u};
             }
             lds_barrier();     // all threads' loads of step kt landed; step kt-1 consumed
             const int tgt = kt + kStages - 1;
             if (tgt < nk) {
                 issue(tgt, (base + tgt) % kStages);
-            } else if (more && tgt - nk < pre_n) {
-                const int j = tgt - nk;
+            } else if (more && nx_issued < pre_n && nx_issued <= tgt - nk) {
+                // the next tile's steps, in order; step j's stage last held
+                // this tile's step nk + j - kStages <= kt - 1 (consumed)
+                const int j = nx_issued;
                 if (j == 0) {
                     set_rows(nxt);
                     issue_scales(nxt, sp ^ 1);

@@ -82,11 +82,8 @@ extern "C" int cat_cov_accumulate(const void* X, int x_dtype, int64_t n, int64_t
 }
 
 extern "C" size_t cat_transform_quant_workspace_bytes(int64_t n, int64_t d, int64_t k) {
-    (void)d;
-    (void)k;
-    if (n < 1) return 0;
-    // one 32-bit running maximum per token, rounded up to 256 bytes
-    return static_cast<size_t>((n * 4 + 255) / 256 * 256);
+    if (n < 1 || d < 1) return 0;
+    return catk::tq_workspace_bytes(n, d, k);
 }
 
 extern "C" int cat_transform_quant(const void* X, int x_dtype, int64_t n, int64_t d, const void* T,

@@ -23,6 +23,8 @@
 // the per-token maximum is a register max plus one lane swap, and codes are
 // packed 4 per lane, joined to 8 per dword with one lane swap.
 // fp32 (or small-k) path: plain fp32 FMA chains on the vector ALU.
+#include <atomic>
+
 #include "device_common.h"
 #include "kernels.h"
 
@@ -399,6 +401,333 @@ __global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
     }
 }
 
+// ------------------------------------------------- single-pass variant
+// bf16, k = 128, d = 4096 (32 blocks), one launch, X read once.  One
+// workgroup per CU owns block b for the token tiles r, r + R, ... (a tile is
+// 64 tokens) and splits its eight waves by role:
+//   waves 0-3  compute: wave w multiplies rows 32w .. 32w + 31 of T_b (held
+//              in registers) with every token of the tile, read from LDS;
+//   waves 4-5  copy: stream token tiles into an 8-stage LDS ring with
+//              global_load_lds_dwordx4, seven tiles ahead;
+//   wave 6     gather: reads the per-token maxima other workgroups published;
+//   wave 7     publish: writes this workgroup's per-token maxima.
+// Each wave issues one kind of vector-memory traffic only, so every wait is
+// exact and no load waits for a store's acknowledgement: the copy waves
+// count their own copies, and the compiler tracks the loads of the gather
+// wave (stores of the others are never waited for).
+//
+// The row maximum of a token needs all 32 blocks, exchanged in two levels
+// through the workspace: every workgroup publishes its block maxima P(b, t)
+// of a tile; workgroup b owns tokens 2b, 2b + 1 of the tile, reduces their
+// 32 P words and has the row maximum F(t) published; every workgroup then
+// reads F of the tile's 64 tokens (1 KiB of reads per workgroup and tile
+// per level instead of 16 KiB for all P words).  A word is
+// (call tag << 32) | maximum bits written with one store, so a reader sees
+// either an old word (another tag) or the whole new one and the workspace
+// needs no clearing between calls.  Tags have bit 31 set, which no
+// absolute-value float pattern has, so 32-bit maxima left by the two-pass
+// path never look published either.  P(j, t) lives at
+// ((t / 16) * 32 + j) * 16 + t % 16 (16 tokens of a block fill one 128-byte
+// line), F(t) at 32 n' + t.
+//
+// Step s has barriers A and F.  A to F: the compute waves multiply tile s
+// and leave per-wave maxima in LDS; the gather wave takes F of tile s-3
+// (requested one phase earlier) and requests P of tile s-1; the publish
+// wave writes F of tile s-2.  F to the next A: the compute waves quantize
+// tile s-3 from the accumulators they kept (four sets rotate); the publish
+// wave writes P of tile s; the gather wave reduces P of tile s-1 and
+// requests F of tile s-2.  Every device crossing thus has about a step.
+// Rows of T_b are permuted inside each 32-row MFMA group so that lane
+// (token, h) accumulates 16 consecutive output channels: its codes are 8
+// contiguous bytes, no cross-lane exchange.
+//
+// Progress: the grid never exceeds the device's resident capacity (see
+// launch_tq_fused) and every workgroup of a token-tile row visits its tiles
+// in the same order, so a workgroup only waits for peers that are running
+// or about to run.  Waits are still bounded: after kTqSpinLimit polls the
+// gather wave records a timeout flag and goes on.
+constexpr uint32_t kTqSpinLimit = 1u << 22;
+constexpr int kFqCompute = 4;                   // compute waves
+constexpr int kFqCopy = 2;                      // copy waves
+constexpr int kFqThreads = (kFqCompute + kFqCopy + 2) * kWave;
+constexpr int kFqStages = 8;
+constexpr int kFqTT = 64;                       // tokens per tile
+constexpr int kFqU = 16;                        // 16-byte units per token row
+constexpr int kFqStage = kFqTT * kFqU;          // units per stage (16 KiB)
+constexpr int kFqCopyOps = kFqStage / (kFqCopy * kWave);   // copies per lane per tile
+constexpr int kFqBlocks = 32;                   // d / 128
+constexpr int kFqLag = 3;                       // tile s is quantized in step s + kFqLag
+static_assert(kFqCopyOps * (kFqStages - 2) < 64, "copies in flight must fit the vmcnt range");
+static_assert(kFqTT == 2 * kFqBlocks, "each workgroup reduces two tokens of a tile");
+
+struct TqFusedWs {
+    uint64_t* pmax;       // P words, then F words (see above)
+    uint32_t* flag;       // timeout flag (0 = fine)
+};
+
+// MFMA row i of a 32-row group -> output row within the group
+__device__ __forceinline__ int fq_row(int i) {
+    return ((i >> 2) & 1) * 16 + (i >> 3) * 4 + (i & 3);
+}
+
+// Low bytes of four words -> one word, byte j from word j.
+__device__ __forceinline__ uint32_t fq_bytes(uint32_t b0, uint32_t b1, uint32_t b2, uint32_t b3) {
+    return __builtin_amdgcn_perm(b1, b0, 0x0C0C0400u) | __builtin_amdgcn_perm(b3, b2, 0x04000C0Cu);
+}
+
+// 16 accumulators (consecutive output channels) -> 16 INT4 codes, channel
+// 2m in the low nibble of byte m.  u = fl(z * inv) is clamped to [-7, 7]
+// and rounded to nearest even by adding 1.5 * 2^23 (exact for |u| < 2^22),
+// which leaves the integer in the low mantissa bits, two's complement.
+__device__ __forceinline__ u32x2 fq_quant16(const f32x16& z, float inv) {
+    uint32_t w[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        float u = z[r] * inv;
+        u = __builtin_amdgcn_fmed3f(u, -kQmax4, kQmax4);
+        w[r] = __float_as_uint(u + 12582912.0f);
+    }
+    u32x2 out;
+#pragma unroll
+    for (int hw = 0; hw < 2; ++hw) {
+        const uint32_t* v = w + 8 * hw;
+        const uint32_t ev = fq_bytes(v[0], v[2], v[4], v[6]);
+        const uint32_t od = fq_bytes(v[1], v[3], v[5], v[7]);
+        out[hw] = (ev & 0x0F0F0F0Fu) | ((od << 4) & 0xF0F0F0F0u);
+    }
+    return out;
+}
+
+// max |z| over 16 values, as float bits.  Read as signed ints, the largest
+// value is the largest positive (or, with none, the largest-magnitude
+// negative); read as unsigned, it is the largest-magnitude negative (or,
+// with none, the largest positive).  The answer is the larger magnitude of
+// the two.
+__device__ __forceinline__ uint32_t fq_absmax16(const f32x16& z) {
+    int32_t mi = static_cast<int32_t>(__float_as_uint(z[0]));
+    uint32_t mu = __float_as_uint(z[0]);
+#pragma unroll
+    for (int r = 1; r < 15; r += 2) {
+        const uint32_t a = __float_as_uint(z[r]), c = __float_as_uint(z[r + 1]);
+        mi = max(mi, max(static_cast<int32_t>(a), static_cast<int32_t>(c)));
+        mu = max(mu, max(a, c));
+    }
+    mi = max(mi, static_cast<int32_t>(__float_as_uint(z[15])));
+    mu = max(mu, __float_as_uint(z[15]));
+    return max(static_cast<uint32_t>(mi) & 0x7FFFFFFFu, mu & 0x7FFFFFFFu);
+}
+
+// tile t has landed once at most `later` tiles of copies issued after it
+// are still in flight
+__device__ __forceinline__ void fq_wait_copies(int later) {
+    switch (later) {
+        case 0: wait_vmcnt<0>(); break;
+        case 1: wait_vmcnt<1 * kFqCopyOps>(); break;
+        case 2: wait_vmcnt<2 * kFqCopyOps>(); break;
+        case 3: wait_vmcnt<3 * kFqCopyOps>(); break;
+        case 4: wait_vmcnt<4 * kFqCopyOps>(); break;
+        case 5: wait_vmcnt<5 * kFqCopyOps>(); break;
+        default: wait_vmcnt<6 * kFqCopyOps>(); break;
+    }
+}
+
+__global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
+    const uint16_t* __restrict__ X, const uint16_t* __restrict__ T, int64_t n, int64_t d,
+    int64_t R, TqFusedWs ws, uint32_t tag, uint8_t* __restrict__ codes,
+    float* __restrict__ s_x) {
+    constexpr int K = 128;
+    constexpr int NS = K / 16;          // 16-deep MFMA steps
+    constexpr int NSB = kFqTT / 32;     // 32-token subtiles
+    __shared__ __attribute__((aligned(16))) u32x4 ring[kFqStages][kFqStage];
+    __shared__ uint32_t red[kFqCompute][kFqTT];   // per-wave maxima of the step's tile
+    __shared__ uint32_t gat[kFqTT];               // row maxima of the tile being quantized
+    __shared__ uint32_t fred[2][2];               // reduced row maxima of the owned tokens
+
+    const int64_t b = blockIdx.x % kFqBlocks;
+    const int64_t r0 = blockIdx.x / kFqBlocks;
+    const int64_t ntiles = (n + kFqTT - 1) / kFqTT;
+    if (r0 >= ntiles) return;           // never taken: the launcher sizes R <= ntiles
+    const int64_t nt = (ntiles - r0 + R - 1) / R;
+    const int64_t nsteps = nt + kFqLag;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    auto tile0 = [&](int64_t it) { return (r0 + it * R) * kFqTT; };   // first token
+
+    if (wave >= kFqCompute + kFqCopy) {
+        // ------------------------------------------ gather / publish waves
+        // The gather wave only loads and the publish wave only stores, so
+        // a wait for a load never includes a store's acknowledgement.
+        const uint64_t hi = static_cast<uint64_t>(tag) << 32;
+        const int64_t n16 = (n + 15) / 16 * 16;
+        uint64_t* const fw = ws.pmax + n16 * kFqBlocks;
+        auto clampt = [&](int64_t t) { return t < n ? t : n - 1; };
+        auto p_word = [&](int64_t t, int64_t j) {
+            return ws.pmax + (t >> 4) * (kFqBlocks * 16) + j * 16 + (t & 15);
+        };
+        auto store = [&](uint64_t* a, uint32_t m) {
+            __hip_atomic_store(a, hi | m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        };
+        if (wave == kFqCompute + kFqCopy + 1) {
+            // publish: F of tile it-2 (reduced in the last step), P of tile it
+            for (int64_t it = 0; it < nsteps; ++it) {
+                lds_barrier();                                        // A
+                if (it >= 2 && it - 2 < nt) {
+                    const int64_t t = tile0(it - 2) + 2 * b + (lane >> 5);
+                    if ((lane & 31) == 0 && t < n) store(fw + t, fred[it & 1][lane >> 5]);
+                }
+                lds_barrier();                                        // F
+                if (it < nt) {
+                    const int64_t t = tile0(it) + lane;
+                    uint32_t mm = red[0][lane];
+#pragma unroll
+                    for (int w = 1; w < kFqCompute; ++w) mm = max(mm, red[w][lane]);
+                    if (t < n) store(p_word(t, b), mm);
+                }
+            }
+            return;
+        }
+        // gather: takes F of tile it-3 after A, then requests P of tile
+        // it-1; takes P after F and reduces it, then requests F of tile
+        // it-2.  Every read has a phase in flight, and only one read is
+        // outstanding when it is waited for.  A word that is not there yet
+        // is re-read (bounded).
+        auto load = [&](const uint64_t* a) {
+            return __hip_atomic_load(a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        };
+        auto await = [&](uint64_t v, const uint64_t* a) {
+            for (uint32_t polls = 0; (v >> 32) != tag;) {
+                if (++polls >= kTqSpinLimit) {
+                    __hip_atomic_store(ws.flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
+                v = load(a);
+            }
+            return static_cast<uint32_t>(v);
+        };
+        // F(token lane of tile j); P(block lane % 32, token 2b + lane / 32 of tile j)
+        auto f_addr = [&](int64_t j) { return fw + clampt(tile0(j) + lane); };
+        auto p_addr = [&](int64_t j) {
+            return p_word(clampt(tile0(j) + 2 * b + (lane >> 5)), lane & 31);
+        };
+        uint64_t fv = 0, pv = 0;
+        for (int64_t it = 0; it < nsteps; ++it) {
+            lds_barrier();                                            // A
+            if (it >= kFqLag) {
+                const int64_t t = tile0(it - kFqLag) + lane;
+                const uint32_t m = await(fv, f_addr(it - kFqLag));
+                gat[lane] = m;
+                if (b == 0 && t < n) s_x[t] = __fdiv_rn(__uint_as_float(m), kQmax4);
+            }
+            if (it >= 1 && it <= nt) pv = load(p_addr(it - 1));
+            lds_barrier();                                            // F
+            if (it >= 1 && it <= nt) {
+                uint32_t m = await(pv, p_addr(it - 1));
+#pragma unroll
+                for (int x = 1; x < 32; x <<= 1)
+                    m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), x)));
+                if ((lane & 31) == 0) fred[(it + 1) & 1][lane >> 5] = m;
+            }
+            if (it + 1 >= kFqLag && it + 1 < nsteps) fv = load(f_addr(it + 1 - kFqLag));
+        }
+        return;
+    }
+
+    if (wave >= kFqCompute) {
+        // ---------------------------------------------------- copy waves
+        const int cw = wave - kFqCompute;
+        auto issue = [&](int64_t it) {
+            const int64_t t0 = tile0(it);
+            const uint16_t* base = X + t0 * d + b * K;
+            const int64_t last = n - 1 - t0;
+            const int st = static_cast<int>(it % kFqStages);
+#pragma unroll
+            for (int q = 0; q < kFqCopyOps; ++q) {
+                const int first = (cw * kFqCopyOps + q) * kWave;   // first slot of this copy
+                const int sl = first + lane;
+                int rr = sl / kFqU;
+                const int u = (sl % kFqU) ^ tq_xswz<K>(rr);
+                rr = rr <= last ? rr : static_cast<int>(last);
+                dma16(base, static_cast<uint32_t>((rr * d + u * 8) * 2), lds_addr(&ring[st][first]));
+            }
+        };
+        for (int64_t it = 0; it < nt && it < kFqStages - 1; ++it) issue(it);
+        for (int64_t it = 0; it < nsteps; ++it) {
+            if (it < nt) {
+                const int64_t hi_t = nt - 1 < it + kFqStages - 2 ? nt - 1 : it + kFqStages - 2;
+                fq_wait_copies(static_cast<int>(hi_t - it));
+            }
+            lds_barrier();                                            // A
+            // the stage of tile it + 7 held tile it - 1, read before A
+            if (it + kFqStages - 1 < nt) issue(it + kFqStages - 1);
+            lds_barrier();                                            // F
+        }
+        return;
+    }
+
+    // ------------------------------------------------------ compute waves
+    const int l32 = lane & 31;
+    const int h = lane >> 5;
+    const int row0 = wave * 32;
+    u32x4 tf[NS];
+    {
+        const u32x4* tg = reinterpret_cast<const u32x4*>(T + (b * K + row0 + fq_row(l32)) * K);
+#pragma unroll
+        for (int s = 0; s < NS; ++s) tf[s] = tg[2 * s + h];
+    }
+    auto mfma = [&](int64_t it, f32x16 (&acc)[NSB]) {
+        const int st = static_cast<int>(it % kFqStages);
+#pragma unroll
+        for (int sb = 0; sb < NSB; ++sb) acc[sb] = f32x16{};
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+#pragma unroll
+            for (int sb = 0; sb < NSB; ++sb) {
+                const int rr = sb * 32 + l32;
+                const u32x4 xf = ring[st][rr * kFqU + ((2 * s + h) ^ tq_xswz<K>(rr))];
+                acc[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(tf[s]), as_bf16x8(xf),
+                                                                  acc[sb], 0, 0, 0);
+            }
+        }
+#pragma unroll
+        for (int sb = 0; sb < NSB; ++sb) {
+            uint32_t m = fq_absmax16(acc[sb]);
+            m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), 32)));
+            if (h == 0) red[wave][sb * 32 + l32] = m;
+        }
+    };
+    auto quant = [&](int64_t it, const f32x16 (&acc)[NSB]) {
+        const int64_t t0 = tile0(it);
+#pragma unroll
+        for (int sb = 0; sb < NSB; ++sb) {
+            const int64_t t = t0 + sb * 32 + l32;
+            const float amax = __uint_as_float(gat[sb * 32 + l32]);
+            const float inv = amax > 0.0f ? __fdiv_rn(kQmax4, amax) : 0.0f;
+            const u32x2 c = fq_quant16(acc[sb], inv);
+            if (t < n)
+                *reinterpret_cast<u32x2*>(codes + t * (d / 2) + b * (K / 2) + row0 / 2 + 8 * h) = c;
+        }
+    };
+    // step it: A, multiply tile it into cur, F, quantize tile it-3 from old
+    auto step = [&](int64_t it, f32x16 (&cur)[NSB], const f32x16 (&old)[NSB]) {
+        lds_barrier();                                                // A
+        if (it < nt) mfma(it, cur);
+        lds_barrier();                                                // F
+        if (it >= kFqLag) quant(it - kFqLag, old);
+    };
+    static_assert(kFqLag == 3, "four accumulator sets rotate");
+    f32x16 s0[NSB], s1[NSB], s2[NSB], s3[NSB];
+    for (int64_t it = 0; it < nsteps; it += 4) {
+        step(it, s0, s1);
+        if (it + 1 >= nsteps) break;
+        step(it + 1, s1, s2);
+        if (it + 2 >= nsteps) break;
+        step(it + 2, s2, s3);
+        if (it + 3 >= nsteps) break;
+        step(it + 3, s3, s0);
+    }
+}
+
 template <int K>
 hipError_t launch_tq_ring(const uint16_t* X, int64_t n, int64_t d, const uint16_t* T,
                           uint8_t* codes, float* s_x, uint32_t* ws, hipStream_t stream) {
@@ -424,6 +753,79 @@ hipError_t launch_tq_ring(const uint16_t* X, int64_t n, int64_t d, const uint16_
     return hipGetLastError();
 }
 
+// Workspace layout (bytes): [0, P) per-token words (two-pass path: one
+// 32-bit running maximum per token; single-pass path: d/128 64-bit tagged
+// block maxima and one tagged row maximum per token, n rounded up to 16,
+// P = 8 n' (max(1, d / 128) + 1)), then the 32-bit timeout flag.
+static int64_t tq_nbj_max(int64_t d) { return d / 128 > 1 ? d / 128 : 1; }
+static size_t tq_flag_offset(int64_t n, int64_t d) {
+    return static_cast<size_t>((n + 15) / 16 * 16 * 8 * (tq_nbj_max(d) + 1));
+}
+size_t tq_workspace_bytes(int64_t n, int64_t d, int64_t k) {
+    (void)k;
+    if (n < 1) return 0;
+    return tq_flag_offset(n, d) + 256;
+}
+
+static uint32_t next_tq_tag() {
+    static std::atomic<uint32_t> tag{0};
+    return 0x80000000u | (++tag & 0x7FFFFFFFu);
+}
+
+// Resident workgroups of tq_fused_kernel on a device (CUs x blocks per CU
+// by its register and LDS use), queried once per device.
+static hipError_t tq_fused_resident(int dev, int64_t& resident) {
+    constexpr int kMaxDev = 64;
+    static std::atomic<int64_t> cache[kMaxDev];   // 0 = not yet known
+    if (dev >= 0 && dev < kMaxDev) {
+        resident = cache[dev].load(std::memory_order_relaxed);
+        if (resident > 0) return hipSuccess;
+    }
+    int cus = 0, per_cu = 0;
+    hipError_t err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (err != hipSuccess) return err;
+    err = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, tq_fused_kernel, kFqThreads, 0);
+    if (err != hipSuccess) return err;
+    resident = static_cast<int64_t>(per_cu) * cus;
+    if (dev >= 0 && dev < kMaxDev && resident > 0) cache[dev].store(resident, std::memory_order_relaxed);
+    return hipSuccess;
+}
+
+// Single-pass launch (k = 128, d = 4096) when the grid (d/128
+// workgroups per token-tile row, as many rows as fit) can be resident all
+// at once; otherwise nothing is launched and the caller takes the two-pass
+// path.
+// The grid never exceeds the resident capacity, so every workgroup is on
+// the device together once other work has drained, and a peer a workgroup
+// waits for is always running or about to run.
+hipError_t launch_tq_fused(const uint16_t* X, int64_t n, int64_t d, const uint16_t* T,
+                           uint8_t* codes, float* s_x, uint8_t* ws, hipStream_t stream,
+                           bool& launched) {
+    launched = false;
+    int dev = 0;
+    hipError_t err = hipGetDevice(&dev);
+    if (err != hipSuccess) return err;
+    int64_t resident = 0;
+    err = tq_fused_resident(dev, resident);
+    if (err != hipSuccess) return err;
+    const int64_t nbj = d / 128;
+    const int64_t ntiles = (n + kFqTT - 1) / kFqTT;
+    if (nbj != kFqBlocks || nbj > resident) return hipSuccess;
+    int64_t R = resident / nbj;
+    if (R > ntiles) R = ntiles;
+    if (R < 1) R = 1;
+    TqFusedWs w;
+    w.pmax = reinterpret_cast<uint64_t*>(ws);
+    w.flag = reinterpret_cast<uint32_t*>(ws + tq_flag_offset(n, d));
+    const uint32_t tag = next_tq_tag();
+    hipLaunchKernelGGL(tq_fused_kernel, dim3(static_cast<uint32_t>(nbj * R)), dim3(kFqThreads),
+                       0, stream, X, T, n, d, R, w, tag, codes, s_x);
+    err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    launched = true;
+    return hipSuccess;
+}
+
 template <typename XT, typename TT>
 hipError_t launch_tq_generic(const XT* X, int64_t n, int64_t d, const TT* T, int64_t k,
                              uint8_t* codes, float* s_x, uint32_t* ws, hipStream_t stream) {
@@ -441,6 +843,13 @@ hipError_t launch_tq_generic(const XT* X, int64_t n, int64_t d, const TT* T, int
 hipError_t launch_transform_quant(const void* X, int x_bf16, int64_t n, int64_t d, const void* T,
                                   int t_bf16, int64_t k, uint8_t* codes, float* s_x,
                                   uint32_t* amax_ws, hipStream_t stream) {
+    if (x_bf16 && t_bf16 && k == 128) {
+        bool launched = false;
+        const hipError_t e = launch_tq_fused(static_cast<const uint16_t*>(X), n, d,
+                                             static_cast<const uint16_t*>(T), codes, s_x,
+                                             reinterpret_cast<uint8_t*>(amax_ws), stream, launched);
+        if (e != hipSuccess || launched) return e;
+    }
     hipLaunchKernelGGL(fill_zero_u32_kernel, dim3(static_cast<uint32_t>((n + 255) / 256)),
                        dim3(256), 0, stream, amax_ws, n);
     hipError_t err = hipGetLastError();

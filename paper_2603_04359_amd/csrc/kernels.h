@@ -17,7 +17,8 @@ hipError_t launch_sqnr(const float* y, const float* yt, int64_t count, double* p
                        double* out, hipStream_t stream);
 
 // ---- transform + quantize
-// amax_ws: n uint32 words of scratch.
+// amax_ws: tq_workspace_bytes(n, d, k) bytes of scratch.
+size_t tq_workspace_bytes(int64_t n, int64_t d, int64_t k);
 hipError_t launch_transform_quant(const void* X, int x_bf16, int64_t n, int64_t d,
                                   const void* T, int t_bf16, int64_t k, uint8_t* codes,
                                   float* s_x, uint32_t* amax_ws, hipStream_t stream);

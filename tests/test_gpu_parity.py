@@ -190,6 +190,75 @@ def test_transform_quant_other_paths(x_dtype, t_dtype, k, n):
     _check_scales(s, s_or, f"{x_dtype}/{t_dtype} k={k}")
 
 
+# ------------------------------------------ single-pass transform+quant
+# k = 128 with d a multiple of 4096 runs the single-pass kernel, which
+# exchanges per-block row maxima between workgroups through the workspace.
+
+def _rand_T(d, k, seed):
+    rng = np.random.default_rng(seed)
+    return o.round_storage(rng.standard_normal((d // k, k, k)) / np.sqrt(k), "bf16")
+
+
+def _mlp_up_X(n, seed):
+    cfg = wl.get_config("mlp_up", n=n, n_cal=16)
+    return wl.make_layer(cfg, seed=seed, with_cal=False, with_weights=False)["X"].astype(np.float64)
+
+
+@pytest.mark.parametrize("n", [1, 300, 2049])
+def test_transform_quant_single_pass(n):
+    say(f"tq single pass d=4096 k=128 n={n}")
+    X = _mlp_up_X(n, seed=n)
+    if n > 1:
+        X[n // 2] = 0.0                           # a zero token row
+    T = _rand_T(4096, 128, seed=1)
+    codes, s = _tq_gpu(X, T, 128, "bf16", "bf16")
+    _, _, s_or = check_codes(codes, X, T, label=f"single pass n={n}")
+    _check_scales(s, s_or, f"single pass n={n}")
+    if n > 1:
+        assert s[n // 2] == 0 and not codes[n // 2].any()
+
+
+def test_transform_quant_single_pass_mlp_up_full_size():
+    # 8192 tokens x 4096 channels, the shape and launch the benchmark times
+    say("tq single pass mlp_up 8192 x 4096")
+    X = _mlp_up_X(8192, seed=0)
+    T = _rand_T(4096, 128, seed=2)
+    codes, s = _tq_gpu(X, T, 128, "bf16", "bf16")
+    _, _, s_or = check_codes(codes, X, T, label="mlp_up full")
+    _check_scales(s, s_or, "mlp_up full")
+
+
+def test_transform_quant_workspace_reuse_across_paths():
+    # One workspace through single-pass, two-pass and single-pass calls on
+    # different data: words left by earlier calls must never pass for the
+    # current call's.
+    say("tq workspace reuse: single pass / two pass / single pass")
+    torch = torch_mod()
+    n = 300
+    wsb = max(cat.cat_transform_quant_workspace_bytes(n, 4096, 128),
+              cat.cat_transform_quant_workspace_bytes(n, 1024, 128))
+    ws = torch.zeros(wsb, dtype=torch.uint8, device="cuda")
+    T4 = _rand_T(4096, 128, seed=3)
+    T1 = _rand_T(1024, 128, seed=4)
+    cases = [(_mlp_up_X(n, seed=10), T4), (_mlp_up_X(n, seed=11)[:, :1024].copy(), T1),
+             (_mlp_up_X(n, seed=12) * 2.0 ** -6, T4), (_mlp_up_X(n, seed=10), T4)]
+    first = None
+    for i, (X, T) in enumerate(cases):
+        d = X.shape[1]
+        codes = torch.empty((n, d // 2), dtype=torch.uint8, device="cuda")
+        s_x = torch.empty(n, dtype=torch.float32, device="cuda")
+        cat.cat_transform_quant(dev(X, "bf16"), dev(T, "bf16"), 128, codes, s_x, ws)
+        c, s = host(codes), host(s_x)
+        _, _, s_or = check_codes(c, X, T, label=f"reuse call {i}")
+        _check_scales(s, s_or, f"reuse call {i}")
+        if i == 0:
+            first = (c, s)
+    assert np.array_equal(first[0], c) and np.array_equal(first[1], s)
+    # the single-pass kernel's bounded waits record a timeout in the first
+    # word of the workspace's last 256 bytes; none may have happened
+    assert int(host(ws[wsb - 256:wsb - 252].view(torch.int32))[0]) == 0
+
+
 # ------------------------------------------------------- second moment
 def _cov_gpu(X, dtype, mode, k, acc0=None, splits=None):
     torch = torch_mod()
@@ -367,3 +436,19 @@ def test_inputs_at_addresses_with_bit31_set():
     ref_acc, _ = o.w4a4_linear(o.unpack_int4(codes), host(sx), qw, host(sw))
     assert np.array_equal(host(acc_i), ref_acc.astype(np.int32))
     del keep, keep2
+
+
+def test_single_pass_transform_quant_at_addresses_with_bit31_set():
+    say("tq single pass on inputs at addresses with bit 31 set")
+    torch = torch_mod()
+    n, d, k = 300, 4096, 128
+    X = o.round_storage(_mlp_up_X(n, seed=31), "bf16")
+    xbits = torch.from_numpy(wl.to_bf16_bits(X).view(np.uint8).reshape(-1).copy())
+    keep, xv = _view_with_bit31(torch, xbits.numel())
+    xv.copy_(xbits.cuda())
+    dX = xv.view(torch.bfloat16).view(n, d)
+    T = _rand_T(d, k, seed=5)
+    codes, s = _tq_gpu_from_device(dX, T, k)
+    _, _, s_or = check_codes(codes, X, T, label="bit31 single pass")
+    _check_scales(s, s_or, "bit31 single pass")
+    del keep

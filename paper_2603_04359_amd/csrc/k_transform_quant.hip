@@ -405,8 +405,9 @@ __global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
 // bf16, k = 128, d = 4096 (32 blocks), one launch, X read once.  One
 // workgroup per CU owns block b for the token tiles r, r + R, ... (a tile is
 // 64 tokens) and splits its eight waves by role:
-//   waves 0-3  compute: wave w multiplies rows 32w .. 32w + 31 of T_b (held
-//              in registers) with every token of the tile, read from LDS;
+//   waves 0-3  compute: wave w multiplies rows 64 (w / 2) .. + 63 of T_b
+//              (held in registers) with tokens 32 (w % 2) .. + 31 of the
+//              tile, read from LDS;
 //   waves 4-5  copy: stream token tiles into an 8-stage LDS ring with
 //              global_load_lds_dwordx4, seven tiles ahead;
 //   wave 6     gather: reads the per-token maxima other workgroups published;
@@ -537,9 +538,9 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
     float* __restrict__ s_x) {
     constexpr int K = 128;
     constexpr int NS = K / 16;          // 16-deep MFMA steps
-    constexpr int NSB = kFqTT / 32;     // 32-token subtiles
+    static_assert(kFqTT == 64 && kFqCompute == 4, "compute waves: 2 token halves x 2 row halves");
     __shared__ __attribute__((aligned(16))) u32x4 ring[kFqStages][kFqStage];
-    __shared__ uint32_t red[kFqCompute][kFqTT];   // per-wave maxima of the step's tile
+    __shared__ uint32_t red[2][kFqTT];            // per-row-half maxima of the step's tile
     __shared__ uint32_t gat[kFqTT];               // row maxima of the tile being quantized
     __shared__ uint32_t fred[2][2];               // reduced row maxima of the owned tokens
 
@@ -578,9 +579,7 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
                 lds_barrier();                                        // F
                 if (it < nt) {
                     const int64_t t = tile0(it) + lane;
-                    uint32_t mm = red[0][lane];
-#pragma unroll
-                    for (int w = 1; w < kFqCompute; ++w) mm = max(mm, red[w][lane]);
+                    const uint32_t mm = max(red[0][lane], red[1][lane]);
                     if (t < n) store(p_word(t, b), mm);
                 }
             }
@@ -666,57 +665,59 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
     }
 
     // ------------------------------------------------------ compute waves
+    // Wave w takes the 32 tokens 32 (w % 2) .. + 31 of a tile against rows
+    // 64 (w / 2) .. + 63 of T_b (two 32-row MFMA groups held in registers),
+    // so each wave reads only its own tokens from LDS.
     const int l32 = lane & 31;
     const int h = lane >> 5;
-    const int row0 = wave * 32;
-    u32x4 tf[NS];
-    {
-        const u32x4* tg = reinterpret_cast<const u32x4*>(T + (b * K + row0 + fq_row(l32)) * K);
+    const int th = wave & 1;            // token half of the tile
+    const int rh = wave >> 1;           // row half of T_b
+    const int tok = th * 32 + l32;      // token (within the tile) of this lane
+    u32x4 tf[2][NS];
 #pragma unroll
-        for (int s = 0; s < NS; ++s) tf[s] = tg[2 * s + h];
+    for (int g = 0; g < 2; ++g) {
+        const int row = (2 * rh + g) * 32 + fq_row(l32);
+        const u32x4* tg = reinterpret_cast<const u32x4*>(T + (b * K + row) * K);
+#pragma unroll
+        for (int s = 0; s < NS; ++s) tf[g][s] = tg[2 * s + h];
     }
-    auto mfma = [&](int64_t it, f32x16 (&acc)[NSB]) {
+    auto mfma = [&](int64_t it, f32x16 (&acc)[2]) {
         const int st = static_cast<int>(it % kFqStages);
 #pragma unroll
-        for (int sb = 0; sb < NSB; ++sb) acc[sb] = f32x16{};
+        for (int g = 0; g < 2; ++g) acc[g] = f32x16{};
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
+            const u32x4 xf = ring[st][tok * kFqU + ((2 * s + h) ^ tq_xswz<K>(tok))];
 #pragma unroll
-            for (int sb = 0; sb < NSB; ++sb) {
-                const int rr = sb * 32 + l32;
-                const u32x4 xf = ring[st][rr * kFqU + ((2 * s + h) ^ tq_xswz<K>(rr))];
-                acc[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(tf[s]), as_bf16x8(xf),
-                                                                  acc[sb], 0, 0, 0);
-            }
+            for (int g = 0; g < 2; ++g)
+                acc[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(tf[g][s]), as_bf16x8(xf),
+                                                                 acc[g], 0, 0, 0);
         }
-#pragma unroll
-        for (int sb = 0; sb < NSB; ++sb) {
-            uint32_t m = fq_absmax16(acc[sb]);
-            m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), 32)));
-            if (h == 0) red[wave][sb * 32 + l32] = m;
-        }
+        uint32_t m = max(fq_absmax16(acc[0]), fq_absmax16(acc[1]));
+        m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), 32)));
+        if (h == 0) red[rh][tok] = m;
     };
-    auto quant = [&](int64_t it, const f32x16 (&acc)[NSB]) {
-        const int64_t t0 = tile0(it);
+    auto quant = [&](int64_t it, const f32x16 (&acc)[2]) {
+        const int64_t t = tile0(it) + tok;
+        const float amax = __uint_as_float(gat[tok]);
+        const float inv = amax > 0.0f ? __fdiv_rn(kQmax4, amax) : 0.0f;
 #pragma unroll
-        for (int sb = 0; sb < NSB; ++sb) {
-            const int64_t t = t0 + sb * 32 + l32;
-            const float amax = __uint_as_float(gat[sb * 32 + l32]);
-            const float inv = amax > 0.0f ? __fdiv_rn(kQmax4, amax) : 0.0f;
-            const u32x2 c = fq_quant16(acc[sb], inv);
+        for (int g = 0; g < 2; ++g) {
+            const u32x2 c = fq_quant16(acc[g], inv);
             if (t < n)
-                *reinterpret_cast<u32x2*>(codes + t * (d / 2) + b * (K / 2) + row0 / 2 + 8 * h) = c;
+                *reinterpret_cast<u32x2*>(codes + t * (d / 2) + b * (K / 2) + (2 * rh + g) * 16 +
+                                          8 * h) = c;
         }
     };
     // step it: A, multiply tile it into cur, F, quantize tile it-3 from old
-    auto step = [&](int64_t it, f32x16 (&cur)[NSB], const f32x16 (&old)[NSB]) {
+    auto step = [&](int64_t it, f32x16 (&cur)[2], const f32x16 (&old)[2]) {
         lds_barrier();                                                // A
         if (it < nt) mfma(it, cur);
         lds_barrier();                                                // F
         if (it >= kFqLag) quant(it - kFqLag, old);
     };
     static_assert(kFqLag == 3, "four accumulator sets rotate");
-    f32x16 s0[NSB], s1[NSB], s2[NSB], s3[NSB];
+    f32x16 s0[2], s1[2], s2[2], s3[2];
     for (int64_t it = 0; it < nsteps; it += 4) {
         step(it, s0, s1);
         if (it + 1 >= nsteps) break;

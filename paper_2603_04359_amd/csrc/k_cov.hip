@@ -262,9 +262,12 @@ __global__ __launch_bounds__(kCovThreads) void cov_valu_kernel(const XT* __restr
 
 // ------------------------------------------- 256 x 256 tiles, stream-K
 // For matrices of at least 256 channels (bf16, channel count a multiple
-// of 32).  Each workgroup (4 waves, one per SIMD) works on 256 x 256 tiles
-// of the upper triangle; every wave keeps 128 x 128 fp32 partial sums (4 x
-// 4 v_mfma_f32_32x32x16_bf16 accumulators).  Token slabs of 32 rows go from
+// of 32).  Each workgroup (8 waves in a 2 x 4 grid, two per SIMD) works on
+// 256 x 256 tiles of the upper triangle; every wave keeps 128 x 64 fp32
+// partial sums (4 x 2 v_mfma_f32_32x32x16_bf16 accumulators).  With two
+// waves per SIMD one wave's MFMAs run while the other waits for its
+// fragment reads; the LDS (slab copies in, transposing reads out) is the
+// busiest unit.  Token slabs of 32 rows go from
 // HBM straight into a 4-stage LDS ring with global_load_lds_dwordx4, in
 // X's own row-major order (no transposition on the way in): 512 bytes of
 // each token row per operand, 16-byte units XOR-swizzled by row.  The
@@ -289,7 +292,8 @@ constexpr int kSkStages = 4;
 static_assert(kSkStages >= 2 && kSkStages <= 4, "wait counts cover at most 2 slabs ahead");
 constexpr int kSkRowUnits = kSkT / 8;            // 16-byte units per token row (32)
 constexpr int kSkOpUnits = kSkSlab * kSkRowUnits;  // units per operand and stage (1024)
-constexpr int kSkLoads = kSkOpUnits / kCovThreads; // direct loads per thread and operand (4)
+constexpr int kSkThreads = 512;                  // 8 waves: 2 x 4 over the tile
+constexpr int kSkLoads = kSkOpUnits / kSkThreads;  // direct loads per thread and operand (2)
 constexpr int kSkMaxSlabs = 256;                 // slabs per launch (8192 tokens)
 constexpr int64_t kSkSlotFloats = int64_t(kSkT) * kSkT;   // one 256 x 256 fp32 tile
 
@@ -353,7 +357,7 @@ __device__ __forceinline__ bf16x8 sk_frag(const char __attribute__((address_spac
     return __builtin_bit_cast(bf16x8, v);
 }
 
-__global__ __launch_bounds__(kCovThreads, 1) void cov_sk_kernel(const uint16_t* __restrict__ X,
+__global__ __launch_bounds__(kSkThreads, 1) void cov_sk_kernel(const uint16_t* __restrict__ X,
                                                                 int64_t n, int64_t d, int mode,
                                                                 int64_t k, SkGeom g,
                                                                 float* __restrict__ acc,
@@ -363,7 +367,7 @@ __global__ __launch_bounds__(kCovThreads, 1) void cov_sk_kernel(const uint16_t* 
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
     const int wave = tid / kWave;
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = wave >> 2, wn = wave & 3;   // wave tile 128 x 64
     const int l32 = lane & 31;
     const int h = lane >> 5;
 
@@ -376,22 +380,26 @@ __global__ __launch_bounds__(kCovThreads, 1) void cov_sk_kernel(const uint16_t* 
     const int64_t t_first = u_begin / g.S, t_last = (u_end - 1) / g.S;
     const bool head_first = (u_begin % g.S) != 0 && t_last > t_first;
 
-    // direct-load geometry: load q of this thread fills unit (q*4+wave)*64+lane
-    // of an operand stage, i.e. token row 8q + rr, swizzled position l32.
+    // direct-load geometry: load q of this thread fills unit (q*8+wave)*64+lane
+    // of an operand stage, i.e. token row 16q + rr, swizzled position l32.
     const int rr = 2 * wave + h;
     const int unit = l32 ^ ((rr & 3) << 2);      // global 16-byte unit of the row
     const uint32_t row_bytes = static_cast<uint32_t>(d) * 2u;
 
     // fragment-read geometry (bytes inside one operand stage)
     const int i16 = lane & 15, e = i16 >> 2, qq = i16 & 3, gg = (lane >> 4) & 1;
-    uint32_t offA[4], offB[4];
+    uint32_t offA[4], offB[2];
 #pragma unroll
     for (int a = 0; a < 4; ++a) {
         const int row = 8 * h + e;                 // token row inside the 16-token step
         const int ua = (wm * 16 + 4 * a + 2 * gg + (qq >> 1)) ^ ((row & 3) << 2);
-        const int ub = (wn * 16 + 4 * a + 2 * gg + (qq >> 1)) ^ ((row & 3) << 2);
         offA[a] = row * (kSkT * 2) + 16 * ua + 8 * (qq & 1);
-        offB[a] = row * (kSkT * 2) + 16 * ub + 8 * (qq & 1);
+    }
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+        const int row = 8 * h + e;
+        const int ub = (wn * 8 + 4 * b + 2 * gg + (qq >> 1)) ^ ((row & 3) << 2);
+        offB[b] = row * (kSkT * 2) + 16 * ub + 8 * (qq & 1);
     }
 
     for (int64_t idx = 0; u_begin < u_end && idx <= t_last - t_first; ++idx) {
@@ -425,29 +433,29 @@ __global__ __launch_bounds__(kCovThreads, 1) void cov_sk_kernel(const uint16_t* 
             const uint32_t lb = lds_addr(&ring[st][1][wave * 64]);
             if (t0 + kSkSlab <= n) {
 #pragma unroll
-                for (int q = 0; q < kSkLoads; ++q) dma16(base, oa + q * 8u * row_bytes, la + q * 4096u);
+                for (int q = 0; q < kSkLoads; ++q) dma16(base, oa + q * 16u * row_bytes, la + q * 8192u);
                 if (!diag) {
 #pragma unroll
                     for (int q = 0; q < kSkLoads; ++q)
-                        dma16(base, ob + q * 8u * row_bytes, lb + q * 4096u);
+                        dma16(base, ob + q * 16u * row_bytes, lb + q * 8192u);
                 }
             } else {
                 // ragged last slab: rows past n load row n-1 (zeroed once landed)
 #pragma unroll
                 for (int q = 0; q < kSkLoads; ++q) {
-                    const int64_t t = t0 + 8 * q + rr;
+                    const int64_t t = t0 + 16 * q + rr;
                     const uint32_t back = t < n ? 0u : static_cast<uint32_t>(t - (n - 1)) * row_bytes;
-                    dma16(base, oa + q * 8u * row_bytes - back, la + q * 4096u);
-                    if (!diag) dma16(base, ob + q * 8u * row_bytes - back, lb + q * 4096u);
+                    dma16(base, oa + q * 16u * row_bytes - back, la + q * 8192u);
+                    if (!diag) dma16(base, ob + q * 16u * row_bytes - back, lb + q * 8192u);
                 }
             }
         };
 
-        f32x16 part[4][4];
+        f32x16 part[4][2];
 #pragma unroll
         for (int a = 0; a < 4; ++a)
 #pragma unroll
-            for (int b = 0; b < 4; ++b) part[a][b] = f32x16{};
+            for (int b = 0; b < 2; ++b) part[a][b] = f32x16{};
 
         // Software pipeline: the fragments of the first 16 tokens of slab
         // s + 1 are read right after the barrier that publishes the slab,
@@ -472,9 +480,9 @@ __global__ __launch_bounds__(kCovThreads, 1) void cov_sk_kernel(const uint16_t* 
                 const int sl = static_cast<int>((s - s0) % kSkStages);
 #pragma unroll
                 for (int q = 0; q < kSkLoads; ++q) {
-                    if (t0 + 8 * q + rr >= n) {
-                        ring[sl][0][(q * 4 + wave) * 64 + lane] = u32x4{0u, 0u, 0u, 0u};
-                        if (!diag) ring[sl][1][(q * 4 + wave) * 64 + lane] = u32x4{0u, 0u, 0u, 0u};
+                    if (t0 + 16 * q + rr >= n) {
+                        ring[sl][0][(q * 8 + wave) * 64 + lane] = u32x4{0u, 0u, 0u, 0u};
+                        if (!diag) ring[sl][1][(q * 8 + wave) * 64 + lane] = u32x4{0u, 0u, 0u, 0u};
                     }
                 }
             }
@@ -486,13 +494,13 @@ __global__ __launch_bounds__(kCovThreads, 1) void cov_sk_kernel(const uint16_t* 
 #pragma unroll
             for (int a = 0; a < 4; ++a) fa[a] = sk_frag(baseA, offA[a] + kk * 16 * kSkT * 2);
 #pragma unroll
-            for (int b = 0; b < 4; ++b) fb[b] = sk_frag(baseB, offB[b] + kk * 16 * kSkT * 2);
+            for (int b = 0; b < 2; ++b) fb[b] = sk_frag(baseB, offB[b] + kk * 16 * kSkT * 2);
         };
         auto mfmas = [&](const bf16x8* fa, const bf16x8* fb) {
 #pragma unroll
             for (int a = 0; a < 4; ++a)
 #pragma unroll
-                for (int b = 0; b < 4; ++b)
+                for (int b = 0; b < 2; ++b)
                     part[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[a], fb[b], part[a][b],
                                                                          0, 0, 0);
         };
@@ -502,7 +510,7 @@ __global__ __launch_bounds__(kCovThreads, 1) void cov_sk_kernel(const uint16_t* 
             if (s0 + p < s1) issue(s0 + p, p);
         wait_slab(s0, (s0 + kSkStages - 2 < s1 - 1) ? s0 + kSkStages - 2 : s1 - 1);
         lds_barrier();
-        bf16x8 fa0[4], fb0[4], fa1[4], fb1[4];
+        bf16x8 fa0[4], fb0[2], fa1[4], fb1[2];
         read_frags(0, 0, fa0, fb0);
         int st = 0;
         for (int64_t s = s0; s < s1; ++s) {
@@ -529,13 +537,13 @@ __global__ __launch_bounds__(kCovThreads, 1) void cov_sk_kernel(const uint16_t* 
         // offsets from being precomputed outside the loop and the chunks
         // apart.
         uint32_t rowb = static_cast<uint32_t>(wm * 128 + 4 * h);
-        uint32_t colb = static_cast<uint32_t>(wn * 128 + l32);
+        uint32_t colb = static_cast<uint32_t>(wn * 64 + l32);
         asm volatile("" : "+v"(rowb), "+v"(colb));
         if (whole) {
             // Through LDS (the ring is free once every wave is past its last
-            // fragment read): the 128 x 256 half of the tile that waves
-            // (h, 0) and (h, 1) hold is written row-major into LDS, then all
-            // 256 threads add it into acc with 16-byte row accesses.  This
+            // fragment read): the 128 x 256 half of the tile that the four
+            // waves with wm == half hold is written row-major into LDS, then
+            // all 512 threads add it into acc with 16-byte row accesses.  This
             // keeps the read-modify-write of acc out of the accumulator
             // registers.
             float* stage = reinterpret_cast<float*>(&ring[0][0][0]);   // 128 x 256 fp32
@@ -548,24 +556,24 @@ __global__ __launch_bounds__(kCovThreads, 1) void cov_sk_kernel(const uint16_t* 
 #pragma unroll
                     for (int a = 0; a < 4; ++a)
 #pragma unroll
-                        for (int b = 0; b < 4; ++b)
+                        for (int b = 0; b < 2; ++b)
 #pragma unroll
                             for (int r = 0; r < 16; ++r)
-                                stage[(32 * a + 8 * (r >> 2) + 4 * h + (r & 3)) * kSkT + wn * 128 +
+                                stage[(32 * a + 8 * (r >> 2) + 4 * h + (r & 3)) * kSkT + wn * 64 +
                                       32 * b + l32] = part[a][b][r];
                 }
                 lds_barrier();
                 // 128 rows x 64 float4 per row; thread tid takes column group
-                // tid % 64 of rows tid / 64 + 4 j
+                // tid % 64 of rows tid / 64 + 8 j
                 const int cg = tid & 63;
                 const int64_t col = J0 + 4 * cg;
                 if (cols_ok || col < dimv) {
 #pragma unroll
-                    for (int j0 = 0; j0 < 32; j0 += 8) {
+                    for (int j0 = 0; j0 < 16; j0 += 8) {
                         f32x4 old[8];
 #pragma unroll
                         for (int j = 0; j < 8; ++j) {
-                            const int row = (tid >> 6) + 4 * (j0 + j);
+                            const int row = (tid >> 6) + 8 * (j0 + j);
                             const int64_t grow = I0 + 128 * half + row;
                             old[j] = (rows_ok || grow < dimv)
                                          ? *reinterpret_cast<const f32x4*>(accm + grow * dimv + col)
@@ -573,7 +581,7 @@ __global__ __launch_bounds__(kCovThreads, 1) void cov_sk_kernel(const uint16_t* 
                         }
 #pragma unroll
                         for (int j = 0; j < 8; ++j) {
-                            const int row = (tid >> 6) + 4 * (j0 + j);
+                            const int row = (tid >> 6) + 8 * (j0 + j);
                             const int64_t grow = I0 + 128 * half + row;
                             const f32x4 add = *reinterpret_cast<const f32x4*>(stage + row * kSkT + 4 * cg);
                             if (rows_ok || grow < dimv)
@@ -587,7 +595,7 @@ __global__ __launch_bounds__(kCovThreads, 1) void cov_sk_kernel(const uint16_t* 
 #pragma unroll
             for (int a = 0; a < 4; ++a)
 #pragma unroll
-                for (int b = 0; b < 4; ++b)
+                for (int b = 0; b < 2; ++b)
 #pragma unroll
                     for (int r = 0; r < 16; ++r)
                         slot[(rowb + 32 * a + 8 * (r >> 2) + (r & 3)) * kSkT + colb + 32 * b] =
@@ -732,7 +740,7 @@ hipError_t launch_cov_accumulate(const void* X, int x_bf16, int64_t n, int64_t d
                                                                        : int64_t(kSkMaxSlabs) * kSkSlab;
             SkGeom g;
             if (!cov_sk_geometry(nc, d, mode, k, cus, g)) return hipSuccess;
-            hipLaunchKernelGGL(cov_sk_kernel, dim3(static_cast<uint32_t>(g.G)), dim3(kCovThreads),
+            hipLaunchKernelGGL(cov_sk_kernel, dim3(static_cast<uint32_t>(g.G)), dim3(kSkThreads),
                                0, stream, Xb + t0 * d, nc, d, mode, k, g, acc,
                                static_cast<float*>(workspace));
             err = hipGetLastError();

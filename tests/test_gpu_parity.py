@@ -97,6 +97,31 @@ def test_w4a4_linear_extreme_codes_at_max_d_in():
     assert host(acc)[0, 0] == 49 * d_in
 
 
+def test_w4a4_linear_mlp_up_full_size_sampled():
+    # 8192 x 4096 -> 14336, the shape and launch the benchmark times; the
+    # oracle checks a 64 x 64 sample of rows and columns spread over every
+    # row panel and column panel, including the last ones
+    torch = torch_mod()
+    n, d_in, d_out = 8192, 4096, 14336
+    say(f"w4a4 mlp_up full size {n} x {d_in} -> {d_out}")
+    qx = wl.random_codes(n, d_in, seed=81)
+    qw = wl.random_codes(d_out, d_in, seed=82)
+    rng = np.random.default_rng(83)
+    sx = rng.uniform(0.01, 1.0, n).astype(np.float32)
+    sw = rng.uniform(0.01, 1.0, d_out).astype(np.float32)
+    y = torch.empty((n, d_out), dtype=torch.float32, device="cuda")
+    acc = torch.empty((n, d_out), dtype=torch.int32, device="cuda")
+    cat.cat_w4a4_linear(dev(o.pack_int4(qx), "u8"), dev(sx, "f32"), dev(o.pack_int4(qw), "u8"),
+                        dev(sw, "f32"), y, acc)
+    rows = np.unique(np.concatenate([rng.choice(n, 62, replace=False), [0, n - 1]]))
+    cols = np.unique(np.concatenate([rng.choice(d_out, 62, replace=False), [0, d_out - 1]]))
+    acc_or, y_or = o.w4a4_linear(qx[rows], sx[rows], qw[cols], sw[cols])
+    acc_g = host(acc[torch.from_numpy(rows).cuda()][:, torch.from_numpy(cols).cuda()])
+    y_g = host(y[torch.from_numpy(rows).cuda()][:, torch.from_numpy(cols).cuda()])
+    assert np.array_equal(acc_g, acc_or)
+    assert np.array_equal(y_g, y_or)
+
+
 # ------------------------------------------------------ transform + quant
 def _tq_gpu(X, T, k, x_dtype, t_dtype):
     torch = torch_mod()

@@ -6,20 +6,32 @@
 //
 // Tiles: 256 x 256 outputs per workgroup of 512 threads = 8 waves in a
 // 2 x 4 grid, each wave 128 x 64 = 4 x 2 MFMA tiles with int32
-// accumulators; one workgroup per CU (two waves per SIMD, 132 KiB of LDS).
+// accumulators; one workgroup per CU (two waves per SIMD, 144 KiB of LDS).
 // One K step covers 128 codes (64 packed bytes per row); a tile reads
 // 32 KiB of packed codes per step.
 //
+// Ping-pong schedule: waves 0-3 (rows 0-127 of the tile, one wave per
+// SIMD) and waves 4-7 (rows 128-255, the other wave of each SIMD) are
+// offset by one phase.  In a compute phase a wave issues the 32 MFMAs of
+// one K step at raised priority; in a load phase it requests the direct
+// loads of a later step and reads the next step's fragments from LDS.  A
+// workgroup barrier separates phases, so on every SIMD one wave computes
+// while the other loads.  Per tile: 2 nk + 2 phases; group 0 stores its
+// half of the tile while group 1 computes the last step, group 1 one phase
+// later.  Each group runs its own straight-line loop.
+//
 // Operand path: packed INT4 tiles go straight from global memory into an
 // LDS ring of kStages (4) steps with global_load_lds_dwordx4 (no register
-// staging, no LDS store instructions), issued kStages-1 steps ahead of
-// use, with one barrier per step that waits for LDS traffic only (a plain
-// workgroup barrier would also drain the loads in flight).  Each lane reads
-// 16 packed bytes (32 codes, two MFMA steps) per fragment and widens them
-// in registers to int8 values 16*code: a packed dword (8 codes) becomes one
-// dword of its low nibbles and one of its high nibbles, two bit operations
-// each.  The widening of the next 32-code step is independent of the MFMAs
-// of the current one, so it co-issues with them.  Both operands are widened
+// staging, no LDS store instructions), requested kStages-1 steps ahead;
+// waves 0-3 load operand A (codes_x), waves 4-7 operand B (codes_w).  The
+// barrier waits for LDS traffic only (a plain workgroup barrier would also
+// drain the loads in flight); each wave waits for its own loads of the next
+// step (vmcnt) before the barrier that publishes it.  Each lane reads 16
+// packed bytes (32 codes, two MFMA steps) per fragment and widens them in
+// registers to int8 values 16*code: a packed dword (8 codes) becomes one
+// dword of its low nibbles and one of its high nibbles.  B is widened in
+// the load phase, A in the compute phase (registers: 128 accumulators,
+// 32 packed A and 32 widened B per lane).  Both operands are widened
 // identically, so each MFMA sums the same index pairs (a permutation of the
 // reduction index) and the int32 result is 256 * acc; an arithmetic shift
 // by 8 recovers acc exactly for d_in <= 131072.
@@ -32,21 +44,22 @@
 // swz(r) in bit 0, so both 16 consecutive lanes and lanes {i..i+7} with
 // {i+32..i+39} land on 16 distinct 16-byte bank groups of a 64-bank LDS.
 // The direct loads fill 64 consecutive slots per wave instruction, so each
-// lane loads the global unit that belongs in its slot
-// (a permutation inside each 64-byte row segment).  Rows past the end of a
-// matrix load a clamped in-bounds row (their outputs are never stored);
-// units past d_in in a ragged last step load any in-bounds unit and the
-// loading thread clears them in LDS before the step's barrier, which
-// zeroes their products.
+// lane loads the global unit that belongs in its slot (a permutation inside
+// each 64-byte row segment).  Rows past the end of a matrix load a clamped
+// in-bounds row (their outputs are never stored); units past d_in in a
+// ragged last step load any in-bounds unit and the loading thread clears
+// them in A before the barrier that publishes the step, which zeroes their
+// products.
 //
-// Persistent launch: kWgPerCu workgroups per CU walk lists of tiles in an
+// Persistent launch: one workgroup per CU walks a list of tiles in an
 // XCD-aware order (workgroups are dealt to the 8 XCDs round-robin; those of
 // XCD x walk one contiguous range of tiles, in groups of kGroupM row
 // panels, so tiles resident on one XCD share panels in its L2).  The
 // operand steps of consecutive tiles form one stream through the ring, and
-// the tile's scales are staged in LDS with the first step, so the epilogue
-// reads no global memory and the next tile never waits behind the output
-// stores.  Output rows stream out with nontemporal stores.
+// each tile's scales are staged in LDS with its first step, so the
+// epilogue reads no global memory.  The epilogue of a full tile is
+// straight-line code with a wave-uniform row base per accumulator row: it
+// runs once per tile, so its instruction footprint is what it costs.
 #include "device_common.h"
 #include "kernels.h"
 
@@ -59,10 +72,6 @@ constexpr int kBN = 256;           // outputs per tile
 constexpr int kKBP = 64;           // packed bytes per row per K step (128 codes)
 constexpr int kUP = kKBP / 16;     // 16-byte units per row per step
 constexpr int kStages = 4;         // LDS ring depth (steps)
-constexpr int kAUnits = kBM * kUP;                   // A units per stage
-constexpr int kBUnits = kBN * kUP;                   // B units per stage
-constexpr int kLoadsA = kAUnits / kGemmThreads;      // direct loads per thread, A
-constexpr int kLoadsB = kBUnits / kGemmThreads;      // direct loads per thread, B
 constexpr int kWgPerCu = 1;
 static_assert(kStages >= 2 && kStages <= 4, "waits cover at most 2 steps ahead");
 constexpr int kGroupM = 4;         // row panels per tile group
@@ -102,244 +111,193 @@ __device__ __forceinline__ i32x4 widen8(u32x4 v, int half) {
                  static_cast<int>(unpack_lo16(w1)), static_cast<int>(unpack_hi16(w1))};
 }
 
+constexpr int kPpUnits = kBM * kUP;                        // units per operand stage
+constexpr int kPpLoads = kPpUnits / (kGemmThreads / 2);    // direct loads per thread per step
+// scale slots: a tile's slot is reused 8 tiles later, after both groups'
+// epilogues of the earlier tile even when every tile is one K step
+constexpr int kScaleSlots = 8;
+static_assert(kBM == kBN, "both operands share the stage layout");
+static_assert(kPpLoads == 4, "four 64-slot instructions per wave per step");
+
 __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
     const uint8_t* __restrict__ qx, const float* __restrict__ s_x,
     const uint8_t* __restrict__ qw, const float* __restrict__ s_w, int64_t n, int64_t d_in,
     int64_t d_out, float* __restrict__ y, int32_t* __restrict__ acc_out) {
-    __shared__ __attribute__((aligned(16))) u32x4 ring_a[kStages][kAUnits];
-    __shared__ __attribute__((aligned(16))) u32x4 ring_b[kStages][kBUnits];
-    // s_x of the tile's rows and s_w of its outputs, double-buffered by tile
-    __shared__ __attribute__((aligned(16))) float sscale[2][kBM + kBN];
+    // ring[o][stage]: operand o (0 = A, 1 = B), kStages steps deep
+    __shared__ __attribute__((aligned(16))) u32x4 ring[2][kStages][kPpUnits];
+    // s_x of a tile's rows and s_w of its outputs; slot = tile index % kScaleSlots
+    __shared__ __attribute__((aligned(16))) float sscale[kScaleSlots][kBM + kBN];
 
     const int64_t row_bytes = d_in / 2;
     const int nk = static_cast<int>((row_bytes + kKBP - 1) / kKBP);
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
-    const int wave = tid / kWave;
-    const int wm = wave >> 2, wn = wave & 3;   // 2 x 4 waves, each 128 x 64
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);   // uniform: SGPR branches
+    const int grp = wave >> 2;                 // 0: rows 0-127, loads A; 1: rows 128-255, loads B
+    const int wm = grp, wn = wave & 3;         // 2 x 4 waves, each 128 x 64
+    const int w4 = wave & 3;
     const int l32 = lane & 31;
     const int h = lane >> 5;
 
-    // Direct loads: instruction q of wave w fills slots [64 I, 64 I + 64)
-    // with I = q * 8 + w (16 rows of 64 bytes); slot s holds row s / 4,
-    // logical unit (s % 4) ^ swz(row).  32-bit offsets from the tile's
-    // first row.
-    const uint8_t* a_base = qx;
-    const uint8_t* b_base = qw;
-    uint32_t a_off[kLoadsA], b_off[kLoadsB];
-    // the byte offset of a thread's unit inside its row segment is the same
-    // for every load q (64 slots per instruction keep row / 8 and slot % 8)
-    const int u_off = ((lane % kUP) ^ gemm_swz((wave * 64 + lane) / kUP)) * 16;
-    static_assert((64 / kUP) % 16 == 0, "swz(row) must not depend on the instruction");
+    // tiles of this workgroup and total steps
+    int n_tiles = 0;
+    {
+        GemmTile t;
+        while (gemm_tile(n_tiles, n, d_out, t)) ++n_tiles;
+    }
+    if (n_tiles == 0) return;
+    const int G = n_tiles * nk;
+
+    // Direct loads of this wave's operand: instruction q fills slots
+    // [64 (4q + w4), +64) of the stage; slot s holds row s / 4, logical unit
+    // (s % 4) ^ swz(row).  swz(row) depends on lane bits 4-5 only.
+    const uint8_t* src = grp == 0 ? qx : qw;
+    const int64_t src_rows = grp == 0 ? n : d_out;
+    const uint8_t* src_base = src;
+    uint32_t src_off[kPpLoads];
+    const int u_off = ((lane % kUP) ^ gemm_swz(lane / kUP)) * 16;
+    // row offsets inside a tile are below 256 * 65536 bytes: 32-bit
+    const uint32_t rb32 = static_cast<uint32_t>(row_bytes);
     auto set_rows = [&](const GemmTile& tl) {
-        a_base = qx + tl.m0 * row_bytes;
-        b_base = qw + tl.n0 * row_bytes;
+        const int64_t r0 = grp == 0 ? tl.m0 : tl.n0;
+        src_base = src + r0 * row_bytes;
+        const int rows_left = static_cast<int>(src_rows - r0 < kBM ? src_rows - r0 : kBM);
+        int el = lane;
+        asm volatile("" : "+v"(el));
 #pragma unroll
-        for (int q = 0; q < kLoadsA; ++q) {
-            const int r = ((q * kGemmWaves + wave) * 64 + lane) / kUP;
-            const int64_t ra = tl.m0 + r < n ? r : n - 1 - tl.m0;   // clamped rows: never stored
-            a_off[q] = static_cast<uint32_t>(ra * row_bytes);
-        }
-#pragma unroll
-        for (int q = 0; q < kLoadsB; ++q) {
-            const int r = ((q * kGemmWaves + wave) * 64 + lane) / kUP;
-            const int64_t rb = tl.n0 + r < d_out ? r : d_out - 1 - tl.n0;
-            b_off[q] = static_cast<uint32_t>(rb * row_bytes);
+        for (int q = 0; q < kPpLoads; ++q) {
+            const int r = (q * 4 + w4) * (64 / kUP) + el / kUP;
+            const int rr = r < rows_left ? r : rows_left - 1;   // clamped rows: never stored
+            src_off[q] = static_cast<uint32_t>(rr) * rb32;
         }
     };
-    // LDS byte addresses of this wave's first slot in stage 0 (wave-uniform)
-    const uint32_t lds_a0 = static_cast<uint32_t>(
-        __builtin_amdgcn_readfirstlane(lds_addr(&ring_a[0][wave * 64])));
-    const uint32_t lds_b0 = static_cast<uint32_t>(
-        __builtin_amdgcn_readfirstlane(lds_addr(&ring_b[0][wave * 64])));
-    auto issue = [&](int kt, int st) {
+    const uint32_t lds0 = static_cast<uint32_t>(
+        __builtin_amdgcn_readfirstlane(lds_addr(&ring[grp][0][w4 * 64])));
+    auto issue_step = [&](int kt, int st) {
         const int64_t k0 = static_cast<int64_t>(kt) * kKBP;
-        const uint32_t la = lds_a0 + static_cast<uint32_t>(st) * (kAUnits * 16);
-        const uint32_t lb = lds_b0 + static_cast<uint32_t>(st) * (kBUnits * 16);
-        if (k0 + kKBP <= row_bytes) {
-            const uint32_t k0u = static_cast<uint32_t>(k0);
+        int64_t col = k0 + u_off;
+        col = col < row_bytes ? col : 0;      // past the row end: any in-bounds unit
+        const uint32_t cu = static_cast<uint32_t>(col);
+        const uint32_t l = lds0 + static_cast<uint32_t>(st) * (kPpUnits * 16);
 #pragma unroll
-            for (int q = 0; q < kLoadsA; ++q)
-                dma16(a_base, a_off[q] + k0u + u_off, la + q * (kGemmWaves * 1024u));
+        for (int q = 0; q < kPpLoads; ++q) dma16(src_base, src_off[q] + cu, l + q * (4 * 1024u));
+    };
+    // s_x (group 0) or s_w (group 1) of a tile into its scale slot: rows /
+    // outputs past the end load the last one (never stored)
+    auto issue_scales = [&](const GemmTile& tl, int slot) {
+        const int64_t r = (grp == 0 ? tl.m0 : tl.n0) + 64 * w4 + lane;
+        dma4(grp == 0 ? s_x : s_w, static_cast<uint32_t>((r < src_rows ? r : src_rows - 1) * 4),
+             lds_addr(&sscale[slot][grp * kBM + 64 * w4]));
+    };
+    // A units of a ragged last step past d_in: zeroed by the threads that loaded them
+    auto clear_ragged = [&](int kt, int st) {
+        if (grp == 0 && kt == nk - 1 && (row_bytes % kKBP) != 0) {
 #pragma unroll
-            for (int q = 0; q < kLoadsB; ++q)
-                dma16(b_base, b_off[q] + k0u + u_off, lb + q * (kGemmWaves * 1024u));
-        } else {
-#pragma unroll
-            for (int q = 0; q < kLoadsA; ++q) {
-                int64_t col = k0 + u_off;
-                col = col < row_bytes ? col : 0;     // past the row end: any in-bounds unit
-                dma16(a_base, a_off[q] + static_cast<uint32_t>(col), la + q * (kGemmWaves * 1024u));
-            }
-#pragma unroll
-            for (int q = 0; q < kLoadsB; ++q) {
-                int64_t col = k0 + u_off;
-                col = col < row_bytes ? col : 0;
-                dma16(b_base, b_off[q] + static_cast<uint32_t>(col), lb + q * (kGemmWaves * 1024u));
-            }
+            for (int q = 0; q < kPpLoads; ++q)
+                if (static_cast<int64_t>(kt) * kKBP + u_off >= row_bytes)
+                    ring[0][st][(q * 4 + w4) * 64 + lane] = u32x4{0u, 0u, 0u, 0u};
         }
     };
-    constexpr int kLoadsPerStep = kLoadsA + kLoadsB;
 
     i32x16 acc[4][2];
-
-    // Fragments: lane half h reads logical units 2h and 2h+1 (c = 0, 1) of
-    // its row; each unit feeds two MFMA steps (its low and high 8 bytes).
-    // Both operands use the same assignment, so the reduction index is only
-    // permuted.
-    struct Packed {
-        u32x4 a[4], b[2];
-    };
-    struct Wide {
-        i32x4 a[4], b[2];
-    };
-    auto read_packed = [&](Packed& p, int st, int c) {
-        const int u = 2 * h + c;
+    // Fragments of one K step, read in the load phase: unit u = 2h + c of
+    // each row (c = 0, 1), 32 codes each; sub-step s = 2c + half covers
+    // codes [32 s, 32 s + 32) of the step (a permutation of the reduction
+    // index shared by both operands).  A stays packed until the compute
+    // phase; B is widened in the load phase.
+    u32x4 pa[2][4];
+    i32x4 fb[4][2];
+    // Row r = base + 32 i + l32 of a fragment has swz(r) = swz(l32) (bits 2
+    // and 3 of r come from l32), so each unit's address is one per-lane
+    // base plus immediate offsets.
+    const int frag_lane = l32 * kUP;
+    const int frag_u0 = (2 * h) ^ gemm_swz(l32);
+    auto load_frags = [&](int st) {
+        const u32x4* ra = &ring[0][st][wm * 128 * kUP + frag_lane];
+        const u32x4* rb = &ring[1][st][wn * 64 * kUP + frag_lane];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int r = wm * 128 + i * 32 + l32;
-            p.a[i] = ring_a[st][r * kUP + (u ^ gemm_swz(r))];
-        }
+        for (int c = 0; c < 2; ++c) {
+            const int uo = frag_u0 ^ c;
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int r = wn * 64 + j * 32 + l32;
-            p.b[j] = ring_b[st][r * kUP + (u ^ gemm_swz(r))];
-        }
-    };
-    auto widen = [&](Wide& w, const Packed& p, int half) {
+            for (int i = 0; i < 4; ++i) pa[c][i] = ra[i * 32 * kUP + uo];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) w.a[i] = widen8(p.a[i], half);
-#pragma unroll
-        for (int j = 0; j < 2; ++j) w.b[j] = widen8(p.b[j], half);
-    };
-    auto mfma16 = [&](const Wide& w) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int j = 0; j < 2; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(w.a[i], w.b[j], acc[i][j], 0, 0,
-                                                                 0);
-    };
-    // one K step = 4 MFMA steps of 32 codes; the widening of MFMA step
-    // m+1 is issued before the 16 MFMAs of step m
-    auto compute = [&](int st) {
-        Packed p;
-        Wide w0, w1;
-        read_packed(p, st, 0);
-        widen(w0, p, 0);
-        widen(w1, p, 1);
-#pragma unroll
-        for (int c = 1; c < kUP / 2; ++c) {
-            read_packed(p, st, c);
-            mfma16(w0);
-            widen(w0, p, 0);
-            mfma16(w1);
-            widen(w1, p, 1);
-        }
-        mfma16(w0);
-        mfma16(w1);
-    };
-
-    // s_x / s_w of a tile into its scale slot: 64 dwords per wave
-    // instruction (rows / outputs past the end load the last one; their
-    // outputs are never stored).  Issued before the tile's first operand
-    // step, so waiting for that step covers them.
-    auto issue_scales = [&](const GemmTile& tl, int slot) {
-        if (wave < 4) {
-            const int64_t r = tl.m0 + 64 * wave + lane;
-            dma4(s_x, static_cast<uint32_t>((r < n ? r : n - 1) * 4),
-                 lds_addr(&sscale[slot][64 * wave]));
-        } else {
-            const int64_t o = tl.n0 + 64 * (wave - 4) + lane;
-            dma4(s_w, static_cast<uint32_t>((o < d_out ? o : d_out - 1) * 4),
-                 lds_addr(&sscale[slot][kBM + 64 * (wave - 4)]));
-        }
-    };
-
-    // The operand steps of consecutive tiles form one stream through the
-    // ring: during a tile's last steps the first steps of the next tile
-    // (and its scales) are already requested, and they have landed before
-    // the tile's output is stored, so the next tile starts without waiting
-    // behind those stores.
-    GemmTile cur;
-    if (!gemm_tile(0, n, d_out, cur)) return;
-    const int pre_n = nk < kStages - 1 ? nk : kStages - 1;   // steps requested ahead of a tile
-    int sp = 0;      // scale slot of the current tile
-    int base = 0;    // ring stage of the current tile's step 0
-    set_rows(cur);
-    issue_scales(cur, sp);
-    for (int j = 0; j < pre_n; ++j) issue(j, j);
-    wait_vmcnt<0>();
-    lds_barrier();
-
-    for (int64_t k = 0;; ++k) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int j = 0; j < 2; ++j) acc[i][j] = i32x16{};
-        GemmTile nxt;
-        const bool more = gemm_tile(k + 1, n, d_out, nxt);
-        int nx_issued = 0;   // steps of the next tile requested so far
-
-        for (int kt = 0; kt < nk; ++kt) {
-            const int st = (base + kt) % kStages;
-            if (kt >= pre_n) {
-                // this thread's loads of step kt have landed once at most the
-                // loads of the one step requested after it are outstanding
-                const int last = nk - 1 + (more ? pre_n : 0);   // last step requested in this tile
-                const int issued = kt + kStages - 2 < last ? kt + kStages - 2 : last;
-                const int ahead = issued - kt;
-                if (ahead >= 2) wait_vmcnt<2 * kLoadsPerStep>();
-                else if (ahead == 1) wait_vmcnt<kLoadsPerStep>();
-                else wait_vmcnt<0>();
+            for (int j = 0; j < 2; ++j) {
+                const u32x4 pbj = rb[j * 32 * kUP + uo];
+                fb[2 * c][j] = widen8(pbj, 0);
+                fb[2 * c + 1][j] = widen8(pbj, 1);
             }
-            if (kt == nk - 1 && (row_bytes % kKBP) != 0) {
-                // ragged last step: codes past d_in read garbage; zero them in
-                // A (each thread clears the slots its own loads filled)
+        }
+    };
+    auto compute_step = [&]() {
+        // the computing wave's instructions go first on its SIMD (the other
+        // wave there is in its load phase)
+        __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-                for (int q = 0; q < kLoadsA; ++q)
-                    if (static_cast<int64_t>(kt) * kKBP + u_off >= row_bytes)
-                        ring_a[st][(q * kGemmWaves + wave) * 64 + lane] = u32x4{0u, 0u, 0u, 0u};
-            }
-            lds_barrier();     // all threads' loads of step kt landed; step kt-1 consumed
-            const int tgt = kt + kStages - 1;
-            if (tgt < nk) {
-                issue(tgt, (base + tgt) % kStages);
-            } else if (more && nx_issued < pre_n && nx_issued <= tgt - nk) {
-                // the next tile's steps, in order; step j's stage last held
-                // this tile's step nk + j - kStages <= kt - 1 (consumed)
-                const int j = nx_issued;
-                if (j == 0) {
-                    set_rows(nxt);
-                    issue_scales(nxt, sp ^ 1);
-                }
-                issue(j, (base + nk + j) % kStages);
-                nx_issued = j + 1;
-            }
-            compute(st);
+        for (int s = 0; s < 4; ++s) {
+            i32x4 wa[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) wa[i] = widen8(pa[s >> 1][i], s & 1);
+            const i32x4* wb = fb[s];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wa[i], wb[j], acc[i][j], 0,
+                                                                     0, 0);
         }
-        if (more) {
-            for (int j = nx_issued; j < pre_n; ++j) {   // only when nk < kStages - 1
-                if (j == 0) {
-                    set_rows(nxt);
-                    issue_scales(nxt, sp ^ 1);
-                }
-                issue(j, (base + nk + j) % kStages);
-            }
-            wait_vmcnt<0>();   // the next tile's first steps and scales have landed
-        }
-        lds_barrier();         // stages of this tile consumed; next tile's first steps visible
-
-        // ---- epilogue: lane holds column n0 + wn*64 + 32j + l32 and rows
-        // m0 + wm*128 + 32i + 8(r/4) + 4h + r%4
-        const float* sc = sscale[sp];
+        __builtin_amdgcn_s_setprio(0);
+    };
+    // lane holds column n0 + wn*64 + 32j + l32 and rows m0 + wm*128 + 32i +
+    // 8(r/4) + 4h + r%4.
+    auto epilogue = [&](const GemmTile& tl, int slot) {
+        // lane-derived values are recomputed here: hoisted out of the loop
+        // they would stay live next to the fragments and accumulators
+        int el = lane;
+        asm volatile("" : "+v"(el));
+        const int l32 = el & 31, h = el >> 5;
+        const float* sc = sscale[slot];
         float sw[2];
 #pragma unroll
         for (int j = 0; j < 2; ++j) sw[j] = sc[kBM + wn * 64 + j * 32 + l32];
+        const int64_t tile_off = tl.m0 * d_out + tl.n0;
+        float* yt = y + tile_off;
+        int32_t* at = acc_out ? acc_out + tile_off : nullptr;
+        const int rows_left = static_cast<int>(n - tl.m0 < kBM ? n - tl.m0 : kBM);
+        const int cols_left = static_cast<int>(d_out - tl.n0 < kBN ? d_out - tl.n0 : kBN);
+        if (rows_left == kBM && cols_left == kBN && !at && d_out < (int64_t{1} << 29)) {
+            // full tile: straight-line code, a wave-uniform row base per
+            // accumulator row plus a 32-bit per-lane offset (row 4h, column
+            // of fragment j; below 2^32 for d_out < 2^29), no bounds checks
+            const uint32_t dout = static_cast<uint32_t>(d_out);
+            uint32_t voff[2];
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                voff[j] = static_cast<uint32_t>(4 * h) * dout + static_cast<uint32_t>(wn * 64 + j * 32 + l32);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                float sx[16];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const f32x4 v = *reinterpret_cast<const f32x4*>(sc + wm * 128 + i * 32 + 8 * q + 4 * h);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) sx[4 * q + e] = v[e];
+                }
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    float* yr = yt + static_cast<int64_t>(wm * 128 + i * 32 + 8 * (r >> 2) + (r & 3)) * d_out;
+#pragma unroll
+                    for (int j = 0; j < 2; ++j) {
+                        const int v = acc[i][j][r] >> 8;
+                        __builtin_nontemporal_store((static_cast<float>(v) * sx[r]) * sw[j], yr + voff[j]);
+                    }
+                }
+            }
+            return;
+        }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const int64_t tb = cur.m0 + wm * 128 + i * 32 + 4 * h;
+            const int rb = wm * 128 + i * 32 + 4 * h;
             float sx[16];
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
@@ -349,23 +307,120 @@ __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
             }
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
-                const int64_t o = cur.n0 + wn * 64 + j * 32 + l32;
-                if (o >= d_out) continue;
+                const int col = wn * 64 + j * 32 + l32;
+                if (col >= cols_left) continue;
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
-                    const int64_t t = tb + 8 * (r >> 2) + (r & 3);
-                    if (t >= n) continue;
+                    const int row = rb + 8 * (r >> 2) + (r & 3);
+                    if (row >= rows_left) continue;
+                    const int64_t off = static_cast<int64_t>(row) * d_out + col;
                     const int v = acc[i][j][r] >> 8;
                     const float yv = (static_cast<float>(v) * sx[r]) * sw[j];
-                    __builtin_nontemporal_store(yv, y + t * d_out + o);
-                    if (acc_out) acc_out[t * d_out + o] = v;
+                    __builtin_nontemporal_store(yv, yt + off);
+                    if (at) at[off] = v;
                 }
             }
         }
-        if (!more) break;
-        cur = nxt;
-        sp ^= 1;
-        base = (base + nk) % kStages;
+    };
+
+    // issue cursor: the next step whose direct loads are requested
+    int is_g = 0, is_kt = 0, is_ti = 0;
+    GemmTile is_tile;
+    gemm_tile(0, n, d_out, is_tile);
+    set_rows(is_tile);
+    auto issue_next = [&]() {
+        if (is_g >= G) return;
+        if (is_kt == 0) issue_scales(is_tile, is_ti % kScaleSlots);
+        issue_step(is_kt, is_g % kStages);
+        ++is_g;
+        if (++is_kt == nk && is_g < G) {
+            is_kt = 0;
+            ++is_ti;
+            gemm_tile(is_ti, n, d_out, is_tile);
+            set_rows(is_tile);
+        }
+    };
+    // waits until this thread's loads of step g have landed, given that the
+    // steps after it up to is_g - 1 have been requested
+    auto wait_step = [&](int g) {
+        if (g >= G) return;
+        const int newer = is_g - 1 - g;
+        if (newer >= 2) wait_vmcnt<2 * kPpLoads>();
+        else if (newer == 1) wait_vmcnt<kPpLoads>();
+        else wait_vmcnt<0>();
+    };
+
+    // A phase boundary: the barrier, with nothing scheduled across it (an
+    // s_barrier does not stop the compiler from moving MFMAs or ALU work)
+    auto phase_end = [&]() {
+        __builtin_amdgcn_sched_barrier(0);
+        lds_barrier();
+        __builtin_amdgcn_sched_barrier(0);
+    };
+
+    // prologue: the first kStages - 1 steps, visible to both groups
+    const int pre = G < kStages - 1 ? G : kStages - 1;
+    for (int g = 0; g < pre; ++g) issue_next();
+    wait_vmcnt<0>();
+    {
+        int kt = 0;
+        for (int g = 0; g < pre; ++g) {
+            clear_ragged(kt, g % kStages);
+            if (++kt == nk) kt = 0;
+        }
+    }
+    lds_barrier();
+
+    // Per tile, 2 nk + 2 phases separated by barriers.  Group 0 loads step i
+    // in phase 2i and computes it in phase 2i + 1; group 1 does the same one
+    // phase later.  Group 0 stores its half of the tile in phase 2 nk (while
+    // group 1 computes the last step), group 1 in phase 2 nk + 1.  Each
+    // group runs its own straight-line loop (same barrier count per tile).
+    auto zero_acc = [&]() {
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j) acc[i][j] = i32x16{};
+    };
+    if (grp == 0) {
+        int g = 0;   // global index of the tile's first step
+        for (int ti = 0; ti < n_tiles; ++ti) {
+            GemmTile tl;
+            gemm_tile(ti, n, d_out, tl);
+            zero_acc();
+            for (int i = 0; i < nk; ++i) {
+                issue_next();                        // phase 2i
+                load_frags((g + i) % kStages);
+                phase_end();
+                compute_step();                      // phase 2i + 1
+                wait_step(g + i + 1);                // A of the next step
+                clear_ragged(i + 1 < nk ? i + 1 : 0, (g + i + 1) % kStages);
+                phase_end();
+            }
+            epilogue(tl, ti % kScaleSlots);          // phase 2 nk
+            phase_end();
+            phase_end();                             // phase 2 nk + 1
+            g += nk;
+        }
+    } else {
+        int g = 0;
+        for (int ti = 0; ti < n_tiles; ++ti) {
+            GemmTile tl;
+            gemm_tile(ti, n, d_out, tl);
+            zero_acc();
+            phase_end();                             // phase 0
+            for (int i = 0; i < nk; ++i) {
+                issue_next();                        // phase 2i + 1
+                load_frags((g + i) % kStages);
+                wait_step(g + i + 1);                // B of the next step
+                phase_end();
+                compute_step();                      // phase 2i + 2
+                phase_end();
+            }
+            epilogue(tl, ti % kScaleSlots);          // phase 2 nk + 1
+            phase_end();
+            g += nk;
+        }
     }
 }
 

@@ -47,7 +47,7 @@ def test_sqnr_zero_error_is_infinite():
 
 
 # ------------------------------------------------------------------ GEMM
-def _gemm_case(n, d_in, d_out, seed, zero_rows=()):
+def _gemm_case(n, d_in, d_out, seed, zero_rows=(), with_acc=True):
     torch = torch_mod()
     qx = wl.random_codes(n, d_in, seed)
     qw = wl.random_codes(d_out, d_in, seed + 1)
@@ -59,10 +59,10 @@ def _gemm_case(n, d_in, d_out, seed, zero_rows=()):
         sx[r] = 0
     acc_or, y_or = o.w4a4_linear(qx, sx, qw, sw)
     y = torch.empty((n, d_out), dtype=torch.float32, device="cuda")
-    acc = torch.empty((n, d_out), dtype=torch.int32, device="cuda")
+    acc = torch.empty((n, d_out), dtype=torch.int32, device="cuda") if with_acc else None
     cat.cat_w4a4_linear(dev(o.pack_int4(qx), "u8"), dev(sx, "f32"), dev(o.pack_int4(qw), "u8"),
                         dev(sw, "f32"), y, acc)
-    return host(acc), host(y), acc_or, y_or
+    return (host(acc) if with_acc else None), host(y), acc_or, y_or
 
 
 @pytest.mark.parametrize("n,d_in,d_out", [
@@ -74,6 +74,18 @@ def test_w4a4_linear_matches_oracle(n, d_in, d_out):
     assert np.array_equal(acc, acc_or)                 # int32 bit-exact
     assert rel_fro(y, y_or) <= 1e-3                    # the stated bar
     assert np.array_equal(y, y_or)                     # same fp32 epilogue order
+    assert not y[0].any()
+
+
+@pytest.mark.parametrize("n,d_in,d_out", [
+    (512, 256, 512), (256, 4096, 768), (300, 1024, 1000), (1, 32, 1), (257, 160, 300),
+    (768, 96, 256),
+])
+def test_w4a4_linear_without_acc_out_matches_oracle(n, d_in, d_out):
+    # without acc_out, full 256 x 256 tiles take a separate store path
+    say(f"w4a4 no acc_out n={n} d_in={d_in} d_out={d_out}")
+    _, y, _, y_or = _gemm_case(n, d_in, d_out, seed=3 * n + d_out, zero_rows=(0,), with_acc=False)
+    assert np.array_equal(y, y_or)
     assert not y[0].any()
 
 
@@ -109,10 +121,16 @@ def test_w4a4_linear_mlp_up_full_size_sampled():
     rng = np.random.default_rng(83)
     sx = rng.uniform(0.01, 1.0, n).astype(np.float32)
     sw = rng.uniform(0.01, 1.0, d_out).astype(np.float32)
+    dqx, dsx, dqw, dsw = dev(o.pack_int4(qx), "u8"), dev(sx, "f32"), dev(o.pack_int4(qw), "u8"), \
+        dev(sw, "f32")
+    # the benchmark's call passes no acc_out (full tiles take the straight-line
+    # store path); the second call also writes the int32 accumulators
+    y_fast = torch.empty((n, d_out), dtype=torch.float32, device="cuda")
+    cat.cat_w4a4_linear(dqx, dsx, dqw, dsw, y_fast)
     y = torch.empty((n, d_out), dtype=torch.float32, device="cuda")
     acc = torch.empty((n, d_out), dtype=torch.int32, device="cuda")
-    cat.cat_w4a4_linear(dev(o.pack_int4(qx), "u8"), dev(sx, "f32"), dev(o.pack_int4(qw), "u8"),
-                        dev(sw, "f32"), y, acc)
+    cat.cat_w4a4_linear(dqx, dsx, dqw, dsw, y, acc)
+    assert torch.equal(y_fast, y)
     rows = np.unique(np.concatenate([rng.choice(n, 62, replace=False), [0, n - 1]]))
     cols = np.unique(np.concatenate([rng.choice(d_out, 62, replace=False), [0, d_out - 1]]))
     acc_or, y_or = o.w4a4_linear(qx[rows], sx[rows], qw[cols], sw[cols])

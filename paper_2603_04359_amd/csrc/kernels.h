@@ -11,7 +11,10 @@
 namespace catk {
 
 // ---- SQNR (two passes)
-constexpr int kSqnrMaxBlocks = 2048;
+// Pass-1 grid cap: two 256-thread workgroups per CU of a 256-CU part.  A
+// sweep of the 8192 x 14336 pair read 6.8 TB/s at 384-512 workgroups and
+// 5.5-6.0 TB/s at 1024-2048 (more concurrent streams, worse DRAM locality).
+constexpr int kSqnrMaxBlocks = 512;
 int sqnr_grid(int64_t count);
 hipError_t launch_sqnr(const float* y, const float* yt, int64_t count, double* partials,
                        double* out, hipStream_t stream);

@@ -264,10 +264,11 @@ __global__ __launch_bounds__(kCovThreads) void cov_valu_kernel(const XT* __restr
 // For matrices of at least 256 channels (bf16, channel count a multiple
 // of 32).  Each workgroup (8 waves in a 2 x 4 grid, two per SIMD) works on
 // 256 x 256 tiles of the upper triangle; every wave keeps 128 x 64 fp32
-// partial sums (4 x 2 v_mfma_f32_32x32x16_bf16 accumulators).  With two
-// waves per SIMD one wave's MFMAs run while the other waits for its
-// fragment reads; the LDS (slab copies in, transposing reads out) is the
-// busiest unit.  Token slabs of 32 rows go from
+// partial sums (4 x 2 v_mfma_f32_32x32x16_bf16 accumulators).  Waves 0-3
+// and 4-7 (one of each per SIMD) run a ping-pong schedule one phase apart:
+// in a load phase a wave requests its operand's slab three slabs ahead
+// and reads all fragments of its next slab; in a compute phase it issues
+// that slab's 16 MFMAs at raised priority.  Token slabs of 32 rows go from
 // HBM straight into a 4-stage LDS ring with global_load_lds_dwordx4, in
 // X's own row-major order (no transposition on the way in): 512 bytes of
 // each token row per operand, 16-byte units XOR-swizzled by row.  The
@@ -293,7 +294,6 @@ static_assert(kSkStages >= 2 && kSkStages <= 4, "wait counts cover at most 2 sla
 constexpr int kSkRowUnits = kSkT / 8;            // 16-byte units per token row (32)
 constexpr int kSkOpUnits = kSkSlab * kSkRowUnits;  // units per operand and stage (1024)
 constexpr int kSkThreads = 512;                  // 8 waves: 2 x 4 over the tile
-constexpr int kSkLoads = kSkOpUnits / kSkThreads;  // direct loads per thread and operand (2)
 constexpr int kSkMaxSlabs = 256;                 // slabs per launch (8192 tokens)
 constexpr int64_t kSkSlotFloats = int64_t(kSkT) * kSkT;   // one 256 x 256 fp32 tile
 
@@ -311,15 +311,15 @@ struct SkGeom {
 __device__ __forceinline__ int64_t sk_begin(const SkGeom& g, int64_t w) { return g.U * w / g.G; }
 
 // The k-th upper-triangle tile of a T x T tile grid in super-tile order:
-// 4 x 4 groups of tiles (row-major over the upper triangle of groups),
+// 8 x 8 groups of tiles (row-major over the upper triangle of groups),
 // row-major inside a group.  Consecutive tiles then share few distinct
 // 256-channel blocks of X, which is what one XCD's L2 holds.
 __device__ __forceinline__ void st_decode(int64_t r, int64_t T, int64_t& I, int64_t& J) {
-    const int64_t Ts = (T + 3) / 4;
+    const int64_t Ts = (T + 7) / 8;
     for (int64_t P = 0; P < Ts; ++P)
         for (int64_t Q = P; Q < Ts; ++Q) {
-            const int64_t i0 = 4 * P, i1 = (4 * P + 4 < T) ? 4 * P + 4 : T;
-            const int64_t j0 = 4 * Q, j1 = (4 * Q + 4 < T) ? 4 * Q + 4 : T;
+            const int64_t i0 = 8 * P, i1 = (8 * P + 8 < T) ? 8 * P + 8 : T;
+            const int64_t j0 = 8 * Q, j1 = (8 * Q + 8 < T) ? 8 * Q + 8 : T;
             const int64_t m = i1 - i0;
             const int64_t cnt = P == Q ? m * (m + 1) / 2 : m * (j1 - j0);
             if (r < cnt) {
@@ -366,7 +366,7 @@ __global__ __launch_bounds__(kSkThreads, 1) void cov_sk_kernel(const uint16_t* _
 
     const int tid = threadIdx.x;
     const int lane = tid & (kWave - 1);
-    const int wave = tid / kWave;
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);   // uniform: SGPR branches
     const int wm = wave >> 2, wn = wave & 3;   // wave tile 128 x 64
     const int l32 = lane & 31;
     const int h = lane >> 5;
@@ -380,27 +380,20 @@ __global__ __launch_bounds__(kSkThreads, 1) void cov_sk_kernel(const uint16_t* _
     const int64_t t_first = u_begin / g.S, t_last = (u_end - 1) / g.S;
     const bool head_first = (u_begin % g.S) != 0 && t_last > t_first;
 
-    // direct-load geometry: load q of this thread fills unit (q*8+wave)*64+lane
-    // of an operand stage, i.e. token row 16q + rr, swizzled position l32.
-    const int rr = 2 * wave + h;
+    // Ping-pong: waves 0-3 (rows 0-127 of the tile, one per SIMD) and waves
+    // 4-7 (rows 128-255) are one phase apart.  In a load phase a wave
+    // requests its operand's slab three slabs ahead (waves 0-3 operand A,
+    // waves 4-7 operand B, which a diagonal tile does not load) and reads
+    // all fragments of its next slab; in a compute phase it issues that
+    // slab's 16 MFMAs.  On every SIMD one wave computes while the other
+    // loads.
+    const int grp = wave >> 2, w4 = wave & 3;
+    // direct-load geometry: load q of this thread fills unit (4q+w4)*64+lane
+    // of its operand's stage, i.e. token row 8q + rr, swizzled position l32.
+    const int rr = 2 * w4 + h;
     const int unit = l32 ^ ((rr & 3) << 2);      // global 16-byte unit of the row
     const uint32_t row_bytes = static_cast<uint32_t>(d) * 2u;
-
-    // fragment-read geometry (bytes inside one operand stage)
-    const int i16 = lane & 15, e = i16 >> 2, qq = i16 & 3, gg = (lane >> 4) & 1;
-    uint32_t offA[4], offB[2];
-#pragma unroll
-    for (int a = 0; a < 4; ++a) {
-        const int row = 8 * h + e;                 // token row inside the 16-token step
-        const int ua = (wm * 16 + 4 * a + 2 * gg + (qq >> 1)) ^ ((row & 3) << 2);
-        offA[a] = row * (kSkT * 2) + 16 * ua + 8 * (qq & 1);
-    }
-#pragma unroll
-    for (int b = 0; b < 2; ++b) {
-        const int row = 8 * h + e;
-        const int ub = (wn * 8 + 4 * b + 2 * gg + (qq >> 1)) ^ ((row & 3) << 2);
-        offB[b] = row * (kSkT * 2) + 16 * ub + 8 * (qq & 1);
-    }
+    constexpr int kPpLoads = kSkOpUnits / (kSkThreads / 2);   // 4
 
     for (int64_t idx = 0; u_begin < u_end && idx <= t_last - t_first; ++idx) {
         // tiles in order of their first slab: t_first + 1 .. t_last, then t_first
@@ -416,117 +409,141 @@ __global__ __launch_bounds__(kSkThreads, 1) void cov_sk_kernel(const uint16_t* _
         const int64_t I0 = I * kSkT, J0 = J * kSkT;
         const bool diag = I == J;
         float* accm = acc + (mode == CAT_COV_FULL ? 0 : mat * k * k);
+        // this wave's operand: A (rows I0..) for group 0, B (J0..) for group 1
+        const bool loads = grp == 0 || !diag;
+        const int op = grp;
 
-        // per-thread source byte offsets inside a slab (columns clamped into
+        // per-thread source byte offset inside a slab (columns clamped into
         // the matrix when the last tile is ragged: those rows/columns of the
         // result are discarded)
-        int64_t ca = I0 + 8 * unit, cb = J0 + 8 * unit;
-        if (ca >= g.dim) ca = I0;
-        if (cb >= g.dim) cb = J0;
-        const uint32_t oa = static_cast<uint32_t>(rr) * row_bytes + static_cast<uint32_t>(colbase + ca) * 2u;
-        const uint32_t ob = static_cast<uint32_t>(rr) * row_bytes + static_cast<uint32_t>(colbase + cb) * 2u;
+        int64_t cx = (grp == 0 ? I0 : J0) + 8 * unit;
+        if (cx >= g.dim) cx = grp == 0 ? I0 : J0;
+        const uint32_t ox = static_cast<uint32_t>(rr) * row_bytes + static_cast<uint32_t>(colbase + cx) * 2u;
+        const uint32_t lx = static_cast<uint32_t>(
+            __builtin_amdgcn_readfirstlane(lds_addr(&ring[0][op][w4 * 64])));
 
         auto issue = [&](int64_t s, int st) {
+            if (!loads) return;
             const int64_t t0 = s * kSkSlab;
             const char* base = reinterpret_cast<const char*>(X + t0 * d);
-            const uint32_t la = lds_addr(&ring[st][0][wave * 64]);
-            const uint32_t lb = lds_addr(&ring[st][1][wave * 64]);
+            const uint32_t l = lx + static_cast<uint32_t>(st) * (2 * kSkOpUnits * 16);
             if (t0 + kSkSlab <= n) {
 #pragma unroll
-                for (int q = 0; q < kSkLoads; ++q) dma16(base, oa + q * 16u * row_bytes, la + q * 8192u);
-                if (!diag) {
-#pragma unroll
-                    for (int q = 0; q < kSkLoads; ++q)
-                        dma16(base, ob + q * 16u * row_bytes, lb + q * 8192u);
-                }
+                for (int q = 0; q < kPpLoads; ++q) dma16(base, ox + q * 8u * row_bytes, l + q * 4096u);
             } else {
                 // ragged last slab: rows past n load row n-1 (zeroed once landed)
 #pragma unroll
-                for (int q = 0; q < kSkLoads; ++q) {
-                    const int64_t t = t0 + 16 * q + rr;
+                for (int q = 0; q < kPpLoads; ++q) {
+                    const int64_t t = t0 + 8 * q + rr;
                     const uint32_t back = t < n ? 0u : static_cast<uint32_t>(t - (n - 1)) * row_bytes;
-                    dma16(base, oa + q * 16u * row_bytes - back, la + q * 8192u);
-                    if (!diag) dma16(base, ob + q * 16u * row_bytes - back, lb + q * 8192u);
+                    dma16(base, ox + q * 8u * row_bytes - back, l + q * 4096u);
                 }
             }
         };
-
+        // this thread's loads of slab s have landed once at most those of the
+        // slabs issued after it (up to `last`) are outstanding; rows past n of
+        // a ragged slab are then zeroed by the thread that loaded them
+        auto wait_slab = [&](int64_t s, int64_t last) {
+            if (!loads || s >= s1) return;
+            const int64_t ahead = last - s;
+            if (ahead >= 2) wait_vmcnt<2 * kPpLoads>();
+            else if (ahead == 1) wait_vmcnt<kPpLoads>();
+            else wait_vmcnt<0>();
+            const int64_t t0 = s * kSkSlab;
+            if (t0 + kSkSlab > n) {
+                const int sl = static_cast<int>((s - s0) % kSkStages);
+#pragma unroll
+                for (int q = 0; q < kPpLoads; ++q)
+                    if (t0 + 8 * q + rr >= n)
+                        ring[sl][op][(q * 4 + w4) * 64 + lane] = u32x4{0u, 0u, 0u, 0u};
+            }
+        };
+        auto last_issued = [&](int64_t s) {   // last slab requested once slab s's load phase ran
+            return (s + kSkStages - 1 < s1 - 1) ? s + kSkStages - 1 : s1 - 1;
+        };
+        typedef const char __attribute__((address_space(3))) * lds_cptr;
+        bf16x8 fa[2][4], fb[2][2];
+        auto read_frags = [&](int sl) {
+            // fragment-read geometry (bytes inside one operand stage),
+            // recomputed per call from a lane index the compiler cannot
+            // hoist: kept live across the loop it would spill
+            int el = lane;
+            asm volatile("" : "+v"(el));
+            const int i16 = el & 15, e = i16 >> 2, qq = i16 & 3, gg = (el >> 4) & 1, hh = el >> 5;
+            const int row = 8 * hh + e;             // token row inside the 16-token step
+            const uint32_t rowoff = static_cast<uint32_t>(row * (kSkT * 2) + 8 * (qq & 1));
+            const int usw = (row & 3) << 2;
+            lds_cptr baseA = (lds_cptr)&ring[sl][0][0];
+            lds_cptr baseB = (lds_cptr)&ring[sl][diag ? 0 : 1][0];
+#pragma unroll
+            for (int kk = 0; kk < 2; ++kk) {
+#pragma unroll
+                for (int a = 0; a < 4; ++a) {
+                    const int ua = (wm * 16 + 4 * a + 2 * gg + (qq >> 1)) ^ usw;
+                    fa[kk][a] = sk_frag(baseA, rowoff + 16 * ua + kk * 16 * kSkT * 2);
+                }
+#pragma unroll
+                for (int b = 0; b < 2; ++b) {
+                    const int ub = (wn * 8 + 4 * b + 2 * gg + (qq >> 1)) ^ usw;
+                    fb[kk][b] = sk_frag(baseB, rowoff + 16 * ub + kk * 16 * kSkT * 2);
+                }
+            }
+        };
         f32x16 part[4][2];
 #pragma unroll
         for (int a = 0; a < 4; ++a)
 #pragma unroll
             for (int b = 0; b < 2; ++b) part[a][b] = f32x16{};
-
-        // Software pipeline: the fragments of the first 16 tokens of slab
-        // s + 1 are read right after the barrier that publishes the slab,
-        // while the MFMAs of the second half of slab s still run.
-        // Wait until this thread's loads of slab s have landed: at most the
-        // loads of the slabs issued after it (up to slab `last`) may still be
-        // outstanding.
-        auto wait_slab = [&](int64_t s, int64_t last) {
-            const int64_t ahead = last - s;
-            if (diag) {
-                if (ahead >= 2) wait_vmcnt<2 * kSkLoads>();
-                else if (ahead == 1) wait_vmcnt<kSkLoads>();
-                else wait_vmcnt<0>();
-            } else {
-                if (ahead >= 2) wait_vmcnt<4 * kSkLoads>();
-                else if (ahead == 1) wait_vmcnt<2 * kSkLoads>();
-                else wait_vmcnt<0>();
-            }
-            const int64_t t0 = s * kSkSlab;
-            if (t0 + kSkSlab > n) {
-                // ragged last slab: rows past n were loaded clamped; zero them
-                const int sl = static_cast<int>((s - s0) % kSkStages);
+        auto mfmas = [&]() {
+            __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-                for (int q = 0; q < kSkLoads; ++q) {
-                    if (t0 + 16 * q + rr >= n) {
-                        ring[sl][0][(q * 8 + wave) * 64 + lane] = u32x4{0u, 0u, 0u, 0u};
-                        if (!diag) ring[sl][1][(q * 8 + wave) * 64 + lane] = u32x4{0u, 0u, 0u, 0u};
-                    }
-                }
-            }
+            for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+                for (int a = 0; a < 4; ++a)
+#pragma unroll
+                    for (int b = 0; b < 2; ++b)
+                        part[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[kk][a], fb[kk][b],
+                                                                             part[a][b], 0, 0, 0);
+            __builtin_amdgcn_s_setprio(0);
         };
-        typedef const char __attribute__((address_space(3))) * lds_cptr;
-        auto read_frags = [&](int sl, int kk, bf16x8* fa, bf16x8* fb) {
-            lds_cptr baseA = (lds_cptr)&ring[sl][0][0];
-            lds_cptr baseB = (lds_cptr)&ring[sl][diag ? 0 : 1][0];
-#pragma unroll
-            for (int a = 0; a < 4; ++a) fa[a] = sk_frag(baseA, offA[a] + kk * 16 * kSkT * 2);
-#pragma unroll
-            for (int b = 0; b < 2; ++b) fb[b] = sk_frag(baseB, offB[b] + kk * 16 * kSkT * 2);
-        };
-        auto mfmas = [&](const bf16x8* fa, const bf16x8* fb) {
-#pragma unroll
-            for (int a = 0; a < 4; ++a)
-#pragma unroll
-                for (int b = 0; b < 2; ++b)
-                    part[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[a], fb[b], part[a][b],
-                                                                         0, 0, 0);
+        auto phase_end = [&]() {
+            __builtin_amdgcn_sched_barrier(0);
+            lds_barrier();
+            __builtin_amdgcn_sched_barrier(0);
         };
 
+        // prologue: slabs s0 .. s0 + 2 requested, s0 landed and published
 #pragma unroll
         for (int p = 0; p < kSkStages - 1; ++p)
             if (s0 + p < s1) issue(s0 + p, p);
         wait_slab(s0, (s0 + kSkStages - 2 < s1 - 1) ? s0 + kSkStages - 2 : s1 - 1);
         lds_barrier();
-        bf16x8 fa0[4], fb0[2], fa1[4], fb1[2];
-        read_frags(0, 0, fa0, fb0);
-        int st = 0;
-        for (int64_t s = s0; s < s1; ++s) {
-            read_frags(st, 1, fa1, fb1);
-            mfmas(fa0, fb0);
-            const int nx = st == kSkStages - 1 ? 0 : st + 1;
-            if (s + 1 < s1) {
-                // slabs issued so far: up to s + kSkStages - 2
-                wait_slab(s + 1, (s + kSkStages - 2 < s1 - 1) ? s + kSkStages - 2 : s1 - 1);
-                lds_barrier();   // slab s+1 landed everywhere; slab s-1 fully consumed
+        // 2 (s1 - s0) + 1 phases: group 0 loads slab i in phase 2i and computes
+        // it in phase 2i + 1; group 1 one phase later
+        if (grp == 0) {
+            for (int64_t s = s0; s < s1; ++s) {
+                const int st = static_cast<int>((s - s0) % kSkStages);
                 if (s + kSkStages - 1 < s1)
                     issue(s + kSkStages - 1, st == 0 ? kSkStages - 1 : st - 1);
-                read_frags(nx, 0, fa0, fb0);
+                read_frags(st);
+                phase_end();
+                mfmas();
+                wait_slab(s + 1, last_issued(s));          // A of the next slab
+                phase_end();
             }
-            mfmas(fa1, fb1);
-            st = nx;
+            phase_end();
+        } else {
+            phase_end();
+            for (int64_t s = s0; s < s1; ++s) {
+                const int st = static_cast<int>((s - s0) % kSkStages);
+                if (s + kSkStages - 1 < s1)
+                    issue(s + kSkStages - 1, st == 0 ? kSkStages - 1 : st - 1);
+                read_frags(st);
+                wait_slab(s + 1, last_issued(s));          // B of the next slab
+                phase_end();
+                mfmas();
+                phase_end();
+            }
         }
 
         // Partial sums out.  A whole tile is added into acc (upper tile,
@@ -553,14 +570,19 @@ __global__ __launch_bounds__(kSkThreads, 1) void cov_sk_kernel(const uint16_t* _
             for (int half = 0; half < 2; ++half) {
                 lds_barrier();
                 if (wm == half) {
+                    // one base per 32-row group keeps every offset inside the
+                    // 64 KiB immediate range of an LDS store
+                    int el = lane;
+                    asm volatile("" : "+v"(el));
 #pragma unroll
-                    for (int a = 0; a < 4; ++a)
+                    for (int a = 0; a < 4; ++a) {
+                        float* sa = stage + (32 * a + 4 * (el >> 5)) * kSkT + wn * 64 + (el & 31);
 #pragma unroll
                         for (int b = 0; b < 2; ++b)
 #pragma unroll
                             for (int r = 0; r < 16; ++r)
-                                stage[(32 * a + 8 * (r >> 2) + 4 * h + (r & 3)) * kSkT + wn * 64 +
-                                      32 * b + l32] = part[a][b][r];
+                                sa[(8 * (r >> 2) + (r & 3)) * kSkT + 32 * b] = part[a][b][r];
+                    }
                 }
                 lds_barrier();
                 // 128 rows x 64 float4 per row; thread tid takes column group

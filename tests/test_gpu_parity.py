@@ -89,6 +89,31 @@ def test_w4a4_linear_without_acc_out_matches_oracle(n, d_in, d_out):
     assert not y[0].any()
 
 
+@pytest.mark.parametrize("d_in", [96, 224])
+def test_w4a4_linear_many_short_tiles_per_workgroup(d_in):
+    # 8192 x 8192 outputs = 1024 tiles, four per workgroup, each only one or
+    # two K steps deep: the scale slots and the operand stream roll over
+    # from tile to tile every step or two
+    torch = torch_mod()
+    n = d_out = 8192
+    say(f"w4a4 short tiles n={n} d_in={d_in} d_out={d_out}")
+    qx = wl.random_codes(n, d_in, seed=d_in)
+    qw = wl.random_codes(d_out, d_in, seed=d_in + 1)
+    rng = np.random.default_rng(d_in + 2)
+    sx = rng.uniform(0.01, 1.0, n).astype(np.float32)
+    sw = rng.uniform(0.01, 1.0, d_out).astype(np.float32)
+    acc_or, y_or = o.w4a4_linear(qx, sx, qw, sw)
+    args = (dev(o.pack_int4(qx), "u8"), dev(sx, "f32"), dev(o.pack_int4(qw), "u8"), dev(sw, "f32"))
+    y = torch.empty((n, d_out), dtype=torch.float32, device="cuda")
+    acc = torch.empty((n, d_out), dtype=torch.int32, device="cuda")
+    cat.cat_w4a4_linear(*args, y, acc)
+    assert np.array_equal(host(acc), acc_or)
+    assert np.array_equal(host(y), y_or)
+    y2 = torch.empty((n, d_out), dtype=torch.float32, device="cuda")
+    cat.cat_w4a4_linear(*args, y2)
+    assert torch.equal(y2, y)
+
+
 def test_w4a4_linear_extreme_codes_at_max_d_in():
     torch = torch_mod()
     d_in = B.CAT_MAX_D_IN

@@ -134,7 +134,16 @@ int cat_cov_accumulate(const void* X, int x_dtype, int64_t n, int64_t d,
  * s_x      device fp32 [n] (written).
  * workspace / workspace_bytes: device scratch of at least
  *          cat_transform_quant_workspace_bytes(n, d, k) bytes; its
- *          contents on entry are ignored and on exit undefined.
+ *          contents on entry are ignored and on exit undefined.  One
+ *          workspace must not be used by calls that run concurrently.
+ * Capture: the call may be captured into a HIP graph and replayed (it
+ *          enqueues kernels only; a captured call also enqueues a one-thread
+ *          kernel that renews the exchange tag for every replay).
+ * The d = 4096, k = 128 bf16 path exchanges row maxima between
+ * workgroups of the same launch with bounded waits.  If a wait ever runs
+ * out (the launch's workgroups were kept from running together for
+ * seconds), the tokens concerned get s_x = NaN and zero codes rather than a
+ * wrong scale.
  */
 size_t cat_transform_quant_workspace_bytes(int64_t n, int64_t d, int64_t k);
 int cat_transform_quant(const void* X, int x_dtype, int64_t n, int64_t d,

@@ -427,7 +427,9 @@ __global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
 // either an old word (another tag) or the whole new one and the workspace
 // needs no clearing between calls.  Tags have bit 31 set, which no
 // absolute-value float pattern has, so 32-bit maxima left by the two-pass
-// path never look published either.  P(j, t) lives at
+// path never look published either.  Eager calls take the tag from a host
+// counter; a call captured into a graph takes it from a word a one-thread
+// kernel advances before every replay (see launch_tq_fused).  P(j, t) lives at
 // ((t / 16) * 32 + j) * 16 + t % 16 (16 tokens of a block fill one 128-byte
 // line), F(t) at 32 n' + t.
 //
@@ -446,7 +448,8 @@ __global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
 // launch_tq_fused) and every workgroup of a token-tile row visits its tiles
 // in the same order, so a workgroup only waits for peers that are running
 // or about to run.  Waits are still bounded: after kTqSpinLimit polls the
-// gather wave records a timeout flag and goes on.
+// gather wave records a timeout flag and goes on with a NaN maximum, which
+// makes the affected scales NaN.
 constexpr uint32_t kTqSpinLimit = 1u << 22;
 constexpr int kFqCompute = 4;                   // compute waves
 constexpr int kFqCopy = 2;                      // copy waves
@@ -464,7 +467,22 @@ static_assert(kFqTT == 2 * kFqBlocks, "each workgroup reduces two tokens of a ti
 struct TqFusedWs {
     uint64_t* pmax;       // P words, then F words (see above)
     uint32_t* flag;       // timeout flag (0 = fine)
+    // The call's tag: the host's when tag_word is NULL, else the word a
+    // preceding tq_device_tag_kernel wrote (calls captured into a graph,
+    // where every replay must publish under a tag of its own).
+    const uint32_t* tag_word;
 };
+
+// Advances the device-side tag in the workspace: one per replay of a
+// captured call.  Device tags have bits 31 and 30 set, host tags bit 31
+// only, so the two never collide; any previous content is a valid start.
+__global__ void tq_device_tag_kernel(uint32_t* word) {
+    if (threadIdx.x == 0) {
+        const uint32_t old = __hip_atomic_load(word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(word, 0xC0000000u | ((old + 1u) & 0x3FFFFFFFu), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
 
 // MFMA row i of a 32-row group -> output row within the group
 __device__ __forceinline__ int fq_row(int i) {
@@ -534,8 +552,11 @@ __device__ __forceinline__ void fq_wait_copies(int later) {
 
 __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ T, int64_t n, int64_t d,
-    int64_t R, TqFusedWs ws, uint32_t tag, uint8_t* __restrict__ codes,
+    int64_t R, TqFusedWs ws, uint32_t host_tag, uint8_t* __restrict__ codes,
     float* __restrict__ s_x) {
+    const uint32_t tag = ws.tag_word ? __hip_atomic_load(ws.tag_word, __ATOMIC_RELAXED,
+                                                         __HIP_MEMORY_SCOPE_AGENT)
+                                     : host_tag;
     constexpr int K = 128;
     constexpr int NS = K / 16;          // 16-deep MFMA steps
     static_assert(kFqTT == 64 && kFqCompute == 4, "compute waves: 2 token halves x 2 row halves");
@@ -593,11 +614,14 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
         auto load = [&](const uint64_t* a) {
             return __hip_atomic_load(a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         };
+        // A wait that runs out yields a quiet NaN: as bits it exceeds every
+        // finite maximum, so it survives both reduction levels, and the
+        // tokens concerned get s_x = NaN instead of a silently wrong scale.
         auto await = [&](uint64_t v, const uint64_t* a) {
             for (uint32_t polls = 0; (v >> 32) != tag;) {
                 if (++polls >= kTqSpinLimit) {
                     __hip_atomic_store(ws.flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    break;
+                    return 0x7FC00000u;
                 }
                 __builtin_amdgcn_s_sleep(1);
                 v = load(a);
@@ -757,7 +781,8 @@ hipError_t launch_tq_ring(const uint16_t* X, int64_t n, int64_t d, const uint16_
 // Workspace layout (bytes): [0, P) per-token words (two-pass path: one
 // 32-bit running maximum per token; single-pass path: d/128 64-bit tagged
 // block maxima and one tagged row maximum per token, n rounded up to 16,
-// P = 8 n' (max(1, d / 128) + 1)), then the 32-bit timeout flag.
+// P = 8 n' (max(1, d / 128) + 1)), then a 256-byte tail: the 32-bit
+// timeout flag at +0 and the device-side tag of captured calls at +64.
 static int64_t tq_nbj_max(int64_t d) { return d / 128 > 1 ? d / 128 : 1; }
 static size_t tq_flag_offset(int64_t n, int64_t d) {
     return static_cast<size_t>((n + 15) / 16 * 16 * 8 * (tq_nbj_max(d) + 1));
@@ -770,7 +795,7 @@ size_t tq_workspace_bytes(int64_t n, int64_t d, int64_t k) {
 
 static uint32_t next_tq_tag() {
     static std::atomic<uint32_t> tag{0};
-    return 0x80000000u | (++tag & 0x7FFFFFFFu);
+    return 0x80000000u | (++tag & 0x3FFFFFFFu);
 }
 
 // Resident workgroups of tq_fused_kernel on a device (CUs x blocks per CU
@@ -818,7 +843,22 @@ hipError_t launch_tq_fused(const uint16_t* X, int64_t n, int64_t d, const uint16
     TqFusedWs w;
     w.pmax = reinterpret_cast<uint64_t*>(ws);
     w.flag = reinterpret_cast<uint32_t*>(ws + tq_flag_offset(n, d));
-    const uint32_t tag = next_tq_tag();
+    w.tag_word = nullptr;
+    uint32_t tag = 0;
+    hipStreamCaptureStatus capture = hipStreamCaptureStatusNone;
+    err = hipStreamIsCapturing(stream, &capture);
+    if (err != hipSuccess) return err;
+    if (capture != hipStreamCaptureStatusNone) {
+        // captured: the tag has to change with every replay, so it is made
+        // on the device, in the workspace tail next to the timeout flag
+        uint32_t* word = reinterpret_cast<uint32_t*>(ws + tq_flag_offset(n, d) + 64);
+        hipLaunchKernelGGL(tq_device_tag_kernel, dim3(1), dim3(kWave), 0, stream, word);
+        err = hipGetLastError();
+        if (err != hipSuccess) return err;
+        w.tag_word = word;
+    } else {
+        tag = next_tq_tag();
+    }
     hipLaunchKernelGGL(tq_fused_kernel, dim3(static_cast<uint32_t>(nbj * R)), dim3(kFqThreads),
                        0, stream, X, T, n, d, R, w, tag, codes, s_x);
     err = hipGetLastError();

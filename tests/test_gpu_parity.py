@@ -327,6 +327,46 @@ def test_transform_quant_workspace_reuse_across_paths():
     assert int(host(ws[wsb - 256:wsb - 252].view(torch.int32))[0]) == 0
 
 
+def test_transform_quant_graph_replays_see_fresh_inputs():
+    # A captured single-pass call replayed with new activations each time:
+    # every replay must publish under a tag of its own (made on the device),
+    # and eager calls on the same workspace in between (host tags) must not
+    # mix with it.  The workspace starts with whatever memory holds.
+    say("tq graph capture: 4 replays with new X, eager calls between")
+    torch = torch_mod()
+    n, d, k = 300, 4096, 128
+    T = _rand_T(d, k, seed=21)
+    dT = dev(T, "bf16")
+    Xs = [_mlp_up_X(n, seed=30 + i) for i in range(4)]
+    Xs[2] = Xs[2] * 2.0 ** -6
+    dX = dev(Xs[0], "bf16")
+    wsb = cat.cat_transform_quant_workspace_bytes(n, d, k)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    ws[wsb - 256:wsb - 252].zero_()   # only the timeout word, to read it afterwards
+    codes = torch.empty((n, d // 2), dtype=torch.uint8, device="cuda")
+    s_x = torch.empty(n, dtype=torch.float32, device="cuda")
+    cat.cat_transform_quant(dX, dT, k, codes, s_x, ws)      # eager warm-up
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    with torch.cuda.graph(g, stream=side):
+        cat.cat_transform_quant(dX, dT, k, codes, s_x, ws)
+    codes_e = torch.empty_like(codes)
+    s_x_e = torch.empty_like(s_x)
+    for i, X in enumerate(Xs):
+        dX.copy_(dev(X, "bf16"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        c, sx = host(codes), host(s_x)
+        _, _, s_or = check_codes(c, X, T, label=f"replay {i}")
+        _check_scales(sx, s_or, f"replay {i}")
+        cat.cat_transform_quant(dX, dT, k, codes_e, s_x_e, ws)   # eager, same workspace
+        torch.cuda.synchronize()
+        assert np.array_equal(host(codes_e), c) and np.array_equal(host(s_x_e), sx)
+    assert int(host(ws[wsb - 256:wsb - 252].view(torch.int32))[0]) == 0
+
+
 # ------------------------------------------------------- second moment
 def _cov_gpu(X, dtype, mode, k, acc0=None, splits=None):
     torch = torch_mod()

@@ -560,3 +560,62 @@ def test_single_pass_transform_quant_at_addresses_with_bit31_set():
     _, _, s_or = check_codes(codes, X, T, label="bit31 single pass")
     _check_scales(s, s_or, "bit31 single pass")
     del keep
+
+
+def test_whole_step_graph_replays_match_eager():
+    # transform_quant (single-pass shape), GEMM, SQNR and a full Sigma_x
+    # accumulation captured once and replayed with new activations; every
+    # replay must equal the same calls run eagerly, bit for bit (all four
+    # kernels are deterministic)
+    say("whole step under graph capture: 3 replays vs eager")
+    torch = torch_mod()
+    n, d_in, d_out, k = 512, 4096, 1024, 128
+    T = _rand_T(d_in, k, seed=41)
+    dT = dev(T, "bf16")
+    qw = wl.random_codes(d_out, d_in, seed=42)
+    rng = np.random.default_rng(43)
+    dqw = dev(o.pack_int4(qw), "u8")
+    dsw = dev(rng.uniform(0.01, 1.0, d_out).astype(np.float32), "f32")
+    Xs = [_mlp_up_X(n, seed=50 + i) for i in range(3)]
+    dy = dev(rng.standard_normal((n, d_out)).astype(np.float32), "f32")
+
+    def buffers():
+        return dict(
+            codes=torch.empty((n, d_in // 2), dtype=torch.uint8, device="cuda"),
+            s_x=torch.empty(n, dtype=torch.float32, device="cuda"),
+            yt=torch.empty((n, d_out), dtype=torch.float32, device="cuda"),
+            out=torch.empty(3, dtype=torch.float64, device="cuda"),
+            acc=torch.zeros((d_in, d_in), dtype=torch.float32, device="cuda"),
+            tq_ws=torch.empty(cat.cat_transform_quant_workspace_bytes(n, d_in, k),
+                              dtype=torch.uint8, device="cuda"),
+            sq_ws=torch.empty(cat.cat_sqnr_workspace_bytes(n * d_out), dtype=torch.uint8,
+                              device="cuda"),
+            cov_ws=torch.empty(max(16, cat.cat_cov_workspace_bytes(B.CAT_BF16, n, d_in,
+                                                                   B.CAT_COV_FULL, 1)),
+                               dtype=torch.uint8, device="cuda"))
+
+    def step(dX, b):
+        cat.cat_transform_quant(dX, dT, k, b["codes"], b["s_x"], b["tq_ws"])
+        cat.cat_w4a4_linear(b["codes"], b["s_x"], dqw, dsw, b["yt"])
+        cat.cat_sqnr(dy, b["yt"], b["sq_ws"], b["out"])
+        cat.cat_cov_accumulate(dX, b["acc"], B.CAT_COV_FULL, 1, workspace=b["cov_ws"])
+
+    dX = dev(Xs[0], "bf16")
+    g_b, e_b = buffers(), buffers()
+    step(dX, g_b)                      # warm-up
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    with torch.cuda.graph(graph, stream=side):
+        step(dX, g_b)
+    for i, X in enumerate(Xs):
+        dX.copy_(dev(X, "bf16"))
+        g_b["acc"].zero_()
+        e_b["acc"].zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        step(dX, e_b)
+        torch.cuda.synchronize()
+        for key in ("codes", "s_x", "yt", "out", "acc"):
+            assert torch.equal(g_b[key], e_b[key]), f"replay {i}: {key}"

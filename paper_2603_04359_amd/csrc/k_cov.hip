@@ -668,12 +668,33 @@ __global__ __launch_bounds__(kCovThreads) void cov_combine_kernel(float* __restr
                   : f32x4{0.f, 0.f, 0.f, 0.f};
     }
     if (!whole) {
-        for (int64_t w = w_lo; w <= w_hi; ++w) {
+        auto slot_of = [&](int64_t w) {
             const int64_t t_first = sk_begin(g, w) / g.S;
-            const float* slot = ws + (w * 2 + (tile == t_first ? 0 : 1)) * kSkSlotFloats;
+            return ws + (w * 2 + (tile == t_first ? 0 : 1)) * kSkSlotFloats;
+        };
+        int64_t w = w_lo;
+        // two pieces per round: all their loads in flight before the adds,
+        // which keep the share order
+        for (; w + 1 <= w_hi; w += 2) {
+            const float* s0 = slot_of(w);
+            const float* s1 = slot_of(w + 1);
+            f32x4 p0[4], p1[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                p0[i] = *reinterpret_cast<const f32x4*>(s0 + (sr + rl + 16 * i) * kSkT + sc + cl);
+                p1[i] = *reinterpret_cast<const f32x4*>(s1 + (sr + rl + 16 * i) * kSkT + sc + cl);
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                v[i] += p0[i];
+                v[i] += p1[i];
+            }
+        }
+        if (w <= w_hi) {
+            const float* s0 = slot_of(w);
 #pragma unroll
             for (int i = 0; i < 4; ++i)
-                v[i] += *reinterpret_cast<const f32x4*>(slot + (sr + rl + 16 * i) * kSkT + sc + cl);
+                v[i] += *reinterpret_cast<const f32x4*>(s0 + (sr + rl + 16 * i) * kSkT + sc + cl);
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {

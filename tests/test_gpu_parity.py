@@ -619,3 +619,78 @@ def test_whole_step_graph_replays_match_eager():
         torch.cuda.synchronize()
         for key in ("codes", "s_x", "yt", "out", "acc"):
             assert torch.equal(g_b[key], e_b[key]), f"replay {i}: {key}"
+
+
+@pytest.mark.parametrize("name,k", [("attn4096", 128), ("mlp_down", 256), ("stress", 128),
+                                    ("stress", 512)])
+def test_full_size_layer_shapes_sampled(name, k):
+    # Every kernel at a layer's full dimensions and token counts, with the
+    # layer's own activation structure; checked on samples the oracle
+    # computes one by one (tokens, a 64 x 64 output block, a 64 x 64 block
+    # of the second moment) and, for SQNR, on all entries in fp64 chunks.
+    torch = torch_mod()
+    cfg = wl.get_config(name, k=k)
+    n, d_in, d_out = cfg.n, cfg.d_in, cfg.d_out
+    say(f"full size {name}: {n} x {d_in} -> {d_out}, k={k}, n_cal={cfg.n_cal}")
+    L = wl.make_layer(cfg, seed=7, with_weights=False)
+    X_cal, X = L["X_cal"], L["X"]
+    rng = np.random.default_rng(sum(map(ord, name)) + k)
+    rows = np.unique(np.concatenate([rng.choice(n, 62, replace=False), [0, n - 1]]))
+
+    # transform + quantize over all n tokens; sampled tokens against the oracle
+    T = _rand_T(d_in, k, seed=k)
+    dX = dev(X, "bf16")
+    codes = torch.empty((n, d_in // 2), dtype=torch.uint8, device="cuda")
+    s_x = torch.empty(n, dtype=torch.float32, device="cuda")
+    ws = torch.empty(cat.cat_transform_quant_workspace_bytes(n, d_in, k), dtype=torch.uint8,
+                     device="cuda")
+    cat.cat_transform_quant(dX, dev(T, "bf16"), k, codes, s_x, ws)
+    dr = torch.from_numpy(rows).cuda()
+    c_rows, s_rows = host(codes[dr]), host(s_x[dr])
+    _, _, s_or = check_codes(c_rows, X[rows].astype(np.float64), T, label=f"{name} tq rows")
+    _check_scales(s_rows, s_or, f"{name} tq rows")
+
+    # GEMM on those codes against random weight codes; sampled block exact
+    qw = wl.random_codes(d_out, d_in, seed=k + 1)
+    sw = rng.uniform(0.01, 1.0, d_out).astype(np.float32)
+    dqw, dsw = dev(o.pack_int4(qw), "u8"), dev(sw, "f32")
+    y = torch.empty((n, d_out), dtype=torch.float32, device="cuda")
+    acc = torch.empty((n, d_out), dtype=torch.int32, device="cuda")
+    cat.cat_w4a4_linear(codes, s_x, dqw, dsw, y, acc)
+    cols = np.unique(np.concatenate([rng.choice(d_out, 62, replace=False), [0, d_out - 1]]))
+    dc = torch.from_numpy(cols).cuda()
+    acc_or, y_or = o.w4a4_linear(o.unpack_int4(c_rows), s_rows, qw[cols], sw[cols])
+    assert np.array_equal(host(acc[dr][:, dc]), acc_or)
+    assert np.array_equal(host(y[dr][:, dc]), y_or)
+    y_fast = torch.empty_like(y)
+    cat.cat_w4a4_linear(codes, s_x, dqw, dsw, y_fast)
+    assert torch.equal(y_fast, y)
+    del acc, y_fast
+
+    # SQNR over all n x d_out entries; the oracle sums fp64 chunks
+    g = torch.Generator(device="cuda")
+    g.manual_seed(k)
+    y_ref = y + 0.1 * torch.randn(y.shape, device="cuda", generator=g)
+    out = torch.empty(3, dtype=torch.float64, device="cuda")
+    sws = torch.empty(cat.cat_sqnr_workspace_bytes(y.numel()), dtype=torch.uint8, device="cuda")
+    cat.cat_sqnr(y_ref, y, sws, out)
+    S = E = 0.0
+    for a in range(0, n, 2048):
+        Sa, Ea, _ = o.sqnr(host(y_ref[a:a + 2048]), host(y[a:a + 2048]))
+        S, E = S + Sa, E + Ea
+    r = host(out)
+    assert r[0] == pytest.approx(S, rel=1e-9) and r[1] == pytest.approx(E, rel=1e-9)
+    assert abs(r[2] - 10.0 * np.log10(S / E)) < 1e-6
+    del y, y_ref
+
+    # full second moment over the n_cal calibration tokens; a sampled block
+    # and exact symmetry
+    dXc = dev(X_cal, "bf16")
+    sacc = torch.zeros((d_in, d_in), dtype=torch.float32, device="cuda")
+    cat.cat_cov_accumulate(dXc, sacc, B.CAT_COV_FULL, 1)
+    I = np.sort(rng.choice(d_in, 64, replace=False))
+    J = np.sort(rng.choice(d_in, 64, replace=False))
+    ref = o.second_moment_sum(np.hstack([X_cal[:, I], X_cal[:, J]]))[:64, 64:]
+    got = host(sacc[torch.from_numpy(I).cuda()][:, torch.from_numpy(J).cuda()])
+    assert rel_fro(got, ref) <= 1e-5
+    assert torch.equal(sacc, sacc.t())

@@ -5,10 +5,15 @@
 // run cov_sk_kernel: 256 x 256 upper-triangle tiles, token slabs streamed
 // HBM -> LDS in X's own layout and transposed by ds_read_tr16_b64 on the
 // way into v_mfma_f32_32x32x16_bf16, work split evenly over the CUs
-// (stream-K over (tile, slab) units), partial sums added with fp32
-// atomics.  The design notes are at that kernel.
+// (stream-K over (tile, slab) units), pieces of split tiles combined in a
+// fixed order.  Diagonal blocks of 32, 64 or 128 channels also run there
+// when the width is a multiple of 256: each 256-channel group is one
+// diagonal tile, of which only the diagonal blocks are stored (the MFMAs
+// of the rest are spent to keep the CUs streaming; the path is bound by
+// the X stream, not by the matrix cores).  The design notes are at that
+// kernel.
 //
-// Smaller bf16 matrices (64 or 128 channels, or widths that are not a
+// Other small bf16 matrices (64 to 255 channels, or widths that are not a
 // multiple of 32) run cov_mfma_kernel: one workgroup per 128 x 128 (or
 // 64 x 64) upper-triangle tile looping over all tokens; each 32-token slab
 // is transposed on its way into LDS (4-byte loads of channel pairs split
@@ -297,15 +302,38 @@ constexpr int kSkThreads = 512;                  // 8 waves: 2 x 4 over the tile
 constexpr int kSkMaxSlabs = 256;                 // slabs per launch (8192 tokens)
 constexpr int64_t kSkSlotFloats = int64_t(kSkT) * kSkT;   // one 256 x 256 fp32 tile
 
+// A launch covers nmat matrices of dim channels each, X columns
+// mat * dim .. mat * dim + dim - 1 for matrix mat: the whole d x d matrix
+// (FULL), one k x k block (BLOCK_DIAG, k >= 256), or, for blocks of
+// 32 .. 128 channels, one 256-channel group of 256 / k blocks ("packed":
+// the group's 256 x 256 square is computed and only its diagonal k x k
+// blocks are stored).
 struct SkGeom {
-    int64_t dim;     // channels of one matrix (d in FULL mode, k in BLOCK_DIAG mode)
+    int64_t dim;     // channels of one matrix
     int64_t T;       // tiles along one edge of a matrix
     int64_t tri;     // upper-triangle tiles per matrix
     int64_t tiles;   // tiles over all matrices
     int64_t S;       // 32-token slabs of this launch
     int64_t U;       // units = tiles * S
     int64_t G;       // workgroups
+    // output addressing (sk_out): matrix mat starts at acc + mat * mbase;
+    // element (r, c) lies in diagonal block r >> lsub (lsub = 62 when the
+    // matrix is stored whole), which starts bsz floats into the matrix per
+    // block and has row stride `stride`
+    int64_t mbase;
+    int64_t bsz;
+    int64_t stride;
+    int lsub;
 };
+
+// Element offset in acc of entry (r, c) of matrix mat, or -1 for an entry
+// off the block diagonal of a packed group (not stored).
+__device__ __forceinline__ int64_t sk_out(const SkGeom& g, int64_t mat, int64_t r, int64_t c) {
+    const int64_t br = r >> g.lsub;
+    if (br != (c >> g.lsub)) return -1;
+    const int64_t o = br << g.lsub;
+    return mat * g.mbase + br * g.bsz + (r - o) * g.stride + (c - o);
+}
 
 // First unit of workgroup w's share (w = G gives U).
 __device__ __forceinline__ int64_t sk_begin(const SkGeom& g, int64_t w) { return g.U * w / g.G; }
@@ -358,8 +386,7 @@ __device__ __forceinline__ bf16x8 sk_frag(const char __attribute__((address_spac
 }
 
 __global__ __launch_bounds__(kSkThreads, 1) void cov_sk_kernel(const uint16_t* __restrict__ X,
-                                                                int64_t n, int64_t d, int mode,
-                                                                int64_t k, SkGeom g,
+                                                                int64_t n, int64_t d, SkGeom g,
                                                                 float* __restrict__ acc,
                                                                 float* __restrict__ ws) {
     __shared__ __attribute__((aligned(16))) u32x4 ring[kSkStages][2][kSkOpUnits];
@@ -405,10 +432,9 @@ __global__ __launch_bounds__(kSkThreads, 1) void cov_sk_kernel(const uint16_t* _
         const int64_t mat = tile / g.tri;
         int64_t I, J;
         st_decode(tile % g.tri, g.T, I, J);
-        const int64_t colbase = mode == CAT_COV_FULL ? 0 : mat * k;
+        const int64_t colbase = mat * g.dim;
         const int64_t I0 = I * kSkT, J0 = J * kSkT;
         const bool diag = I == J;
-        float* accm = acc + (mode == CAT_COV_FULL ? 0 : mat * k * k);
         // this wave's operand: A (rows I0..) for group 0, B (J0..) for group 1
         const bool loads = grp == 0 || !diag;
         const int op = grp;
@@ -597,17 +623,17 @@ __global__ __launch_bounds__(kSkThreads, 1) void cov_sk_kernel(const uint16_t* _
                         for (int j = 0; j < 8; ++j) {
                             const int row = (tid >> 6) + 8 * (j0 + j);
                             const int64_t grow = I0 + 128 * half + row;
-                            old[j] = (rows_ok || grow < dimv)
-                                         ? *reinterpret_cast<const f32x4*>(accm + grow * dimv + col)
-                                         : f32x4{0.f, 0.f, 0.f, 0.f};
+                            const int64_t o = (rows_ok || grow < dimv) ? sk_out(g, mat, grow, col) : -1;
+                            old[j] = o >= 0 ? *reinterpret_cast<const f32x4*>(acc + o)
+                                            : f32x4{0.f, 0.f, 0.f, 0.f};
                         }
 #pragma unroll
                         for (int j = 0; j < 8; ++j) {
                             const int row = (tid >> 6) + 8 * (j0 + j);
                             const int64_t grow = I0 + 128 * half + row;
                             const f32x4 add = *reinterpret_cast<const f32x4*>(stage + row * kSkT + 4 * cg);
-                            if (rows_ok || grow < dimv)
-                                *reinterpret_cast<f32x4*>(accm + grow * dimv + col) = old[j] + add;
+                            const int64_t o = (rows_ok || grow < dimv) ? sk_out(g, mat, grow, col) : -1;
+                            if (o >= 0) *reinterpret_cast<f32x4*>(acc + o) = old[j] + add;
                         }
                     }
                 }
@@ -617,11 +643,16 @@ __global__ __launch_bounds__(kSkThreads, 1) void cov_sk_kernel(const uint16_t* _
 #pragma unroll
             for (int a = 0; a < 4; ++a)
 #pragma unroll
-                for (int b = 0; b < 2; ++b)
+                for (int b = 0; b < 2; ++b) {
+                    // a packed group keeps only its diagonal blocks (each
+                    // 32 x 32 accumulator lies inside one block)
+                    if ((int64_t(wm * 128 + 32 * a) >> g.lsub) != (int64_t(wn * 64 + 32 * b) >> g.lsub))
+                        continue;
 #pragma unroll
                     for (int r = 0; r < 16; ++r)
                         slot[(rowb + 32 * a + 8 * (r >> 2) + (r & 3)) * kSkT + colb + 32 * b] =
                             part[a][b][r];
+                }
         }
         lds_barrier();   // every wave is done with the ring before the next tile refills it
     }
@@ -640,8 +671,7 @@ __device__ __forceinline__ int64_t sk_owner(const SkGeom& g, int64_t u) {
 // off-diagonal tile's transpose is written below the diagonal.  One
 // workgroup per 64 x 64 sub-block of a tile: coalesced 16-byte row reads,
 // transposition through LDS, coalesced 16-byte row writes.
-__global__ __launch_bounds__(kCovThreads) void cov_combine_kernel(float* __restrict__ acc, int mode,
-                                                                  int64_t k, SkGeom g,
+__global__ __launch_bounds__(kCovThreads) void cov_combine_kernel(float* __restrict__ acc, SkGeom g,
                                                                   const float* __restrict__ ws) {
     __shared__ float tr[64][65];
     const int64_t tile = blockIdx.x / 16;
@@ -652,20 +682,23 @@ __global__ __launch_bounds__(kCovThreads) void cov_combine_kernel(float* __restr
     const int sr = (sub >> 2) * 64, sc = (sub & 3) * 64;   // sub-block origin inside the tile
     const int64_t r0 = I * kSkT + sr, c0 = J * kSkT + sc;
     if (r0 >= g.dim || c0 >= g.dim) return;
+    // a packed group's sub-blocks off its block diagonal are not stored
+    const int lb = g.lsub > 6 ? g.lsub : 6;
+    if ((r0 >> lb) != (c0 >> lb)) return;
     const int64_t w_lo = sk_owner(g, tile * g.S), w_hi = sk_owner(g, (tile + 1) * g.S - 1);
     const bool whole = w_lo == w_hi && sk_begin(g, w_lo) <= tile * g.S &&
                        sk_begin(g, w_lo + 1) >= (tile + 1) * g.S;
     if (whole && I == J) return;   // added in place by the main kernel, no mirror
-    float* m = acc + (mode == CAT_COV_FULL ? 0 : mat * k * k);
     const int tid = threadIdx.x;
     const int rl = tid >> 4, cl = 4 * (tid & 15);
     f32x4 v[4];
+    int64_t o[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int row = rl + 16 * i;
         const bool ok = r0 + row < g.dim && c0 + cl < g.dim;
-        v[i] = ok ? *reinterpret_cast<const f32x4*>(m + (r0 + row) * g.dim + c0 + cl)
-                  : f32x4{0.f, 0.f, 0.f, 0.f};
+        o[i] = ok ? sk_out(g, mat, r0 + row, c0 + cl) : -1;
+        v[i] = o[i] >= 0 ? *reinterpret_cast<const f32x4*>(acc + o[i]) : f32x4{0.f, 0.f, 0.f, 0.f};
     }
     if (!whole) {
         auto slot_of = [&](int64_t w) {
@@ -697,11 +730,8 @@ __global__ __launch_bounds__(kCovThreads) void cov_combine_kernel(float* __restr
                 v[i] += *reinterpret_cast<const f32x4*>(s0 + (sr + rl + 16 * i) * kSkT + sc + cl);
         }
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int row = rl + 16 * i;
-            if (r0 + row < g.dim && c0 + cl < g.dim)
-                *reinterpret_cast<f32x4*>(m + (r0 + row) * g.dim + c0 + cl) = v[i];
-        }
+        for (int i = 0; i < 4; ++i)
+            if (o[i] >= 0) *reinterpret_cast<f32x4*>(acc + o[i]) = v[i];
     }
     if (I == J) return;
 #pragma unroll
@@ -716,14 +746,33 @@ __global__ __launch_bounds__(kCovThreads) void cov_combine_kernel(float* __restr
         const int row = rl + 16 * i;   // row of the lower block = column of the upper one
         if (c0 + row >= g.dim || r0 + cl >= g.dim) continue;
         const f32x4 t = {tr[cl][row], tr[cl + 1][row], tr[cl + 2][row], tr[cl + 3][row]};
-        *reinterpret_cast<f32x4*>(m + (c0 + row) * g.dim + r0 + cl) = t;
+        *reinterpret_cast<f32x4*>(acc + sk_out(g, mat, c0 + row, r0 + cl)) = t;   // whole matrix
     }
 }
 
 // Geometry of one launch over n <= kSkMaxSlabs * 32 tokens.
+// Blocks of 32 .. 128 channels in whole 256-channel groups run packed.
+static bool cov_sk_packed(int64_t d, int mode, int64_t k) {
+    return mode == CAT_COV_BLOCK_DIAG && k >= 32 && k < kSkT && (d % kSkT) == 0;
+}
+
 static bool cov_sk_geometry(int64_t n, int64_t d, int mode, int64_t k, int64_t cus, SkGeom& g) {
-    g.dim = mode == CAT_COV_FULL ? d : k;
-    const int64_t nmat = mode == CAT_COV_FULL ? 1 : d / k;
+    const bool packed = cov_sk_packed(d, mode, k);
+    g.dim = packed ? kSkT : (mode == CAT_COV_FULL ? d : k);
+    const int64_t nmat = mode == CAT_COV_FULL ? 1 : d / g.dim;
+    if (packed) {
+        int l = 0;
+        while ((int64_t(1) << l) < k) ++l;   // k is a power of two
+        g.lsub = l;
+        g.bsz = k * k;
+        g.stride = k;
+        g.mbase = kSkT * k;
+    } else {
+        g.lsub = 62;
+        g.bsz = 0;
+        g.stride = g.dim;
+        g.mbase = g.dim * g.dim;
+    }
     g.T = (g.dim + kSkT - 1) / kSkT;
     g.tri = g.T * (g.T + 1) / 2;
     g.tiles = nmat * g.tri;
@@ -735,7 +784,8 @@ static bool cov_sk_geometry(int64_t n, int64_t d, int mode, int64_t k, int64_t c
 
 static bool cov_uses_sk(int x_bf16, int64_t d, int mode, int64_t k) {
     const int64_t dim = mode == CAT_COV_FULL ? d : k;
-    return x_bf16 && dim >= kSkT && (d % 8) == 0 && (dim % 32) == 0;
+    return x_bf16 && (d % 8) == 0 &&
+           ((dim >= kSkT && (dim % 32) == 0) || cov_sk_packed(d, mode, k));
 }
 
 static hipError_t device_cus(int& cus) {
@@ -784,12 +834,12 @@ hipError_t launch_cov_accumulate(const void* X, int x_bf16, int64_t n, int64_t d
             SkGeom g;
             if (!cov_sk_geometry(nc, d, mode, k, cus, g)) return hipSuccess;
             hipLaunchKernelGGL(cov_sk_kernel, dim3(static_cast<uint32_t>(g.G)), dim3(kSkThreads),
-                               0, stream, Xb + t0 * d, nc, d, mode, k, g, acc,
+                               0, stream, Xb + t0 * d, nc, d, g, acc,
                                static_cast<float*>(workspace));
             err = hipGetLastError();
             if (err != hipSuccess) return err;
             hipLaunchKernelGGL(cov_combine_kernel, dim3(static_cast<uint32_t>(g.tiles * 16)),
-                               dim3(kCovThreads), 0, stream, acc, mode, k, g,
+                               dim3(kCovThreads), 0, stream, acc, g,
                                static_cast<const float*>(workspace));
             err = hipGetLastError();
             if (err != hipSuccess) return err;

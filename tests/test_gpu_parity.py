@@ -386,8 +386,8 @@ def _blocks(S, k):
 
 
 def _assert_symmetric(acc):
-    # split tiles are added with atomics, so the two triangles may round
-    # their sums in different orders: equal to within a few ulp
+    # a diagonal tile is computed as a full square, whose two triangles may
+    # round their sums differently: equal to within a few ulp
     asym = np.max(np.abs(acc - acc.T))
     assert asym <= 4e-7 * max(1.0, float(np.max(np.abs(acc))))
 
@@ -437,6 +437,44 @@ def test_cov_block_diag_matches_oracle(k, dtype):
                         dtype)
     acc = _cov_gpu(X, dtype, B.CAT_COV_BLOCK_DIAG, k)
     ref = _blocks(o.second_moment_sum(X), k)
+    err = rel_fro(acc, ref)
+    say(f"  rel fro {err:.2e}")
+    assert err <= 1e-5
+
+
+@pytest.mark.parametrize("d,k,n", [(320, 64, 3001), (384, 128, 700), (768, 64, 33),
+                                   (256, 128, 1), (512, 32, 8193)])
+def test_cov_block_diag_shapes(d, k, n):
+    """Blocks of 32-128 channels: whole 256-channel groups (d % 256 == 0) run
+    packed through the 256-tile kernel, other widths through the 128/64-tile
+    kernel; ragged token counts, one token, and a batch over 8192 tokens
+    (two launches)."""
+    say(f"cov block d={d} k={k} n={n}")
+    cfg = wl.get_config("attn4096", d_in=d, d_out=d, n_cal=n, n=1)
+    X = o.round_storage(wl.make_layer(cfg, seed=d + k + n, with_eval=False,
+                                      with_weights=False)["X_cal"], "bf16")
+    acc = _cov_gpu(X, "bf16", B.CAT_COV_BLOCK_DIAG, k)
+    ref = _blocks(o.second_moment_sum(X), k)
+    err = rel_fro(acc, ref)
+    say(f"  rel fro {err:.2e}")
+    assert err <= 1e-5
+
+
+@pytest.mark.parametrize("name,k", [("mlp_up", 128), ("stress", 64)])
+def test_cov_block_diag_full_size_batch(name, k):
+    """Calibration blocks at layer width over one 8192-token batch, onto a
+    non-zero start (the packed 256-channel groups)."""
+    torch = torch_mod()
+    cfg = wl.get_config(name, n_cal=8192, n=1)
+    d = cfg.d_in
+    say(f"cov block full size {name} d={d} k={k}")
+    X = wl.make_layer(cfg, seed=7, with_eval=False, with_weights=False)["X_cal"]
+    start = wl.random_spd(k, seed=4).astype(np.float32)
+    S0 = np.broadcast_to(start, (d // k, k, k)).copy()
+    acc0 = torch.from_numpy(S0).cuda()
+    acc = _cov_gpu(X, "bf16", B.CAT_COV_BLOCK_DIAG, k, acc0=acc0)
+    ref = S0.astype(np.float64) + np.stack(
+        [o.second_moment_sum(X[:, b * k:(b + 1) * k]) for b in range(d // k)])
     err = rel_fro(acc, ref)
     say(f"  rel fro {err:.2e}")
     assert err <= 1e-5

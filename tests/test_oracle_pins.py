@@ -224,15 +224,17 @@ def test_quantizer_hand_examples():
         assert float(scale[0]) == s
 
 
-def test_quantizer_is_nearest_grid_point_brute_force():
-    # Every code is the nearest of the 15 grid levels to z * (7/amax)
-    # (brute-force argmin), ties aside.
+@pytest.mark.parametrize("bits", [4, 6, 8])
+def test_quantizer_is_nearest_grid_point_brute_force(bits):
+    # Every code is the nearest of the 2 qmax + 1 grid levels to
+    # z * (qmax/amax) (brute-force argmin), ties aside; qmax = 7, 31, 127.
+    qm = {4: 7, 6: 31, 8: 127}[bits]
     rng = np.random.default_rng(12)
     Z = (rng.standard_normal((64, 48)) * np.exp(rng.standard_normal(48))).astype(np.float32)
-    codes, scale = o.quantize_rows(Z, 4)
-    levels = np.arange(-7, 8)
+    codes, scale = o.quantize_rows(Z, bits)
+    levels = np.arange(-qm, qm + 1)
     amax = np.abs(Z.astype(np.float64)).max(1)
-    u = Z.astype(np.float64) * (7.0 / amax)[:, None]
+    u = Z.astype(np.float64) * (qm / amax)[:, None]
     dist = np.abs(u[..., None] - levels[None, None, :])
     best = levels[np.argmin(dist, axis=-1)]
     near_tie = np.abs(np.abs(u - np.floor(u)) - 0.5) < 1e-5
@@ -242,40 +244,42 @@ def test_quantizer_is_nearest_grid_point_brute_force():
     assert np.all(err <= 0.5 * scale[:, None] * (1 + 1e-5))
 
 
-def test_quantizer_extremes_and_range():
+@pytest.mark.parametrize("bits,qm", [(4, 7), (6, 31), (8, 127)])
+def test_quantizer_extremes_and_range(bits, qm):
     rng = np.random.default_rng(13)
     Z = rng.standard_normal((32, 40)).astype(np.float32)
-    codes, scale = o.quantize_rows(Z, 4)
-    assert codes.min() >= -7 and codes.max() <= 7
+    codes, scale = o.quantize_rows(Z, bits)
+    assert codes.min() >= -qm and codes.max() <= qm
     i = np.argmax(np.abs(Z), axis=1)
-    assert np.all(np.abs(codes[np.arange(32), i]) == 7)
-    z0, s0 = o.quantize_rows(np.zeros((2, 8), np.float32), 4)
+    assert np.all(np.abs(codes[np.arange(32), i]) == qm)
+    z0, s0 = o.quantize_rows(np.zeros((2, 8), np.float32), bits)
     assert not z0.any() and not s0.any()
 
 
-def test_quantizer_power_of_two_scale_invariance():
+@pytest.mark.parametrize("bits", [4, 6, 8])
+def test_quantizer_power_of_two_scale_invariance(bits):
     rng = np.random.default_rng(14)
     Z = rng.standard_normal((16, 32)).astype(np.float32)
-    c0, s0 = o.quantize_rows(Z, 4)
+    c0, s0 = o.quantize_rows(Z, bits)
     for m in (-7, -1, 3, 20):
-        c, s = o.quantize_rows(Z * np.float32(2.0 ** m), 4)
+        c, s = o.quantize_rows(Z * np.float32(2.0 ** m), bits)
         assert np.array_equal(c, c0)
         assert np.array_equal(s, (s0 * np.float32(2.0 ** m)).astype(np.float32))
 
 
-def test_transform_quant_identity_is_plain_rtn():
+@pytest.mark.parametrize("bits,qm", [(4, 7), (6, 31), (8, 127)])
+def test_transform_quant_identity_is_plain_rtn(bits, qm):
     # T = I: codes are the nearest grid points of x itself (brute force).
-    rng = np.random.default_rng(15)
     X = wl.random_bf16_matrix(40, 64, seed=15, scale=3.0).astype(np.float64)
     T = np.stack([np.eye(16)] * 4)
-    codes, scale = o.transform_quant(X, T, 4)
+    codes, scale = o.transform_quant(X, T, bits)
     amax = np.abs(X).max(1)
-    u = X * (7.0 / amax)[:, None]
-    levels = np.arange(-7, 8)
+    u = X * (qm / amax)[:, None]
+    levels = np.arange(-qm, qm + 1)
     best = levels[np.argmin(np.abs(u[..., None] - levels), axis=-1)]
-    near_tie = np.abs(np.abs(u - np.floor(u)) - 0.5) < 1e-6
+    near_tie = np.abs(np.abs(u - np.floor(u)) - 0.5) < 1e-5
     assert np.all((codes == best) | near_tie)
-    np.testing.assert_allclose(scale, amax / 7.0, rtol=1e-7)
+    np.testing.assert_allclose(scale, amax / qm, rtol=1e-7)
 
 
 def test_transform_quant_orthogonal_T_preserves_unquantized_output():
@@ -323,6 +327,26 @@ def test_w4a4_linear_brute_force_loops():
             assert acc[t, j] == ref
             # power-of-two scales: the dequantized value is exact
             assert float(y[t, j]) == ref * float(sx[t]) * float(sw[j])
+
+
+def test_linear_int8_codes_brute_force_loops():
+    # 8-bit codes over a 4096-long reduction: sums reach 127^2 * 4096 > 2^24,
+    # so acc is exact in int32 while its fp32 conversion rounds (to nearest
+    # even, the conversion the dequantization starts from).
+    qx = wl.random_codes(2, 4096, seed=23, qmax=127)
+    qw = wl.random_codes(3, 4096, seed=24, qmax=127)
+    qx[0] = 127
+    qw[0] = 127
+    sx = np.array([0.375, 1.5], np.float32)
+    sw = np.array([0.5, 2.0, 0.0625], np.float32)
+    acc, y = o.w4a4_linear(qx, sx, qw, sw)
+    for t in range(2):
+        for j in range(3):
+            ref = sum(int(a) * int(b) for a, b in zip(qx[t], qw[j]))
+            assert acc[t, j] == ref
+            want = np.float32(np.float32(np.float32(ref) * sx[t]) * sw[j])
+            assert y[t, j] == want
+    assert acc[0, 0] == 127 * 127 * 4096 and acc[0, 0] > 2 ** 24
 
 
 def test_w4a4_linear_equals_fake_quant_and_is_permutation_invariant():

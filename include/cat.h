@@ -29,6 +29,8 @@
  *    = row length).  Device pointers must be 16-byte aligned.
  *  - Packed INT4: byte j of a row holds element 2j in bits 0-3 and element
  *    2j+1 in bits 4-7, two's complement; codes lie in [-7, 7].
+ *  - 6- and 8-bit codes (the W6A6 / W8A8 comparison widths): one int8 per
+ *    element, codes in [-31, 31] or [-127, 127].
  *  - Calls are stateless and may be issued from several threads.
  *  - NaN / Inf inputs give undefined (but memory-safe) results.
  */
@@ -129,8 +131,9 @@ int cat_cov_accumulate(const void* X, int x_dtype, int64_t n, int64_t d,
  * X        device [n x d], x_dtype.
  * T        device [d/k x k x k], t_dtype; block b row-major (row j = output j).
  * k        power of two in [1, CAT_MAX_BLOCK]; d % k == 0; d even.
- * bits     4 (other widths return CAT_ERR_UNSUPPORTED).
- * codes    device uint8 [n x d/2], packed INT4 (written).
+ * bits     4, 6 or 8 (other widths return CAT_ERR_UNSUPPORTED).
+ * codes    device, written: bits 4: uint8 [n x d/2] packed INT4;
+ *          bits 6, 8: int8 [n x d], one code per byte.
  * s_x      device fp32 [n] (written).
  * workspace / workspace_bytes: device scratch of at least
  *          cat_transform_quant_workspace_bytes(n, d, k) bytes; its
@@ -166,6 +169,20 @@ int cat_transform_quant(const void* X, int x_dtype, int64_t n, int64_t d,
  */
 int cat_w4a4_linear(const uint8_t* codes_x, const float* s_x,
                     const uint8_t* codes_w, const float* s_w, int64_t n,
+                    int64_t d_in, int64_t d_out, float* y_tilde,
+                    int32_t* acc_out, void* stream);
+
+/* The same product for codes stored one int8 per element: the W6A6 and
+ * W8A8 layers the paper compares W4A4 against (Sec. 5; Sec. 3, eq. 5 at
+ * those widths).  Same formula, arguments and errors as cat_w4a4_linear,
+ * except:
+ * codes_x  device int8 [n x d_in], s_x device fp32 [n].
+ * codes_w  device int8 [d_out x d_in], s_w device fp32 [d_out].
+ * Codes must lie in [-127, 127] (what cat_transform_quant and
+ * cat_quantize_weights produce at 8 bits or fewer): with d_in <=
+ * CAT_MAX_D_IN every int32 sum is then exact.  -128 is not checked. */
+int cat_int8_linear(const int8_t* codes_x, const float* s_x,
+                    const int8_t* codes_w, const float* s_w, int64_t n,
                     int64_t d_in, int64_t d_out, float* y_tilde,
                     int32_t* acc_out, void* stream);
 
@@ -218,8 +235,10 @@ int cat_build_transform(const double* sigma_x_blocks, const float* W,
 /* Per-output-channel symmetric weight quantization (Sec. 6: weights per
  * channel, symmetric, round to nearest), on fp32(W_prime) with exactly
  * the arithmetic of cat_transform_quant.
- * W_prime host fp64 [d_out x d_in]; codes_w_out host uint8
- * [d_out x d_in/2]; s_w_out host fp32 [d_out]; bits == 4; d_in even. */
+ * W_prime host fp64 [d_out x d_in]; s_w_out host fp32 [d_out]; d_in even.
+ * bits 4: codes_w_out host uint8 [d_out x d_in/2], packed INT4;
+ * bits 6, 8: codes_w_out host int8 [d_out x d_in] (as uint8 storage).
+ * Other widths return CAT_ERR_UNSUPPORTED. */
 int cat_quantize_weights(const double* W_prime, int64_t d_out, int64_t d_in,
                          int bits, uint8_t* codes_w_out, float* s_w_out);
 

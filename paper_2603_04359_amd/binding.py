@@ -42,7 +42,7 @@ CAT_MAX_BLOCK = 512
 EXPORTED = (
     "cat_cov_workspace_bytes", "cat_cov_accumulate", "cat_transform_quant_workspace_bytes",
     "cat_transform_quant",
-    "cat_w4a4_linear", "cat_sqnr_workspace_bytes", "cat_sqnr", "cat_build_transform",
+    "cat_w4a4_linear", "cat_int8_linear", "cat_sqnr_workspace_bytes", "cat_sqnr", "cat_build_transform",
     "cat_quantize_weights", "cat_last_error", "cat_version",
 )
 
@@ -82,6 +82,8 @@ def lib() -> ctypes.CDLL:
     L.cat_transform_quant.restype = _int
     L.cat_w4a4_linear.argtypes = [_vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp]
     L.cat_w4a4_linear.restype = _int
+    L.cat_int8_linear.argtypes = [_vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp]
+    L.cat_int8_linear.restype = _int
     L.cat_sqnr_workspace_bytes.argtypes = [_i64]
     L.cat_sqnr_workspace_bytes.restype = _sz
     L.cat_sqnr.argtypes = [_vp, _vp, _i64, _vp, _sz, _vp, _vp]
@@ -182,16 +184,19 @@ def cat_transform_quant_workspace_bytes(n: int, d: int, k: int) -> int:
 
 
 def cat_transform_quant(X, T, k: int, codes, s_x, workspace, bits: int = 4, stream=None):
-    """codes [n, d/2] uint8 and s_x [n] fp32 from X [n, d] and T [d/k, k, k]."""
+    """codes and s_x [n] fp32 from X [n, d] and T [d/k, k, k].  codes:
+    bits 4: uint8 [n, d/2] packed INT4; bits 6, 8: int8 [n, d]."""
     torch = _torch()
     px = _dev_ptr(X, "X", (torch.bfloat16, torch.float32))
     pt = _dev_ptr(T, "T", (torch.bfloat16, torch.float32))
-    pc = _dev_ptr(codes, "codes", (torch.uint8,))
+    pc = _dev_ptr(codes, "codes", (torch.uint8,) if bits == 4 else (torch.int8,))
     ps = _dev_ptr(s_x, "s_x", (torch.float32,))
     pw = _dev_ptr(workspace, "workspace")
     if X.dim() != 2:
         raise ValueError("X must be [n, d]")
     n, d = X.shape
+    if tuple(codes.shape) != (n, d // 2 if bits == 4 else d):
+        raise ValueError(f"codes must be [{n}, {d // 2 if bits == 4 else d}] for bits={bits}")
     wbytes = workspace.numel() * workspace.element_size()
     _check("cat_transform_quant",
            lib().cat_transform_quant(px, _dtype_code(X), n, d, pt, _dtype_code(T), k, bits, pc, ps,
@@ -213,6 +218,25 @@ def cat_w4a4_linear(codes_x, s_x, codes_w, s_w, y_tilde, acc_out=None, stream=No
         raise ValueError("codes_x and codes_w disagree on d_in")
     _check("cat_w4a4_linear",
            lib().cat_w4a4_linear(pcx, psx, pcw, psw, n, 2 * half, d_out, py, pacc,
+                                 _stream_ptr(stream)))
+
+
+def cat_int8_linear(codes_x, s_x, codes_w, s_w, y_tilde, acc_out=None, stream=None):
+    """y_tilde [n, d_out] fp32 (and optionally acc_out int32) from int8
+    codes, one per element (the 6- and 8-bit widths)."""
+    torch = _torch()
+    pcx = _dev_ptr(codes_x, "codes_x", (torch.int8,))
+    psx = _dev_ptr(s_x, "s_x", (torch.float32,))
+    pcw = _dev_ptr(codes_w, "codes_w", (torch.int8,))
+    psw = _dev_ptr(s_w, "s_w", (torch.float32,))
+    py = _dev_ptr(y_tilde, "y_tilde", (torch.float32,))
+    pacc = _dev_ptr(acc_out, "acc_out", (torch.int32,), allow_none=True)
+    n, d_in = codes_x.shape
+    d_out = codes_w.shape[0]
+    if codes_w.shape[1] != d_in:
+        raise ValueError("codes_x and codes_w disagree on d_in")
+    _check("cat_int8_linear",
+           lib().cat_int8_linear(pcx, psx, pcw, psw, n, d_in, d_out, py, pacc,
                                  _stream_ptr(stream)))
 
 
@@ -263,10 +287,13 @@ def cat_build_transform(sigma_x_blocks, W, k: int, flags: int = CAT_BUILD_CAT,
 
 
 def cat_quantize_weights(W_prime, bits: int = 4):
-    """Host per-output-channel quantization: returns (codes uint8 [d_out, d_in/2], s_w fp32)."""
+    """Host per-output-channel quantization: returns (codes, s_w fp32);
+    codes uint8 [d_out, d_in/2] packed INT4 (bits 4) or int8 [d_out, d_in]
+    (bits 6, 8)."""
     Wp, pwp = _host(W_prime, np.float64, "W_prime")
     d_out, d_in = Wp.shape
-    codes = np.empty((d_out, d_in // 2), dtype=np.uint8)
+    codes = (np.empty((d_out, d_in // 2), dtype=np.uint8) if bits == 4
+             else np.empty((d_out, d_in), dtype=np.int8))
     s_w = np.empty(d_out, dtype=np.float32)
     _check("cat_quantize_weights",
            lib().cat_quantize_weights(pwp, d_out, d_in, bits, codes.ctypes.data, s_w.ctypes.data))

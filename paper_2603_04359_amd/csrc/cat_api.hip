@@ -100,7 +100,8 @@ extern "C" int cat_transform_quant(const void* X, int x_dtype, int64_t n, int64_
         if (!cat::is_pow2(k) || k > CAT_MAX_BLOCK)
             return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": k must be a power of two <= 512");
         if (d % k) return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": d % k != 0");
-        if (bits != 4) return fail(CAT_ERR_UNSUPPORTED, std::string(fn) + ": only bits == 4");
+        if (bits != 4 && bits != 6 && bits != 8)
+            return fail(CAT_ERR_UNSUPPORTED, std::string(fn) + ": bits must be 4, 6 or 8");
         if (!cat::aligned16(X) || !cat::aligned16(T) || !cat::aligned16(codes) ||
             !cat::aligned16(s_x))
             return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": pointers must be 16-byte aligned");
@@ -110,7 +111,7 @@ extern "C" int cat_transform_quant(const void* X, int x_dtype, int64_t n, int64_
             return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": workspace must be 16-byte aligned");
         if (int rc = require_device(fn)) return rc;
         const hipError_t err = catk::launch_transform_quant(
-            X, x_dtype == CAT_BF16, n, d, T, t_dtype == CAT_BF16, k, codes, s_x,
+            X, x_dtype == CAT_BF16, n, d, T, t_dtype == CAT_BF16, k, bits, codes, s_x,
             static_cast<uint32_t*>(workspace), static_cast<hipStream_t>(stream));
         if (err != hipSuccess) return hip_fail(fn, err);
         return CAT_OK;
@@ -121,10 +122,12 @@ extern "C" int cat_transform_quant(const void* X, int x_dtype, int64_t n, int64_
     }
 }
 
-extern "C" int cat_w4a4_linear(const uint8_t* codes_x, const float* s_x, const uint8_t* codes_w,
-                               const float* s_w, int64_t n, int64_t d_in, int64_t d_out,
-                               float* y_tilde, int32_t* acc_out, void* stream) {
-    const char* fn = "cat_w4a4_linear";
+namespace {
+
+// Shared checks and launch of the two integer GEMM entry points.
+int linear_call(const char* fn, bool i8, const void* codes_x, const float* s_x,
+                const void* codes_w, const float* s_w, int64_t n, int64_t d_in, int64_t d_out,
+                float* y_tilde, int32_t* acc_out, void* stream) {
     try {
         if (!codes_x || !s_x || !codes_w || !s_w || !y_tilde)
             return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": NULL pointer");
@@ -137,9 +140,14 @@ extern "C" int cat_w4a4_linear(const uint8_t* codes_x, const float* s_x, const u
             !cat::aligned16(s_w) || !cat::aligned16(y_tilde) || (acc_out && !cat::aligned16(acc_out)))
             return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": pointers must be 16-byte aligned");
         if (int rc = require_device(fn)) return rc;
-        const hipError_t err = catk::launch_w4a4_linear(codes_x, s_x, codes_w, s_w, n, d_in, d_out,
-                                                        y_tilde, acc_out,
-                                                        static_cast<hipStream_t>(stream));
+        const hipStream_t st = static_cast<hipStream_t>(stream);
+        const hipError_t err =
+            i8 ? catk::launch_int8_linear(static_cast<const int8_t*>(codes_x), s_x,
+                                          static_cast<const int8_t*>(codes_w), s_w, n, d_in, d_out,
+                                          y_tilde, acc_out, st)
+               : catk::launch_w4a4_linear(static_cast<const uint8_t*>(codes_x), s_x,
+                                          static_cast<const uint8_t*>(codes_w), s_w, n, d_in, d_out,
+                                          y_tilde, acc_out, st);
         if (err != hipSuccess) return hip_fail(fn, err);
         return CAT_OK;
     } catch (const std::exception& e) {
@@ -147,6 +155,22 @@ extern "C" int cat_w4a4_linear(const uint8_t* codes_x, const float* s_x, const u
     } catch (...) {
         return fail(CAT_ERR_INTERNAL, std::string(fn) + ": unknown error");
     }
+}
+
+}  // namespace
+
+extern "C" int cat_w4a4_linear(const uint8_t* codes_x, const float* s_x, const uint8_t* codes_w,
+                               const float* s_w, int64_t n, int64_t d_in, int64_t d_out,
+                               float* y_tilde, int32_t* acc_out, void* stream) {
+    return linear_call("cat_w4a4_linear", false, codes_x, s_x, codes_w, s_w, n, d_in, d_out,
+                       y_tilde, acc_out, stream);
+}
+
+extern "C" int cat_int8_linear(const int8_t* codes_x, const float* s_x, const int8_t* codes_w,
+                               const float* s_w, int64_t n, int64_t d_in, int64_t d_out,
+                               float* y_tilde, int32_t* acc_out, void* stream) {
+    return linear_call("cat_int8_linear", true, codes_x, s_x, codes_w, s_w, n, d_in, d_out,
+                       y_tilde, acc_out, stream);
 }
 
 extern "C" size_t cat_sqnr_workspace_bytes(int64_t count) {

@@ -355,32 +355,38 @@ extern "C" int cat_quantize_weights(const double* W_prime, int64_t d_out, int64_
         return fail(CAT_ERR_INVALID_ARG, "cat_quantize_weights: NULL pointer");
     if (d_out < 1 || d_in < 2 || (d_in & 1))
         return fail(CAT_ERR_INVALID_ARG, "cat_quantize_weights: d_out >= 1, d_in even >= 2");
-    if (bits != 4) return fail(CAT_ERR_UNSUPPORTED, "cat_quantize_weights: only bits == 4");
-    const float qmax = 7.0f;
+    if (bits != 4 && bits != 6 && bits != 8)
+        return fail(CAT_ERR_UNSUPPORTED, "cat_quantize_weights: bits must be 4, 6 or 8");
+    const float qmax = static_cast<float>((1 << (bits - 1)) - 1);
+    // bits 4: two codes per byte; 6 and 8: one int8 per code
+    const int64_t row_out = bits == 4 ? d_in / 2 : d_in;
     std::vector<float> row(static_cast<size_t>(d_in));
+    std::vector<int> q(static_cast<size_t>(d_in));
     for (int64_t o = 0; o < d_out; ++o) {
         float amax = 0.0f;
         for (int64_t j = 0; j < d_in; ++j) {
             row[j] = static_cast<float>(W_prime[o * d_in + j]);
             amax = std::max(amax, std::fabs(row[j]));
         }
-        uint8_t* out = codes_w_out + o * (d_in / 2);
+        uint8_t* out = codes_w_out + o * row_out;
         if (amax == 0.0f) {
             s_w_out[o] = 0.0f;
-            std::memset(out, 0, static_cast<size_t>(d_in / 2));
+            std::memset(out, 0, static_cast<size_t>(row_out));
             continue;
         }
         s_w_out[o] = amax / qmax;
         const float inv = qmax / amax;
-        for (int64_t j = 0; j < d_in; j += 2) {
-            int q[2];
-            for (int h = 0; h < 2; ++h) {
-                const float u = row[j + h] * inv;
-                float r = std::nearbyint(u);
-                r = std::min(qmax, std::max(-qmax, r));
-                q[h] = static_cast<int>(r);
-            }
-            out[j / 2] = static_cast<uint8_t>((q[0] & 0xF) | ((q[1] & 0xF) << 4));
+        for (int64_t j = 0; j < d_in; ++j) {
+            const float u = row[j] * inv;
+            float r = std::nearbyint(u);
+            r = std::min(qmax, std::max(-qmax, r));
+            q[j] = static_cast<int>(r);
+        }
+        if (bits == 4) {
+            for (int64_t j = 0; j < d_in; j += 2)
+                out[j / 2] = static_cast<uint8_t>((q[j] & 0xF) | ((q[j + 1] & 0xF) << 4));
+        } else {
+            for (int64_t j = 0; j < d_in; ++j) out[j] = static_cast<uint8_t>(q[j] & 0xFF);
         }
     }
     return CAT_OK;

@@ -1,10 +1,14 @@
-// Block transform fused with symmetric per-token INT4 quantization.
+// Block transform fused with symmetric per-token integer quantization.
 //
 // For each token x (a row of X) and each diagonal block b of the
 // block-diagonal transform (Sec. 4, eq. 10):  z_b = T_b x_b.
 // The token's scale uses the range of the WHOLE transformed row
 // (dynamic per-token range, Lemma 2.2 / Sec. 6):
-//   amax = max |z|,  s = amax / 7,  code = clamp(rint(z * (7 / amax)), -7, 7).
+//   amax = max |z|,  s = amax / qmax,
+//   code = clamp(rint(z * (qmax / amax)), -qmax, qmax),
+// with qmax = 2^(bits-1) - 1: 7 for INT4 (codes packed two per byte), 31
+// and 127 for the 6- and 8-bit comparison widths (one int8 per code).
+// Every kernel below takes qmax as the template parameter QM.
 //
 // The row maximum couples all d/k blocks of a token, while reuse of T_b
 // wants many tokens per workgroup.  The kernels therefore split the work
@@ -39,12 +43,14 @@ __global__ void fill_zero_u32_kernel(uint32_t* p, int64_t n) {
     if (i < n) p[i] = 0u;
 }
 
-// Quantize one value given inv = 7/amax (amax > 0); returns the code in
-// [-7, 7] as an int.
+// Quantize one value given inv = qmax/amax (amax > 0); returns the code
+// in [-qmax, qmax] as an int.
+template <int QM>
 __device__ __forceinline__ int quant_code(float z, float inv) {
+    constexpr float q = static_cast<float>(QM);
     float u = z * inv;
     u = __builtin_rintf(u);
-    u = fminf(fmaxf(u, -kQmax4), kQmax4);
+    u = fminf(fmaxf(u, -q), q);
     return static_cast<int>(u);
 }
 
@@ -76,25 +82,31 @@ __global__ __launch_bounds__(kTqThreads) void tq_generic_amax_kernel(
     if (m) atomicMax(amax_ws + t, m);
 }
 
-template <typename XT, typename TT>
+template <typename XT, typename TT, int QM>
 __global__ __launch_bounds__(kTqThreads) void tq_generic_quant_kernel(
     const XT* __restrict__ X, const TT* __restrict__ T, int64_t n, int64_t d, int64_t k,
     const uint32_t* __restrict__ amax_ws, uint8_t* __restrict__ codes, float* __restrict__ s_x) {
+    constexpr float qmax = static_cast<float>(QM);
     const int64_t pairs = d / 2;
     const int64_t u = static_cast<int64_t>(blockIdx.x) * kTqThreads + threadIdx.x;
     if (u >= n * pairs) return;
     const int64_t t = u / pairs;
     const int64_t cp = u - t * pairs;
     const float amax = __uint_as_float(amax_ws[t]);
-    if (cp == 0) s_x[t] = __fdiv_rn(amax, kQmax4);
-    uint8_t byte = 0;
+    if (cp == 0) s_x[t] = __fdiv_rn(amax, qmax);
+    int q0 = 0, q1 = 0;
     if (amax > 0.0f) {
-        const float inv = __fdiv_rn(kQmax4, amax);
-        const float z0 = tq_dot(X, T, t, d, k, 2 * cp);
-        const float z1 = tq_dot(X, T, t, d, k, 2 * cp + 1);
-        byte = static_cast<uint8_t>((quant_code(z0, inv) & 0xF) | ((quant_code(z1, inv) & 0xF) << 4));
+        const float inv = __fdiv_rn(qmax, amax);
+        q0 = quant_code<QM>(tq_dot(X, T, t, d, k, 2 * cp), inv);
+        q1 = quant_code<QM>(tq_dot(X, T, t, d, k, 2 * cp + 1), inv);
     }
-    codes[t * pairs + cp] = byte;
+    if constexpr (QM == 7) {
+        codes[t * pairs + cp] = static_cast<uint8_t>((q0 & 0xF) | ((q1 & 0xF) << 4));
+    } else {
+        // one int8 per code: the pair is two consecutive bytes
+        *reinterpret_cast<uint16_t*>(codes + t * d + 2 * cp) =
+            static_cast<uint16_t>((q0 & 0xFF) | ((q1 & 0xFF) << 8));
+    }
 }
 
 // --------------------------------------------------------------- MFMA path
@@ -115,7 +127,7 @@ __device__ __forceinline__ int tq_swz(int r) {
     return (r / R) & M;
 }
 
-template <int K, int JC, bool QUANT>
+template <int K, int JC, bool QUANT, int QM>
 __global__ __launch_bounds__(kTqThreads) void tq_mfma_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ T, int64_t n, int64_t d,
     int64_t R, uint32_t* __restrict__ amax_ws, uint8_t* __restrict__ codes,
@@ -187,6 +199,29 @@ __global__ __launch_bounds__(kTqThreads) void tq_mfma_kernel(
                 for (int q = 0; q < 16; ++q) m_bits = max(m_bits, abs_bits(acc[m][q]));
             m_bits = max(m_bits, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m_bits), 32)));
             if (valid && h == 0 && m_bits) atomicMax(amax_ws + t, m_bits);
+        } else if constexpr (QM != 7) {
+            // one int8 per code: rows 32m + 8q + 4h + (0..3) of the lane's
+            // token are 4 consecutive bytes
+            constexpr float qmax = static_cast<float>(QM);
+            const float amax = valid ? __uint_as_float(amax_ws[t]) : 0.0f;
+            if (valid && h == 0 && b == 0 && jc == 0) s_x[t] = __fdiv_rn(amax, qmax);
+            const bool nz = amax > 0.0f;
+            const float inv = nz ? __fdiv_rn(qmax, amax) : 0.0f;
+            uint32_t* crow = reinterpret_cast<uint32_t*>(codes + t * d + b * K +
+                                                         static_cast<int64_t>(jc) * JC);
+#pragma unroll
+            for (int m = 0; m < NM; ++m)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    uint32_t p = 0;
+                    if (nz) {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            p |= static_cast<uint32_t>(quant_code<QM>(acc[m][4 * q + e], inv) & 0xFF)
+                                 << (8 * e);
+                    }
+                    if (valid) crow[(m * 32 + 8 * q + 4 * h) / 4] = p;
+                }
         } else {
             const float amax = valid ? __uint_as_float(amax_ws[t]) : 0.0f;
             if (valid && h == 0 && b == 0 && jc == 0) s_x[t] = __fdiv_rn(amax, kQmax4);
@@ -204,7 +239,7 @@ __global__ __launch_bounds__(kTqThreads) void tq_mfma_kernel(
                     if (nz) {
 #pragma unroll
                         for (int e = 0; e < 4; ++e)
-                            p |= static_cast<uint32_t>(quant_code(acc[m][4 * q + e], inv) & 0xF)
+                            p |= static_cast<uint32_t>(quant_code<7>(acc[m][4 * q + e], inv) & 0xF)
                                  << (4 * e);
                     }
                     v[q] = p;
@@ -229,7 +264,7 @@ __global__ __launch_bounds__(kTqThreads) void tq_mfma_kernel(
     }
 }
 
-template <int K, int JC>
+template <int K, int JC, int QM>
 hipError_t launch_tq_mfma(const uint16_t* X, int64_t n, int64_t d, const uint16_t* T,
                           uint8_t* codes, float* s_x, uint32_t* ws, hipStream_t stream) {
     const int64_t tiles = (n + 127) / 128;
@@ -239,11 +274,11 @@ hipError_t launch_tq_mfma(const uint16_t* X, int64_t n, int64_t d, const uint16_
     if (R > tiles) R = tiles;
     if (R < 1) R = 1;
     const int64_t grid = nbj * R;
-    hipLaunchKernelGGL((tq_mfma_kernel<K, JC, false>), dim3(static_cast<uint32_t>(grid)),
+    hipLaunchKernelGGL((tq_mfma_kernel<K, JC, false, 7>), dim3(static_cast<uint32_t>(grid)),
                        dim3(kTqThreads), 0, stream, X, T, n, d, R, ws, codes, s_x);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
-    hipLaunchKernelGGL((tq_mfma_kernel<K, JC, true>), dim3(static_cast<uint32_t>(grid)),
+    hipLaunchKernelGGL((tq_mfma_kernel<K, JC, true, QM>), dim3(static_cast<uint32_t>(grid)),
                        dim3(kTqThreads), 0, stream, X, T, n, d, R, ws, codes, s_x);
     return hipGetLastError();
 }
@@ -278,7 +313,7 @@ __device__ __forceinline__ int tq_xswz(int r) {
     return K == 128 ? ((r ^ (r >> 4)) & 15) : (r & 31);
 }
 
-template <int K, bool QUANT>
+template <int K, bool QUANT, int QM>
 __global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ T, int64_t n, int64_t d,
     int64_t R, uint32_t* __restrict__ amax_ws, uint8_t* __restrict__ codes,
@@ -362,6 +397,32 @@ __global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
                 const int64_t t = tile * C::TT + idx;
                 if (t < n && m) atomicMax(amax_ws + t, m);
             }
+        } else if constexpr (QM != 7) {
+            // one int8 per code: rows row0 + 8q + 4h + (0..3) of the lane's
+            // token are 4 consecutive bytes
+            constexpr float qmax = static_cast<float>(QM);
+#pragma unroll
+            for (int sb = 0; sb < C::NSB; ++sb) {
+                const int64_t t = tile * C::TT + sb * 32 + l32;
+                const bool valid = t < n;
+                const float amax = valid ? __uint_as_float(amax_ws[t]) : 0.0f;
+                if (valid && h == 0 && wave == 0 && b == 0 && jc == 0)
+                    s_x[t] = __fdiv_rn(amax, qmax);
+                const bool nz = amax > 0.0f;
+                const float inv = nz ? __fdiv_rn(qmax, amax) : 0.0f;
+                uint32_t* crow = reinterpret_cast<uint32_t*>(codes + t * d + b * K + row0);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    uint32_t pk = 0;
+                    if (nz) {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            pk |= static_cast<uint32_t>(quant_code<QM>(acc[sb][4 * q + e], inv) & 0xFF)
+                                  << (8 * e);
+                    }
+                    if (valid) crow[2 * q + h] = pk;
+                }
+            }
         } else {
 #pragma unroll
             for (int sb = 0; sb < C::NSB; ++sb) {
@@ -380,7 +441,7 @@ __global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
                     if (nz) {
 #pragma unroll
                         for (int e = 0; e < 4; ++e)
-                            pk |= static_cast<uint32_t>(quant_code(acc[sb][4 * q + e], inv) & 0xF)
+                            pk |= static_cast<uint32_t>(quant_code<7>(acc[sb][4 * q + e], inv) & 0xF)
                                   << (4 * e);
                     }
                     v[q] = pk;
@@ -494,18 +555,25 @@ __device__ __forceinline__ uint32_t fq_bytes(uint32_t b0, uint32_t b1, uint32_t 
     return __builtin_amdgcn_perm(b1, b0, 0x0C0C0400u) | __builtin_amdgcn_perm(b3, b2, 0x04000C0Cu);
 }
 
-// 16 accumulators (consecutive output channels) -> 16 INT4 codes, channel
-// 2m in the low nibble of byte m.  u = fl(z * inv) is clamped to [-7, 7]
-// and rounded to nearest even by adding 1.5 * 2^23 (exact for |u| < 2^22),
-// which leaves the integer in the low mantissa bits, two's complement.
-__device__ __forceinline__ u32x2 fq_quant16(const f32x16& z, float inv) {
-    uint32_t w[16];
+// 16 accumulators (consecutive output channels) -> 16 codes.  u =
+// fl(z * inv) is clamped to [-qmax, qmax] and rounded to nearest even by
+// adding 1.5 * 2^23 (exact for |u| < 2^22), which leaves the integer in the
+// low mantissa bits, two's complement.
+template <int QM>
+__device__ __forceinline__ void fq_round16(const f32x16& z, float inv, uint32_t (&w)[16]) {
+    constexpr float q = static_cast<float>(QM);
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
         float u = z[r] * inv;
-        u = __builtin_amdgcn_fmed3f(u, -kQmax4, kQmax4);
+        u = __builtin_amdgcn_fmed3f(u, -q, q);
         w[r] = __float_as_uint(u + 12582912.0f);
     }
+}
+
+// INT4: channel 2m in the low nibble of byte m.
+__device__ __forceinline__ u32x2 fq_quant16(const f32x16& z, float inv) {
+    uint32_t w[16];
+    fq_round16<7>(z, inv, w);
     u32x2 out;
 #pragma unroll
     for (int hw = 0; hw < 2; ++hw) {
@@ -515,6 +583,15 @@ __device__ __forceinline__ u32x2 fq_quant16(const f32x16& z, float inv) {
         out[hw] = (ev & 0x0F0F0F0Fu) | ((od << 4) & 0xF0F0F0F0u);
     }
     return out;
+}
+
+// 6- and 8-bit widths: one int8 per channel, channel m in byte m.
+template <int QM>
+__device__ __forceinline__ u32x4 fq_quant16_i8(const f32x16& z, float inv) {
+    uint32_t w[16];
+    fq_round16<QM>(z, inv, w);
+    return u32x4{fq_bytes(w[0], w[1], w[2], w[3]), fq_bytes(w[4], w[5], w[6], w[7]),
+                 fq_bytes(w[8], w[9], w[10], w[11]), fq_bytes(w[12], w[13], w[14], w[15])};
 }
 
 // max |z| over 16 values, as float bits.  Read as signed ints, the largest
@@ -550,6 +627,7 @@ __device__ __forceinline__ void fq_wait_copies(int later) {
     }
 }
 
+template <int QM>
 __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ T, int64_t n, int64_t d,
     int64_t R, TqFusedWs ws, uint32_t host_tag, uint8_t* __restrict__ codes,
@@ -640,7 +718,7 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
                 const int64_t t = tile0(it - kFqLag) + lane;
                 const uint32_t m = await(fv, f_addr(it - kFqLag));
                 gat[lane] = m;
-                if (b == 0 && t < n) s_x[t] = __fdiv_rn(__uint_as_float(m), kQmax4);
+                if (b == 0 && t < n) s_x[t] = __fdiv_rn(__uint_as_float(m), static_cast<float>(QM));
             }
             if (it >= 1 && it <= nt) pv = load(p_addr(it - 1));
             lds_barrier();                                            // F
@@ -724,13 +802,20 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
     auto quant = [&](int64_t it, const f32x16 (&acc)[2]) {
         const int64_t t = tile0(it) + tok;
         const float amax = __uint_as_float(gat[tok]);
-        const float inv = amax > 0.0f ? __fdiv_rn(kQmax4, amax) : 0.0f;
+        const float inv = amax > 0.0f ? __fdiv_rn(static_cast<float>(QM), amax) : 0.0f;
 #pragma unroll
         for (int g = 0; g < 2; ++g) {
-            const u32x2 c = fq_quant16(acc[g], inv);
-            if (t < n)
-                *reinterpret_cast<u32x2*>(codes + t * (d / 2) + b * (K / 2) + (2 * rh + g) * 16 +
-                                          8 * h) = c;
+            // lane (token, h) holds channels (2 rh + g) 32 + 16 h .. + 15
+            if constexpr (QM == 7) {
+                const u32x2 c = fq_quant16(acc[g], inv);
+                if (t < n)
+                    *reinterpret_cast<u32x2*>(codes + t * (d / 2) + b * (K / 2) +
+                                              (2 * rh + g) * 16 + 8 * h) = c;
+            } else {
+                const u32x4 c = fq_quant16_i8<QM>(acc[g], inv);
+                if (t < n)
+                    *reinterpret_cast<u32x4*>(codes + t * d + b * K + (2 * rh + g) * 32 + 16 * h) = c;
+            }
         }
     };
     // step it: A, multiply tile it into cur, F, quantize tile it-3 from old
@@ -753,7 +838,7 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
     }
 }
 
-template <int K>
+template <int K, int QM>
 hipError_t launch_tq_ring(const uint16_t* X, int64_t n, int64_t d, const uint16_t* T,
                           uint8_t* codes, float* s_x, uint32_t* ws, hipStream_t stream) {
     using C = TqRing<K>;
@@ -769,11 +854,11 @@ hipError_t launch_tq_ring(const uint16_t* X, int64_t n, int64_t d, const uint16_
     if (R > ntiles) R = ntiles;
     if (R < 1) R = 1;
     const int64_t grid = nbj * R;
-    hipLaunchKernelGGL((tq_ring_kernel<K, false>), dim3(static_cast<uint32_t>(grid)),
+    hipLaunchKernelGGL((tq_ring_kernel<K, false, 7>), dim3(static_cast<uint32_t>(grid)),
                        dim3(kTqThreads), 0, stream, X, T, n, d, R, ws, codes, s_x);
     err = hipGetLastError();
     if (err != hipSuccess) return err;
-    hipLaunchKernelGGL((tq_ring_kernel<K, true>), dim3(static_cast<uint32_t>(grid)),
+    hipLaunchKernelGGL((tq_ring_kernel<K, true, QM>), dim3(static_cast<uint32_t>(grid)),
                        dim3(kTqThreads), 0, stream, X, T, n, d, R, ws, codes, s_x);
     return hipGetLastError();
 }
@@ -800,6 +885,7 @@ static uint32_t next_tq_tag() {
 
 // Resident workgroups of tq_fused_kernel on a device (CUs x blocks per CU
 // by its register and LDS use), queried once per device.
+template <int QM>
 static hipError_t tq_fused_resident(int dev, int64_t& resident) {
     constexpr int kMaxDev = 64;
     static std::atomic<int64_t> cache[kMaxDev];   // 0 = not yet known
@@ -810,7 +896,7 @@ static hipError_t tq_fused_resident(int dev, int64_t& resident) {
     int cus = 0, per_cu = 0;
     hipError_t err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (err != hipSuccess) return err;
-    err = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, tq_fused_kernel, kFqThreads, 0);
+    err = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, tq_fused_kernel<QM>, kFqThreads, 0);
     if (err != hipSuccess) return err;
     resident = static_cast<int64_t>(per_cu) * cus;
     if (dev >= 0 && dev < kMaxDev && resident > 0) cache[dev].store(resident, std::memory_order_relaxed);
@@ -824,6 +910,7 @@ static hipError_t tq_fused_resident(int dev, int64_t& resident) {
 // The grid never exceeds the resident capacity, so every workgroup is on
 // the device together once other work has drained, and a peer a workgroup
 // waits for is always running or about to run.
+template <int QM>
 hipError_t launch_tq_fused(const uint16_t* X, int64_t n, int64_t d, const uint16_t* T,
                            uint8_t* codes, float* s_x, uint8_t* ws, hipStream_t stream,
                            bool& launched) {
@@ -832,7 +919,7 @@ hipError_t launch_tq_fused(const uint16_t* X, int64_t n, int64_t d, const uint16
     hipError_t err = hipGetDevice(&dev);
     if (err != hipSuccess) return err;
     int64_t resident = 0;
-    err = tq_fused_resident(dev, resident);
+    err = tq_fused_resident<QM>(dev, resident);
     if (err != hipSuccess) return err;
     const int64_t nbj = d / 128;
     const int64_t ntiles = (n + kFqTT - 1) / kFqTT;
@@ -859,7 +946,7 @@ hipError_t launch_tq_fused(const uint16_t* X, int64_t n, int64_t d, const uint16
     } else {
         tag = next_tq_tag();
     }
-    hipLaunchKernelGGL(tq_fused_kernel, dim3(static_cast<uint32_t>(nbj * R)), dim3(kFqThreads),
+    hipLaunchKernelGGL(tq_fused_kernel<QM>, dim3(static_cast<uint32_t>(nbj * R)), dim3(kFqThreads),
                        0, stream, X, T, n, d, R, w, tag, codes, s_x);
     err = hipGetLastError();
     if (err != hipSuccess) return err;
@@ -867,7 +954,7 @@ hipError_t launch_tq_fused(const uint16_t* X, int64_t n, int64_t d, const uint16
     return hipSuccess;
 }
 
-template <typename XT, typename TT>
+template <int QM, typename XT, typename TT>
 hipError_t launch_tq_generic(const XT* X, int64_t n, int64_t d, const TT* T, int64_t k,
                              uint8_t* codes, float* s_x, uint32_t* ws, hipStream_t stream) {
     const int64_t units = n * (d / 2);
@@ -876,19 +963,21 @@ hipError_t launch_tq_generic(const XT* X, int64_t n, int64_t d, const TT* T, int
                        dim3(kTqThreads), 0, stream, X, T, n, d, k, ws);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
-    hipLaunchKernelGGL((tq_generic_quant_kernel<XT, TT>), dim3(static_cast<uint32_t>(grid)),
+    hipLaunchKernelGGL((tq_generic_quant_kernel<XT, TT, QM>), dim3(static_cast<uint32_t>(grid)),
                        dim3(kTqThreads), 0, stream, X, T, n, d, k, ws, codes, s_x);
     return hipGetLastError();
 }
 
-hipError_t launch_transform_quant(const void* X, int x_bf16, int64_t n, int64_t d, const void* T,
-                                  int t_bf16, int64_t k, uint8_t* codes, float* s_x,
-                                  uint32_t* amax_ws, hipStream_t stream) {
+template <int QM>
+static hipError_t launch_tq_qm(const void* X, int x_bf16, int64_t n, int64_t d, const void* T,
+                               int t_bf16, int64_t k, uint8_t* codes, float* s_x,
+                               uint32_t* amax_ws, hipStream_t stream) {
     if (x_bf16 && t_bf16 && k == 128) {
         bool launched = false;
-        const hipError_t e = launch_tq_fused(static_cast<const uint16_t*>(X), n, d,
-                                             static_cast<const uint16_t*>(T), codes, s_x,
-                                             reinterpret_cast<uint8_t*>(amax_ws), stream, launched);
+        const hipError_t e = launch_tq_fused<QM>(static_cast<const uint16_t*>(X), n, d,
+                                                 static_cast<const uint16_t*>(T), codes, s_x,
+                                                 reinterpret_cast<uint8_t*>(amax_ws), stream,
+                                                 launched);
         if (e != hipSuccess || launched) return e;
     }
     hipLaunchKernelGGL(fill_zero_u32_kernel, dim3(static_cast<uint32_t>((n + 255) / 256)),
@@ -899,25 +988,38 @@ hipError_t launch_transform_quant(const void* X, int x_bf16, int64_t n, int64_t 
         const uint16_t* Xb = static_cast<const uint16_t*>(X);
         const uint16_t* Tb = static_cast<const uint16_t*>(T);
         switch (k) {
-            case 32: return launch_tq_mfma<32, 32>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
-            case 64: return launch_tq_mfma<64, 64>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
-            case 128: return launch_tq_ring<128>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
-            case 256: return launch_tq_ring<256>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
-            case 512: return launch_tq_ring<512>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
+            case 32: return launch_tq_mfma<32, 32, QM>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
+            case 64: return launch_tq_mfma<64, 64, QM>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
+            case 128: return launch_tq_ring<128, QM>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
+            case 256: return launch_tq_ring<256, QM>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
+            case 512: return launch_tq_ring<512, QM>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
             default: break;
         }
     }
     if (x_bf16 && t_bf16)
-        return launch_tq_generic(static_cast<const uint16_t*>(X), n, d,
-                                 static_cast<const uint16_t*>(T), k, codes, s_x, amax_ws, stream);
+        return launch_tq_generic<QM>(static_cast<const uint16_t*>(X), n, d,
+                                     static_cast<const uint16_t*>(T), k, codes, s_x, amax_ws,
+                                     stream);
     if (x_bf16)
-        return launch_tq_generic(static_cast<const uint16_t*>(X), n, d,
-                                 static_cast<const float*>(T), k, codes, s_x, amax_ws, stream);
+        return launch_tq_generic<QM>(static_cast<const uint16_t*>(X), n, d,
+                                     static_cast<const float*>(T), k, codes, s_x, amax_ws, stream);
     if (t_bf16)
-        return launch_tq_generic(static_cast<const float*>(X), n, d,
-                                 static_cast<const uint16_t*>(T), k, codes, s_x, amax_ws, stream);
-    return launch_tq_generic(static_cast<const float*>(X), n, d, static_cast<const float*>(T), k,
-                             codes, s_x, amax_ws, stream);
+        return launch_tq_generic<QM>(static_cast<const float*>(X), n, d,
+                                     static_cast<const uint16_t*>(T), k, codes, s_x, amax_ws,
+                                     stream);
+    return launch_tq_generic<QM>(static_cast<const float*>(X), n, d, static_cast<const float*>(T),
+                                 k, codes, s_x, amax_ws, stream);
+}
+
+hipError_t launch_transform_quant(const void* X, int x_bf16, int64_t n, int64_t d, const void* T,
+                                  int t_bf16, int64_t k, int bits, uint8_t* codes, float* s_x,
+                                  uint32_t* amax_ws, hipStream_t stream) {
+    switch (bits) {
+        case 4: return launch_tq_qm<7>(X, x_bf16, n, d, T, t_bf16, k, codes, s_x, amax_ws, stream);
+        case 6: return launch_tq_qm<31>(X, x_bf16, n, d, T, t_bf16, k, codes, s_x, amax_ws, stream);
+        case 8: return launch_tq_qm<127>(X, x_bf16, n, d, T, t_bf16, k, codes, s_x, amax_ws, stream);
+        default: return hipErrorInvalidValue;   // rejected by the caller
+    }
 }
 
 }  // namespace catk

@@ -119,16 +119,23 @@ constexpr int kScaleSlots = 8;
 static_assert(kBM == kBN, "both operands share the stage layout");
 static_assert(kPpLoads == 4, "four 64-slot instructions per wave per step");
 
-__global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
+// ring[o][stage]: operand o (0 = A, 1 = B), kStages steps deep.
+// sscale[slot]: s_x of a tile's rows and s_w of its outputs; slot = tile
+// index % kScaleSlots.
+typedef u32x4 GemmRing[2][kStages][kPpUnits];
+typedef float GemmScales[kScaleSlots][kBM + kBN];
+
+// I8: codes are one int8 per element (rows of d_in bytes), used by the
+// MFMA as they are; otherwise packed INT4 (rows of d_in / 2 bytes), widened
+// to 16 * code in registers.  A K step is 64 bytes of a row either way:
+// 128 INT4 codes (4 MFMA sub-steps) or 64 int8 codes (2).
+template <bool I8>
+__device__ __forceinline__ void gemm_body(
     const uint8_t* __restrict__ qx, const float* __restrict__ s_x,
     const uint8_t* __restrict__ qw, const float* __restrict__ s_w, int64_t n, int64_t d_in,
-    int64_t d_out, float* __restrict__ y, int32_t* __restrict__ acc_out) {
-    // ring[o][stage]: operand o (0 = A, 1 = B), kStages steps deep
-    __shared__ __attribute__((aligned(16))) u32x4 ring[2][kStages][kPpUnits];
-    // s_x of a tile's rows and s_w of its outputs; slot = tile index % kScaleSlots
-    __shared__ __attribute__((aligned(16))) float sscale[kScaleSlots][kBM + kBN];
-
-    const int64_t row_bytes = d_in / 2;
+    int64_t d_out, float* __restrict__ y, int32_t* __restrict__ acc_out, GemmRing& ring,
+    GemmScales& sscale) {
+    const int64_t row_bytes = I8 ? d_in : d_in / 2;
     const int nk = static_cast<int>((row_bytes + kKBP - 1) / kKBP);
 
     const int tid = threadIdx.x;
@@ -213,6 +220,8 @@ __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
     // base plus immediate offsets.
     const int frag_lane = l32 * kUP;
     const int frag_u0 = (2 * h) ^ gemm_swz(l32);
+    // (int8 codes: unit c of the lane is sub-step c as it is; fb[0..1] hold
+    // B's two units)
     auto load_frags = [&](int st) {
         const u32x4* ra = &ring[0][st][wm * 128 * kUP + frag_lane];
         const u32x4* rb = &ring[1][st][wn * 64 * kUP + frag_lane];
@@ -224,8 +233,12 @@ __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
                 const u32x4 pbj = rb[j * 32 * kUP + uo];
-                fb[2 * c][j] = widen8(pbj, 0);
-                fb[2 * c + 1][j] = widen8(pbj, 1);
+                if constexpr (I8) {
+                    fb[c][j] = __builtin_bit_cast(i32x4, pbj);
+                } else {
+                    fb[2 * c][j] = widen8(pbj, 0);
+                    fb[2 * c + 1][j] = widen8(pbj, 1);
+                }
             }
         }
     };
@@ -234,10 +247,11 @@ __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
         // wave there is in its load phase)
         __builtin_amdgcn_s_setprio(1);
 #pragma unroll
-        for (int s = 0; s < 4; ++s) {
+        for (int s = 0; s < (I8 ? 2 : 4); ++s) {
             i32x4 wa[4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) wa[i] = widen8(pa[s >> 1][i], s & 1);
+            for (int i = 0; i < 4; ++i)
+                wa[i] = I8 ? __builtin_bit_cast(i32x4, pa[s][i]) : widen8(pa[s >> 1][i], s & 1);
             const i32x4* wb = fb[s];
 #pragma unroll
             for (int i = 0; i < 4; ++i)
@@ -249,7 +263,8 @@ __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
         __builtin_amdgcn_s_setprio(0);
     };
     // lane holds column n0 + wn*64 + 32j + l32 and rows m0 + wm*128 + 32i +
-    // 8(r/4) + 4h + r%4.
+    // 8(r/4) + 4h + r%4.  Widened INT4 products carry a factor 256.
+    constexpr int kShift = I8 ? 0 : 8;
     auto epilogue = [&](const GemmTile& tl, int slot) {
         // lane-derived values are recomputed here: hoisted out of the loop
         // they would stay live next to the fragments and accumulators
@@ -288,7 +303,7 @@ __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
                     float* yr = yt + static_cast<int64_t>(wm * 128 + i * 32 + 8 * (r >> 2) + (r & 3)) * d_out;
 #pragma unroll
                     for (int j = 0; j < 2; ++j) {
-                        const int v = acc[i][j][r] >> 8;
+                        const int v = acc[i][j][r] >> kShift;
                         __builtin_nontemporal_store((static_cast<float>(v) * sx[r]) * sw[j], yr + voff[j]);
                     }
                 }
@@ -314,7 +329,7 @@ __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
                     const int row = rb + 8 * (r >> 2) + (r & 3);
                     if (row >= rows_left) continue;
                     const int64_t off = static_cast<int64_t>(row) * d_out + col;
-                    const int v = acc[i][j][r] >> 8;
+                    const int v = acc[i][j][r] >> kShift;
                     const float yv = (static_cast<float>(v) * sx[r]) * sw[j];
                     __builtin_nontemporal_store(yv, yt + off);
                     if (at) at[off] = v;
@@ -424,9 +439,27 @@ __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
     }
 }
 
-hipError_t launch_w4a4_linear(const uint8_t* codes_x, const float* s_x, const uint8_t* codes_w,
-                              const float* s_w, int64_t n, int64_t d_in, int64_t d_out, float* y,
-                              int32_t* acc_out, hipStream_t stream) {
+__global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
+    const uint8_t* __restrict__ qx, const float* __restrict__ s_x,
+    const uint8_t* __restrict__ qw, const float* __restrict__ s_w, int64_t n, int64_t d_in,
+    int64_t d_out, float* __restrict__ y, int32_t* __restrict__ acc_out) {
+    __shared__ __attribute__((aligned(16))) GemmRing ring;
+    __shared__ __attribute__((aligned(16))) GemmScales sscale;
+    gemm_body<false>(qx, s_x, qw, s_w, n, d_in, d_out, y, acc_out, ring, sscale);
+}
+
+__global__ __launch_bounds__(kGemmThreads, kWgPerCu) void int8_gemm_kernel(
+    const uint8_t* __restrict__ qx, const float* __restrict__ s_x,
+    const uint8_t* __restrict__ qw, const float* __restrict__ s_w, int64_t n, int64_t d_in,
+    int64_t d_out, float* __restrict__ y, int32_t* __restrict__ acc_out) {
+    __shared__ __attribute__((aligned(16))) GemmRing ring;
+    __shared__ __attribute__((aligned(16))) GemmScales sscale;
+    gemm_body<true>(qx, s_x, qw, s_w, n, d_in, d_out, y, acc_out, ring, sscale);
+}
+
+static hipError_t launch_gemm(bool i8, const uint8_t* codes_x, const float* s_x,
+                              const uint8_t* codes_w, const float* s_w, int64_t n, int64_t d_in,
+                              int64_t d_out, float* y, int32_t* acc_out, hipStream_t stream) {
     int dev = 0, cus = 0;
     hipError_t err = hipGetDevice(&dev);
     if (err != hipSuccess) return err;
@@ -438,9 +471,24 @@ hipError_t launch_w4a4_linear(const uint8_t* codes_x, const float* s_x, const ui
     const int64_t t_pad = ((T + kXcd - 1) / kXcd) * kXcd;
     if (grid > t_pad) grid = t_pad;
     if (grid < kXcd) grid = kXcd;
-    hipLaunchKernelGGL(w4a4_gemm_kernel, dim3(static_cast<uint32_t>(grid)), dim3(kGemmThreads), 0,
-                       stream, codes_x, s_x, codes_w, s_w, n, d_in, d_out, y, acc_out);
+    hipLaunchKernelGGL(i8 ? int8_gemm_kernel : w4a4_gemm_kernel, dim3(static_cast<uint32_t>(grid)),
+                       dim3(kGemmThreads), 0, stream, codes_x, s_x, codes_w, s_w, n, d_in, d_out, y,
+                       acc_out);
     return hipGetLastError();
+}
+
+hipError_t launch_w4a4_linear(const uint8_t* codes_x, const float* s_x, const uint8_t* codes_w,
+                              const float* s_w, int64_t n, int64_t d_in, int64_t d_out, float* y,
+                              int32_t* acc_out, hipStream_t stream) {
+    return launch_gemm(false, codes_x, s_x, codes_w, s_w, n, d_in, d_out, y, acc_out, stream);
+}
+
+hipError_t launch_int8_linear(const int8_t* codes_x, const float* s_x, const int8_t* codes_w,
+                              const float* s_w, int64_t n, int64_t d_in, int64_t d_out, float* y,
+                              int32_t* acc_out, hipStream_t stream) {
+    return launch_gemm(true, reinterpret_cast<const uint8_t*>(codes_x), s_x,
+                       reinterpret_cast<const uint8_t*>(codes_w), s_w, n, d_in, d_out, y, acc_out,
+                       stream);
 }
 
 }  // namespace catk

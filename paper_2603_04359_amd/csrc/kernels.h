@@ -20,14 +20,19 @@ hipError_t launch_sqnr(const float* y, const float* yt, int64_t count, double* p
                        double* out, hipStream_t stream);
 
 // ---- transform + quantize
-// amax_ws: tq_workspace_bytes(n, d, k) bytes of scratch.
+// amax_ws: tq_workspace_bytes(n, d, k) bytes of scratch.  bits 4: codes
+// [n x d/2] packed INT4; bits 6, 8: codes [n x d] int8.
 size_t tq_workspace_bytes(int64_t n, int64_t d, int64_t k);
 hipError_t launch_transform_quant(const void* X, int x_bf16, int64_t n, int64_t d,
-                                  const void* T, int t_bf16, int64_t k, uint8_t* codes,
-                                  float* s_x, uint32_t* amax_ws, hipStream_t stream);
+                                  const void* T, int t_bf16, int64_t k, int bits,
+                                  uint8_t* codes, float* s_x, uint32_t* amax_ws,
+                                  hipStream_t stream);
 
-// ---- W4A4 GEMM
+// ---- integer GEMM: packed INT4 codes (w4a4) or one int8 per code (int8)
 hipError_t launch_w4a4_linear(const uint8_t* codes_x, const float* s_x, const uint8_t* codes_w,
+                              const float* s_w, int64_t n, int64_t d_in, int64_t d_out,
+                              float* y, int32_t* acc_out, hipStream_t stream);
+hipError_t launch_int8_linear(const int8_t* codes_x, const float* s_x, const int8_t* codes_w,
                               const float* s_w, int64_t n, int64_t d_in, int64_t d_out,
                               float* y, int32_t* acc_out, hipStream_t stream);
 

@@ -70,15 +70,17 @@ def test_transform_quant_invalid_args():
     assert call(d=63) == B.CAT_ERR_INVALID_ARG
     assert call(k=12) == B.CAT_ERR_INVALID_ARG
     assert call(d=80, k=32) == B.CAT_ERR_INVALID_ARG
-    assert call(bits=8) == B.CAT_ERR_UNSUPPORTED
+    assert call(bits=5) == B.CAT_ERR_UNSUPPORTED
+    assert call(bits=3) == B.CAT_ERR_UNSUPPORTED
     assert call(ws=None) == B.CAT_ERR_WORKSPACE
     assert call(wsb=ws - 1) == B.CAT_ERR_WORKSPACE
     assert call(codes=P + 8) == B.CAT_ERR_INVALID_ARG
 
 
-def test_w4a4_invalid_args():
+@pytest.mark.parametrize("fn", ["cat_w4a4_linear", "cat_int8_linear"])
+def test_linear_invalid_args(fn):
     L = cat.lib()
-    f = L.cat_w4a4_linear
+    f = getattr(L, fn)
     assert f(None, P, P, P, 4, 64, 8, P, None, None) == B.CAT_ERR_INVALID_ARG
     assert f(P, P, P, P, 0, 64, 8, P, None, None) == B.CAT_ERR_INVALID_ARG
     assert f(P, P, P, P, 4, 48, 8, P, None, None) == B.CAT_ERR_INVALID_ARG
@@ -116,6 +118,7 @@ def test_host_calls_invalid_args():
         B.CAT_ERR_INVALID_ARG
     assert L.cat_quantize_weights(None, 4, 8, 4, P, P) == B.CAT_ERR_INVALID_ARG
     assert L.cat_quantize_weights(P, 4, 7, 4, P, P) == B.CAT_ERR_INVALID_ARG
+    assert L.cat_quantize_weights(P, 4, 8, 5, P, P) == B.CAT_ERR_UNSUPPORTED
 
 
 def test_binding_rejects_cpu_tensors():

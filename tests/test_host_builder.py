@@ -102,13 +102,14 @@ def test_build_transform_ill_conditioned_block():
     assert np.abs(Te - T_or).max() / np.abs(T_or).max() < 1e-15 * cond
 
 
-def test_quantize_weights_matches_oracle_bit_exact():
+@pytest.mark.parametrize("bits", [4, 6, 8])
+def test_quantize_weights_matches_oracle_bit_exact(bits):
     rng = np.random.default_rng(9)
     Wp = rng.standard_normal((70, 96)) * np.exp(rng.standard_normal(70))[:, None]
     Wp[3] = 0.0
     Wp[5, 7] = 1e3
-    codes, s_w = cat.cat_quantize_weights(Wp, 4)
-    q_or, s_or = o.quantize_weights(Wp, 4)
-    assert np.array_equal(codes, o.pack_int4(q_or))
+    codes, s_w = cat.cat_quantize_weights(Wp, bits)
+    q_or, s_or = o.quantize_weights(Wp, bits)
+    assert np.array_equal(codes, o.pack_int4(q_or) if bits == 4 else q_or)
     assert np.array_equal(s_w, s_or)
     assert s_w[3] == 0 and not codes[3].any()

@@ -47,6 +47,8 @@ def parse():
     p.add_argument("--config", default="mlp_up")
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--wide-steps", type=int, default=10,
+                   help="timed iterations of each 6- and 8-bit comparison pair")
     p.add_argument("--cpu-seconds", type=float, default=10.0,
                    help="minimum CPU time of the oracle sample")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -178,7 +180,6 @@ def main():
     T_host, _, Wp = cat.cat_build_transform(sx_blocks, lay["W"], k, B.CAT_BUILD_CAT, tdt)
     codes_w_h, s_w_h = cat.cat_quantize_weights(Wp, 4)
     t_build = time.perf_counter() - t0
-    del Wp
 
     # ---------------- device-resident inputs (two alternating sets)
     X0 = torch.from_numpy(lay["X"]).to(dev).to(xdt)
@@ -299,6 +300,40 @@ def main():
         "roofline": roofline,
         "host_transform_build_s": t_build,
     }
+    # ---------------- the W6A6 / W8A8 comparison widths (after the timed
+    # steps; not part of the step): the same layer and tokens through
+    # transform+quant at 6 or 8 bits and the int8-code GEMM
+    wide = {"W4A4": {"sqnr_db": sqnr_db}}
+    codes8 = torch.empty((n, d_in), dtype=torch.int8, device=dev)
+    for bits in (6, 8):
+        cw_h, sw_h = cat.cat_quantize_weights(Wp, bits)
+        cw, sw = torch.from_numpy(cw_h).to(dev), torch.from_numpy(sw_h).to(dev)
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)]
+              for _ in range(args.wide_steps)]
+        for i in range(2 + args.wide_steps):
+            e = ev[i - 2] if i >= 2 else None
+            if e: e[0].record()
+            cat.cat_transform_quant(Xs[i % 2], T_dev, k, codes8, s_x, ws_q, bits=bits)
+            if e: e[1].record()
+            cat.cat_int8_linear(codes8, s_x, cw, sw, y_t)
+            if e: e[2].record()
+        cat.cat_sqnr(Ys[(1 + args.wide_steps) % 2], y_t, ws_s, out)
+        torch.cuda.synchronize()
+        tq_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+        g_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+        tq_b = tq_bytes + n * d_in / 2          # one byte per code instead of half
+        g_tops = gemm_ops / (g_ms * 1e-3) / 1e12
+        wide[f"W{bits}A{bits}"] = {
+            "sqnr_db": float(out[2].item()),
+            "transform_quant": {"ms": tq_ms, "GBps": tq_b / (tq_ms * 1e-3) / 1e9,
+                                "frac_hbm_peak": tq_b / (tq_ms * 1e-3) / 1e9 / PEAK["hbm_GBps"]},
+            "int8_linear": {"ms": g_ms, "TOPS": g_tops, "frac_int8_peak": g_tops / PEAK["int8_TOPS"]},
+            "linear_tokens_per_s": n / ((tq_ms + g_ms) * 1e-3)}
+        log(f"[bench] W{bits}A{bits}: transform_quant {tq_ms:.4f} ms, int8_linear {g_ms:.4f} ms "
+            f"({g_tops:.0f} TOP/s), SQNR {wide[f'W{bits}A{bits}']['sqnr_db']:.2f} dB")
+    del Wp
+    rec["wide_codes"] = wide
+
     if not args.no_cpu_baseline:
         log("[bench] CPU oracle baseline")
         T_vals = wl.bf16_bits_to_f32(T_host) if tdt == B.CAT_BF16 else T_host

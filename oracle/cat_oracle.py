@@ -39,6 +39,15 @@ Function -> passage -> what pins it (tests/test_oracle_*.py):
   transform_quant    Sec. 3 eq. 5 (Q(T x)), Sec. 4 eq. 10
                                                 -> T = I gives plain RTN,
                      orthogonal T preserves W x
+  quantize_rows_asym Sec. 2 after Lemma 2.2 (asymmetric range), Sec. 6
+                     (activations per token, asymmetric)
+                                                -> nearest affine grid point
+                     (brute force), min/max map to 0 and 2^b - 1,
+                     constant rows exact, Lemma 2.2 closed form with
+                     2^b - 1 intervals on Gaussian data
+  linear_asym        Sec. 3, eq. 5 with asymmetric activations
+                                                -> brute-force loops,
+                     dequantize-then-multiply product
   pack_int4          storage layout (no passage) -> hand-computed bytes
   w4a4_linear        Sec. 3, eq. 5 (Q(W T^-1) Q(T x))
                                                 -> brute-force loops,
@@ -54,6 +63,11 @@ Every function is pinned; none is "parity unpinned".
 
 Readings where the paper is silent, ambiguous or garbled (same list as in
 the design notes):
+  * Asymmetric activations: 2^b levels from the row minimum, s = fl(r /
+    (2^b - 1)) with r = fl(max - min); codes clamp(rint(fl(fl(z - min) *
+    fl((2^b - 1) / r))), 0, 2^b - 1); dequantized as s q + min (no integer
+    zero point: the minimum is kept in fp32).  A constant row gets s = 0.
+    The product's fp32 order: fl(fl(fl(acc) s_x) + fl(min fl(R))) s_w.
   * Symmetric integer grid: codes in [-qmax, qmax], qmax = 2^(b-1)-1, so
     the grid has N(b) = 2^b - 2 intervals (the paper's N(b) is "the number
     of quantization intervals"; its 2^b - 1 counts a 2^b-level grid).
@@ -265,6 +279,72 @@ def transform_quant(X, T_blocks, bits: int = 4):
 def quantize_weights(W_prime, bits: int = 4):
     """Per-output-channel symmetric RTN of fp32(W') (Sec. 6)."""
     return quantize_rows(np.asarray(W_prime, dtype=np.float64).astype(np.float32), bits)
+
+
+# ------------------------------------------- asymmetric activations
+def quantize_rows_asym(Z32, bits: int = 4):
+    """Asymmetric dynamic per-row quantizer in fp32 (Sec. 2 after Lemma
+    2.2: range r = max_i x_i - min_i x_i; Sec. 6: activations per token,
+    asymmetric).  Affine grid of 2^b levels from the row minimum:
+      r = fl(max - min), s = fl(r / (2^b - 1)), inv = fl((2^b - 1) / r),
+      q = clamp(rint(fl(fl(z - min) * inv)), 0, 2^b - 1),
+    dequantized as s q + min.  A row with r = 0 gets s = 0, q = 0 and is
+    reconstructed exactly by its minimum.
+    Returns (codes int16 [rows, cols] in [0, 2^b - 1], scale fp32 [rows],
+    minimum fp32 [rows])."""
+    Z = _f32(Z32)
+    if Z.ndim != 2:
+        raise ValueError("expected a 2-D array")
+    lv = np.float32((1 << bits) - 1)
+    zmax = np.max(Z, axis=1).astype(np.float32)
+    zmin = np.min(Z, axis=1).astype(np.float32)
+    r = (zmax - zmin).astype(np.float32)
+    nz = r > 0
+    scale = np.zeros_like(r)
+    inv = np.zeros_like(r)
+    scale[nz] = (r[nz] / lv).astype(np.float32)
+    inv[nz] = (lv / r[nz]).astype(np.float32)
+    u = ((Z - zmin[:, None]).astype(np.float32) * inv[:, None]).astype(np.float32)
+    q = np.clip(np.rint(u), 0, lv).astype(np.int16)
+    return q, scale, zmin
+
+
+def transform_quant_asym(X, T_blocks, bits: int = 4):
+    """Q_asym(T x) per token: the block transform as in transform_quant,
+    then the asymmetric per-token quantizer over the whole row."""
+    Z32 = transform_rows(X, T_blocks).astype(np.float32)
+    return quantize_rows_asym(Z32, bits)
+
+
+def linear_asym(codes_x, s_x, min_x, codes_w, s_w):
+    """Q_asym(x)-by-Q(W) product (Sec. 3, eq. 5 with asymmetric
+    activations): sum_j (s q_j + m) w~_j = s sum_j q_j qw_j + m sum_j qw_j,
+    both integer sums exact, then in fp32
+      y_tilde = fl(fl(fl(acc) s_x[t]) + fl(m_t fl(R_o))) s_w[o],
+    acc = sum_j q_tj qw_oj and R_o = sum_j qw_oj.
+    Returns (acc int32 [n, d_out], y_tilde fp32 [n, d_out])."""
+    qx = np.asarray(codes_x, dtype=np.float64)
+    qw = np.asarray(codes_w, dtype=np.float64)
+    acc = qx @ qw.T
+    R = qw.sum(axis=1)
+    for a in (acc, R):
+        if not np.array_equal(a.astype(np.int64).astype(np.float64), a):
+            raise AssertionError("integer sum not exact")
+    sx, mx, sw = _f32(s_x), _f32(min_x), _f32(s_w)
+    t1 = (acc.astype(np.float32) * sx[:, None]).astype(np.float32)
+    t2 = (mx[:, None] * R.astype(np.float32)[None, :]).astype(np.float32)
+    y = ((t1 + t2).astype(np.float32) * sw[None, :]).astype(np.float32)
+    return acc.astype(np.int64).astype(np.int32), y
+
+
+def quantized_forward_asym(X, T_blocks, W_prime, bits: int = 4):
+    """The whole layer with asymmetric per-token activations and
+    symmetric per-channel weights (the paper's set-up, Sec. 6)."""
+    qx, sx, mx = transform_quant_asym(X, T_blocks, bits)
+    qw, sw = quantize_weights(W_prime, bits)
+    acc, yt = linear_asym(qx, sx, mx, qw, sw)
+    return {"codes_x": qx, "s_x": sx, "min_x": mx, "codes_w": qw, "s_w": sw,
+            "acc": acc, "y_tilde": yt}
 
 
 # ------------------------------------------------------------ packing

@@ -467,3 +467,83 @@ def test_cat_improves_sqnr_on_outlier_layer():
         fw = o.quantized_forward(X, T, o.transform_weights(W, T), 4)
         res[name] = o.sqnr(y, fw["y_tilde"])[2]
     assert res["CAT"] > res["H"] + 3.0 > res["I"] + 3.0
+
+
+# ------------------------------------------------- asymmetric activations
+@pytest.mark.parametrize("bits", [4, 8])
+def test_asym_quantizer_is_nearest_affine_grid_point_brute_force(bits):
+    # Every code is the nearest of the 2^b levels min + s l (l = 0 .. 2^b - 1)
+    # to z (brute-force argmin), ties aside; error within half a step.
+    L = (1 << bits) - 1
+    rng = np.random.default_rng(31 + bits)
+    Z = (rng.standard_normal((64, 48)) * np.exp(rng.standard_normal(48)) +
+         rng.standard_normal((64, 1)) * 3).astype(np.float32)
+    q, s, m = o.quantize_rows_asym(Z, bits)
+    Zd = Z.astype(np.float64)
+    r = Zd.max(1) - Zd.min(1)
+    u = (Zd - Zd.min(1)[:, None]) * (L / r)[:, None]
+    levels = np.arange(L + 1)
+    best = levels[np.argmin(np.abs(u[..., None] - levels), axis=-1)]
+    near_tie = np.abs(np.abs(u - np.floor(u)) - 0.5) < 1e-5
+    assert np.all((q == best) | near_tie)
+    assert q.min() >= 0 and q.max() <= L
+    err = np.abs(Zd - (q * s[:, None].astype(np.float64) + m[:, None]))
+    assert np.all(err <= 0.5 * s[:, None] * (1 + 1e-5) + 1e-6 * np.abs(Zd))
+
+
+def test_asym_quantizer_extremes_and_constant_rows():
+    rng = np.random.default_rng(33)
+    Z = rng.standard_normal((32, 40)).astype(np.float32)
+    Z[3] = 2.5                                    # constant row
+    Z[4] = 0.0                                    # zero row
+    Z[5] = np.abs(Z[5]) + 1.0                     # all positive: no zero inside
+    q, s, m = o.quantize_rows_asym(Z, 4)
+    rows = [i for i in range(32) if i not in (3, 4)]
+    assert np.all(q[rows, np.argmin(Z[rows], axis=1)] == 0)
+    assert np.all(q[rows, np.argmax(Z[rows], axis=1)] == 15)
+    for i in (3, 4):
+        assert s[i] == 0 and not q[i].any() and m[i] == Z[i, 0]
+    assert m[5] == Z[5].min() and m[5] > 0
+
+
+def test_asym_sqnr_matches_lemma_2_2_closed_form():
+    # Lemma 2.2 with the asymmetric range and its 2^b - 1 intervals:
+    # SQNR(W x~) ~= 12 (2^b - 1)^2 C_asym(x) A(x, W), on shifted Gaussian
+    # data (where the asymmetric range is the smaller one).
+    rng = np.random.default_rng(34)
+    X = rng.standard_normal((4096, 256)) + 1.5
+    W = rng.standard_normal((128, 256))
+    for bits in (4, 6):
+        q, s, m = o.quantize_rows_asym(X.astype(np.float32), bits)
+        Xq = q * s[:, None].astype(np.float64) + m[:, None]
+        Y = X @ W.T
+        E = (X - Xq) @ W.T
+        brute = 10 * np.log10(np.sum(Y * Y) / np.sum(E * E))
+        pred = 10 * np.log10(12 * ((1 << bits) - 1) ** 2 *
+                             o.concentration_act(X, asymmetric=True) * o.alignment(X, W))
+        assert brute == pytest.approx(pred, abs=0.15), (bits, brute, pred)
+        # and it beats the symmetric quantizer on this shifted data
+        qs, ss = o.quantize_rows(X.astype(np.float32), bits)
+        Es = (X - qs * ss[:, None]) @ W.T
+        assert brute > 10 * np.log10(np.sum(Y * Y) / np.sum(Es * Es)) + 2.0
+
+
+def test_linear_asym_brute_force_loops_and_fake_quant():
+    rng = np.random.default_rng(35)
+    qx = rng.integers(0, 16, size=(3, 40)).astype(np.int16)
+    qw = wl.random_codes(4, 40, seed=36)
+    sx = np.array([0.5, 0.25, 0.0], np.float32)
+    mx = np.array([-1.25, 0.5, 3.0], np.float32)
+    sw = np.array([1.0, 0.125, 2.0, 0.75], np.float32)
+    acc, y = o.linear_asym(qx, sx, mx, qw, sw)
+    for t in range(3):
+        for j in range(4):
+            ref = sum(int(a) * int(b) for a, b in zip(qx[t], qw[j]))
+            assert acc[t, j] == ref
+            R = int(qw[j].astype(np.int64).sum())
+            # power-of-two scales and short sums: every fp32 step is exact
+            assert float(y[t, j]) == (ref * float(sx[t]) + float(mx[t]) * R) * float(sw[j])
+    # dequantize-then-multiply in fp64 gives the same product
+    X = qx * sx[:, None].astype(np.float64) + mx[:, None]
+    Wq = qw * sw[:, None].astype(np.float64)
+    np.testing.assert_allclose(y, X @ Wq.T, rtol=1e-6, atol=1e-6)

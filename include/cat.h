@@ -186,6 +186,43 @@ int cat_int8_linear(const int8_t* codes_x, const float* s_x,
                     int64_t d_in, int64_t d_out, float* y_tilde,
                     int32_t* acc_out, void* stream);
 
+/* ------------------------------------------------------------------
+ * Asymmetric per-token activations (the paper's own set-up, Sec. 6:
+ * activations per token, asymmetric; range r = max - min, Sec. 2 after
+ * Lemma 2.2), INT4.
+ *
+ * cat_transform_quant_asym: z as in cat_transform_quant, then per token
+ *   zmin = min z, r = fl(max z - zmin),
+ *   s_x = fl(r / 15), inv = fl(15 / r)                 (both 0 if r == 0)
+ *   q = clamp(rint(fl(fl(z - zmin) * inv)), 0, 15)     (ties to even)
+ * so that z ~ s_x q + zmin.  codes hold q - 8 as packed INT4 (the layout
+ * above, values in [-8, 7]); zmin_x device fp32 [n] (written).  Other
+ * arguments, the workspace and errors as cat_transform_quant (bits is 4).
+ *
+ * cat_w4a4_linear_asym: the product of those activations with symmetric
+ * INT4 weights,
+ *   acc[t, o] = sum_j q[t, j] qw[o, j] (q in [0, 15]; int32, exact)
+ *   y_tilde   = fl(fl(fl(acc) s_x[t]) + fl(zmin_x[t] fl(rsum_w[o]))) s_w[o]
+ * with rsum_w[o] = sum_j qw[o, j] (device int32 [d_out], from
+ * cat_weight_code_sums).  acc_out, when non-NULL, receives acc.  Other
+ * arguments and errors as cat_w4a4_linear.
+ *
+ * cat_weight_code_sums: host; rsum_out[o] = sum of row o's codes of the
+ * packed INT4 [d_out x d_in/2] codes_w; d_in even.
+ */
+int cat_transform_quant_asym(const void* X, int x_dtype, int64_t n, int64_t d,
+                             const void* T, int t_dtype, int64_t k,
+                             uint8_t* codes, float* s_x, float* zmin_x,
+                             void* workspace, size_t workspace_bytes,
+                             void* stream);
+int cat_w4a4_linear_asym(const uint8_t* codes_x, const float* s_x,
+                         const float* zmin_x, const uint8_t* codes_w,
+                         const float* s_w, const int32_t* rsum_w, int64_t n,
+                         int64_t d_in, int64_t d_out, float* y_tilde,
+                         int32_t* acc_out, void* stream);
+int cat_weight_code_sums(const uint8_t* codes_w, int64_t d_out, int64_t d_in,
+                         int32_t* rsum_out);
+
 /* ------------------------------------------------------------------ (4)
  * SQNR reduction (Sec. 2, eq. 1: E||W x||^2 / E||W x - W~ x~||^2, with
  * the expectations replaced by sums over all tokens and outputs).

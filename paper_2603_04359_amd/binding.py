@@ -42,7 +42,8 @@ CAT_MAX_BLOCK = 512
 EXPORTED = (
     "cat_cov_workspace_bytes", "cat_cov_accumulate", "cat_transform_quant_workspace_bytes",
     "cat_transform_quant",
-    "cat_w4a4_linear", "cat_int8_linear", "cat_sqnr_workspace_bytes", "cat_sqnr", "cat_build_transform",
+    "cat_w4a4_linear", "cat_int8_linear", "cat_transform_quant_asym", "cat_w4a4_linear_asym",
+    "cat_weight_code_sums", "cat_sqnr_workspace_bytes", "cat_sqnr", "cat_build_transform",
     "cat_quantize_weights", "cat_last_error", "cat_version",
 )
 
@@ -84,6 +85,14 @@ def lib() -> ctypes.CDLL:
     L.cat_w4a4_linear.restype = _int
     L.cat_int8_linear.argtypes = [_vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp]
     L.cat_int8_linear.restype = _int
+    L.cat_transform_quant_asym.argtypes = [_vp, _int, _i64, _i64, _vp, _int, _i64, _vp, _vp, _vp,
+                                           _vp, _sz, _vp]
+    L.cat_transform_quant_asym.restype = _int
+    L.cat_w4a4_linear_asym.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp,
+                                       _vp]
+    L.cat_w4a4_linear_asym.restype = _int
+    L.cat_weight_code_sums.argtypes = [_vp, _i64, _i64, _vp]
+    L.cat_weight_code_sums.restype = _int
     L.cat_sqnr_workspace_bytes.argtypes = [_i64]
     L.cat_sqnr_workspace_bytes.restype = _sz
     L.cat_sqnr.argtypes = [_vp, _vp, _i64, _vp, _sz, _vp, _vp]
@@ -238,6 +247,58 @@ def cat_int8_linear(codes_x, s_x, codes_w, s_w, y_tilde, acc_out=None, stream=No
     _check("cat_int8_linear",
            lib().cat_int8_linear(pcx, psx, pcw, psw, n, d_in, d_out, py, pacc,
                                  _stream_ptr(stream)))
+
+
+def cat_transform_quant_asym(X, T, k: int, codes, s_x, zmin_x, workspace, stream=None):
+    """Asymmetric INT4: codes uint8 [n, d/2] (q - 8 packed), s_x and
+    zmin_x [n] fp32, from X [n, d] and T [d/k, k, k]."""
+    torch = _torch()
+    px = _dev_ptr(X, "X", (torch.bfloat16, torch.float32))
+    pt = _dev_ptr(T, "T", (torch.bfloat16, torch.float32))
+    pc = _dev_ptr(codes, "codes", (torch.uint8,))
+    ps = _dev_ptr(s_x, "s_x", (torch.float32,))
+    pm = _dev_ptr(zmin_x, "zmin_x", (torch.float32,))
+    pw = _dev_ptr(workspace, "workspace")
+    if X.dim() != 2:
+        raise ValueError("X must be [n, d]")
+    n, d = X.shape
+    if tuple(codes.shape) != (n, d // 2):
+        raise ValueError(f"codes must be [{n}, {d // 2}]")
+    wbytes = workspace.numel() * workspace.element_size()
+    _check("cat_transform_quant_asym",
+           lib().cat_transform_quant_asym(px, _dtype_code(X), n, d, pt, _dtype_code(T), k, pc, ps,
+                                          pm, pw, wbytes, _stream_ptr(stream)))
+
+
+def cat_w4a4_linear_asym(codes_x, s_x, zmin_x, codes_w, s_w, rsum_w, y_tilde, acc_out=None,
+                         stream=None):
+    """y_tilde [n, d_out] fp32 from asymmetric activation codes and
+    symmetric weight codes with their row sums rsum_w int32 [d_out]."""
+    torch = _torch()
+    pcx = _dev_ptr(codes_x, "codes_x", (torch.uint8,))
+    psx = _dev_ptr(s_x, "s_x", (torch.float32,))
+    pmx = _dev_ptr(zmin_x, "zmin_x", (torch.float32,))
+    pcw = _dev_ptr(codes_w, "codes_w", (torch.uint8,))
+    psw = _dev_ptr(s_w, "s_w", (torch.float32,))
+    prs = _dev_ptr(rsum_w, "rsum_w", (torch.int32,))
+    py = _dev_ptr(y_tilde, "y_tilde", (torch.float32,))
+    pacc = _dev_ptr(acc_out, "acc_out", (torch.int32,), allow_none=True)
+    n, half = codes_x.shape
+    d_out = codes_w.shape[0]
+    if codes_w.shape[1] != half:
+        raise ValueError("codes_x and codes_w disagree on d_in")
+    _check("cat_w4a4_linear_asym",
+           lib().cat_w4a4_linear_asym(pcx, psx, pmx, pcw, psw, prs, n, 2 * half, d_out, py, pacc,
+                                      _stream_ptr(stream)))
+
+
+def cat_weight_code_sums(codes_w):
+    """Host: int32 [d_out] row sums of packed INT4 weight codes [d_out, d_in/2]."""
+    c, pc = _host(codes_w, np.uint8, "codes_w")
+    d_out, half = c.shape
+    out = np.empty(d_out, dtype=np.int32)
+    _check("cat_weight_code_sums", lib().cat_weight_code_sums(pc, d_out, 2 * half, out.ctypes.data))
+    return out
 
 
 def cat_sqnr_workspace_bytes(count: int) -> int:

@@ -122,14 +122,50 @@ extern "C" int cat_transform_quant(const void* X, int x_dtype, int64_t n, int64_
     }
 }
 
+extern "C" int cat_transform_quant_asym(const void* X, int x_dtype, int64_t n, int64_t d,
+                                        const void* T, int t_dtype, int64_t k, uint8_t* codes,
+                                        float* s_x, float* zmin_x, void* workspace,
+                                        size_t workspace_bytes, void* stream) {
+    const char* fn = "cat_transform_quant_asym";
+    try {
+        if (!X || !T || !codes || !s_x || !zmin_x)
+            return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": NULL pointer");
+        if (!valid_dtype(x_dtype) || !valid_dtype(t_dtype))
+            return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": bad dtype");
+        if (n < 1 || d < 2) return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": need n >= 1, d >= 2");
+        if (d % 2) return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": d must be even");
+        if (!cat::is_pow2(k) || k > CAT_MAX_BLOCK)
+            return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": k must be a power of two <= 512");
+        if (d % k) return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": d % k != 0");
+        if (!cat::aligned16(X) || !cat::aligned16(T) || !cat::aligned16(codes) ||
+            !cat::aligned16(s_x) || !cat::aligned16(zmin_x))
+            return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": pointers must be 16-byte aligned");
+        if (!workspace || workspace_bytes < cat_transform_quant_workspace_bytes(n, d, k))
+            return fail(CAT_ERR_WORKSPACE, std::string(fn) + ": workspace missing or too small");
+        if (!cat::aligned16(workspace))
+            return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": workspace must be 16-byte aligned");
+        if (int rc = require_device(fn)) return rc;
+        const hipError_t err = catk::launch_transform_quant_asym(
+            X, x_dtype == CAT_BF16, n, d, T, t_dtype == CAT_BF16, k, codes, s_x, zmin_x,
+            static_cast<uint32_t*>(workspace), static_cast<hipStream_t>(stream));
+        if (err != hipSuccess) return hip_fail(fn, err);
+        return CAT_OK;
+    } catch (const std::exception& e) {
+        return fail(CAT_ERR_INTERNAL, std::string(fn) + ": " + e.what());
+    } catch (...) {
+        return fail(CAT_ERR_INTERNAL, std::string(fn) + ": unknown error");
+    }
+}
+
 namespace {
 
 // Shared checks and launch of the two integer GEMM entry points.
 int linear_call(const char* fn, bool i8, const void* codes_x, const float* s_x,
                 const void* codes_w, const float* s_w, int64_t n, int64_t d_in, int64_t d_out,
-                float* y_tilde, int32_t* acc_out, void* stream) {
+                float* y_tilde, int32_t* acc_out, void* stream, bool asym = false,
+                const float* zmin_x = nullptr, const int32_t* rsum_w = nullptr) {
     try {
-        if (!codes_x || !s_x || !codes_w || !s_w || !y_tilde)
+        if (!codes_x || !s_x || !codes_w || !s_w || !y_tilde || (asym && (!zmin_x || !rsum_w)))
             return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": NULL pointer");
         if (n < 1 || d_out < 1 || d_in < 32)
             return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": need n, d_out >= 1 and d_in >= 32");
@@ -137,12 +173,16 @@ int linear_call(const char* fn, bool i8, const void* codes_x, const float* s_x,
         if (d_in > CAT_MAX_D_IN)
             return fail(CAT_ERR_UNSUPPORTED, std::string(fn) + ": d_in exceeds CAT_MAX_D_IN");
         if (!cat::aligned16(codes_x) || !cat::aligned16(codes_w) || !cat::aligned16(s_x) ||
-            !cat::aligned16(s_w) || !cat::aligned16(y_tilde) || (acc_out && !cat::aligned16(acc_out)))
+            !cat::aligned16(s_w) || !cat::aligned16(y_tilde) || (acc_out && !cat::aligned16(acc_out)) ||
+            (asym && (!cat::aligned16(zmin_x) || !cat::aligned16(rsum_w))))
             return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": pointers must be 16-byte aligned");
         if (int rc = require_device(fn)) return rc;
         const hipStream_t st = static_cast<hipStream_t>(stream);
         const hipError_t err =
-            i8 ? catk::launch_int8_linear(static_cast<const int8_t*>(codes_x), s_x,
+            asym ? catk::launch_w4a4_linear_asym(static_cast<const uint8_t*>(codes_x), s_x, zmin_x,
+                                                 static_cast<const uint8_t*>(codes_w), s_w, rsum_w,
+                                                 n, d_in, d_out, y_tilde, acc_out, st)
+            : i8 ? catk::launch_int8_linear(static_cast<const int8_t*>(codes_x), s_x,
                                           static_cast<const int8_t*>(codes_w), s_w, n, d_in, d_out,
                                           y_tilde, acc_out, st)
                : catk::launch_w4a4_linear(static_cast<const uint8_t*>(codes_x), s_x,
@@ -164,6 +204,14 @@ extern "C" int cat_w4a4_linear(const uint8_t* codes_x, const float* s_x, const u
                                float* y_tilde, int32_t* acc_out, void* stream) {
     return linear_call("cat_w4a4_linear", false, codes_x, s_x, codes_w, s_w, n, d_in, d_out,
                        y_tilde, acc_out, stream);
+}
+
+extern "C" int cat_w4a4_linear_asym(const uint8_t* codes_x, const float* s_x, const float* zmin_x,
+                                    const uint8_t* codes_w, const float* s_w, const int32_t* rsum_w,
+                                    int64_t n, int64_t d_in, int64_t d_out, float* y_tilde,
+                                    int32_t* acc_out, void* stream) {
+    return linear_call("cat_w4a4_linear_asym", false, codes_x, s_x, codes_w, s_w, n, d_in, d_out,
+                       y_tilde, acc_out, stream, true, zmin_x, rsum_w);
 }
 
 extern "C" int cat_int8_linear(const int8_t* codes_x, const float* s_x, const int8_t* codes_w,

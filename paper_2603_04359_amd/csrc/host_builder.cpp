@@ -391,3 +391,21 @@ extern "C" int cat_quantize_weights(const double* W_prime, int64_t d_out, int64_
     }
     return CAT_OK;
 }
+
+extern "C" int cat_weight_code_sums(const uint8_t* codes_w, int64_t d_out, int64_t d_in,
+                                    int32_t* rsum_out) {
+    using cat::fail;
+    if (!codes_w || !rsum_out) return fail(CAT_ERR_INVALID_ARG, "cat_weight_code_sums: NULL pointer");
+    if (d_out < 1 || d_in < 2 || (d_in & 1))
+        return fail(CAT_ERR_INVALID_ARG, "cat_weight_code_sums: d_out >= 1, d_in even >= 2");
+    for (int64_t o = 0; o < d_out; ++o) {
+        const uint8_t* row = codes_w + o * (d_in / 2);
+        int64_t sum = 0;
+        for (int64_t j = 0; j < d_in / 2; ++j) {
+            const int lo = row[j] & 0xF, hi = row[j] >> 4;   // two's complement nibbles
+            sum += (lo >= 8 ? lo - 16 : lo) + (hi >= 8 ? hi - 16 : hi);
+        }
+        rsum_out[o] = static_cast<int32_t>(sum);
+    }
+    return CAT_OK;
+}

@@ -54,6 +54,36 @@ __device__ __forceinline__ int quant_code(float z, float inv) {
     return static_cast<int>(u);
 }
 
+// Asymmetric INT4 (activations per token, Sec. 6): the row's minimum and
+// maximum of z are kept as order-preserving 32-bit keys (larger key =
+// larger float; 0 = no value yet), the maximum as a key and the minimum as
+// the key's complement, so both fold with an unsigned atomic max.
+__device__ __forceinline__ uint32_t fkey(float f) {
+    const uint32_t b = __float_as_uint(f);
+    return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+__device__ __forceinline__ float fkey_value(uint32_t k) {
+    return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
+}
+// Code q - 8 (q in [0, 15] on the affine grid from the minimum) as a
+// signed INT4 value, given inv = fl(15 / r).
+__device__ __forceinline__ int asym_code(float z, float zmin, float inv) {
+    float u = (z - zmin) * inv;
+    u = __builtin_rintf(u);
+    u = fminf(fmaxf(u, 0.0f), 15.0f);
+    return static_cast<int>(u) - 8;
+}
+// Scale and inverse from the row's keys (ws_max[t], ws_min[t]).
+__device__ __forceinline__ void asym_scale(uint32_t kmax, uint32_t kmin_c, float& zmin, float& s,
+                                           float& inv) {
+    const float zmax = fkey_value(kmax);
+    zmin = fkey_value(~kmin_c);
+    const float r = zmax - zmin;
+    const bool nz = r > 0.0f;
+    s = nz ? __fdiv_rn(r, 15.0f) : 0.0f;
+    inv = nz ? __fdiv_rn(15.0f, r) : 0.0f;
+}
+
 // ------------------------------------------------------------ generic path
 template <typename XT, typename TT>
 __device__ __forceinline__ float tq_dot(const XT* __restrict__ X, const TT* __restrict__ T,
@@ -107,6 +137,42 @@ __global__ __launch_bounds__(kTqThreads) void tq_generic_quant_kernel(
         *reinterpret_cast<uint16_t*>(codes + t * d + 2 * cp) =
             static_cast<uint16_t>((q0 & 0xFF) | ((q1 & 0xFF) << 8));
     }
+}
+
+template <typename XT, typename TT>
+__global__ __launch_bounds__(kTqThreads) void tq_generic_minmax_kernel(
+    const XT* __restrict__ X, const TT* __restrict__ T, int64_t n, int64_t d, int64_t k,
+    uint32_t* __restrict__ ws) {
+    const int64_t pairs = d / 2;
+    const int64_t u = static_cast<int64_t>(blockIdx.x) * kTqThreads + threadIdx.x;
+    if (u >= n * pairs) return;
+    const int64_t t = u / pairs;
+    const int64_t c = 2 * (u - t * pairs);
+    const uint32_t k0 = fkey(tq_dot(X, T, t, d, k, c));
+    const uint32_t k1 = fkey(tq_dot(X, T, t, d, k, c + 1));
+    atomicMax(ws + t, max(k0, k1));
+    atomicMax(ws + n + t, max(~k0, ~k1));
+}
+
+template <typename XT, typename TT>
+__global__ __launch_bounds__(kTqThreads) void tq_generic_quant_asym_kernel(
+    const XT* __restrict__ X, const TT* __restrict__ T, int64_t n, int64_t d, int64_t k,
+    const uint32_t* __restrict__ ws, uint8_t* __restrict__ codes, float* __restrict__ s_x,
+    float* __restrict__ zmin_x) {
+    const int64_t pairs = d / 2;
+    const int64_t u = static_cast<int64_t>(blockIdx.x) * kTqThreads + threadIdx.x;
+    if (u >= n * pairs) return;
+    const int64_t t = u / pairs;
+    const int64_t cp = u - t * pairs;
+    float zmin, s, inv;
+    asym_scale(ws[t], ws[n + t], zmin, s, inv);
+    if (cp == 0) {
+        s_x[t] = s;
+        zmin_x[t] = zmin;
+    }
+    const int q0 = asym_code(tq_dot(X, T, t, d, k, 2 * cp), zmin, inv);
+    const int q1 = asym_code(tq_dot(X, T, t, d, k, 2 * cp + 1), zmin, inv);
+    codes[t * pairs + cp] = static_cast<uint8_t>((q0 & 0xF) | ((q1 & 0xF) << 4));
 }
 
 // --------------------------------------------------------------- MFMA path
@@ -313,14 +379,16 @@ __device__ __forceinline__ int tq_xswz(int r) {
     return K == 128 ? ((r ^ (r >> 4)) & 15) : (r & 31);
 }
 
-template <int K, bool QUANT, int QM>
+// ASYM: asymmetric INT4 (pass 1 folds the row's max and min keys, pass 2
+// writes codes q - 8 and the row minimum to zmin_x).
+template <int K, bool QUANT, int QM, bool ASYM = false>
 __global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ T, int64_t n, int64_t d,
     int64_t R, uint32_t* __restrict__ amax_ws, uint8_t* __restrict__ codes,
-    float* __restrict__ s_x) {
+    float* __restrict__ s_x, float* __restrict__ zmin_x) {
     using C = TqRing<K>;
     __shared__ __attribute__((aligned(16))) u32x4 ring[2][C::STAGE];
-    __shared__ uint32_t red[4][C::TT];
+    __shared__ uint32_t red[ASYM ? 8 : 4][C::TT];
 
     const int64_t nbj = (d / K) * C::NCHUNK;
     const int64_t bj = blockIdx.x % nbj;
@@ -382,7 +450,67 @@ __global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
             }
         }
 
-        if constexpr (!QUANT) {
+        if constexpr (!QUANT && ASYM) {
+#pragma unroll
+            for (int sb = 0; sb < C::NSB; ++sb) {
+                uint32_t mx = 0, mn = 0;
+#pragma unroll
+                for (int q = 0; q < 16; ++q) {
+                    const uint32_t kq = fkey(acc[sb][q]);
+                    mx = max(mx, kq);
+                    mn = max(mn, ~kq);
+                }
+                mx = max(mx, static_cast<uint32_t>(__shfl_xor(static_cast<int>(mx), 32)));
+                mn = max(mn, static_cast<uint32_t>(__shfl_xor(static_cast<int>(mn), 32)));
+                if (h == 0) {
+                    red[wave][sb * 32 + l32] = mx;
+                    red[4 + wave][sb * 32 + l32] = mn;
+                }
+            }
+            lds_barrier();
+            for (int idx = threadIdx.x; idx < C::TT; idx += kTqThreads) {
+                const uint32_t mx = max(max(red[0][idx], red[1][idx]), max(red[2][idx], red[3][idx]));
+                const uint32_t mn = max(max(red[4][idx], red[5][idx]), max(red[6][idx], red[7][idx]));
+                const int64_t t = tile * C::TT + idx;
+                if (t < n) {
+                    atomicMax(amax_ws + t, mx);
+                    atomicMax(amax_ws + n + t, mn);
+                }
+            }
+        } else if constexpr (ASYM) {
+            // packed like the symmetric INT4 branch below, codes q - 8
+#pragma unroll
+            for (int sb = 0; sb < C::NSB; ++sb) {
+                const int64_t t = tile * C::TT + sb * 32 + l32;
+                const bool valid = t < n;
+                float zmin = 0.0f, s = 0.0f, inv = 0.0f;
+                if (valid) asym_scale(amax_ws[t], amax_ws[n + t], zmin, s, inv);
+                if (valid && h == 0 && wave == 0 && b == 0 && jc == 0) {
+                    s_x[t] = s;
+                    zmin_x[t] = zmin;
+                }
+                uint32_t v[4];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    uint32_t pk = 0;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        pk |= static_cast<uint32_t>(asym_code(acc[sb][4 * q + e], zmin, inv) & 0xF)
+                              << (4 * e);
+                    v[q] = pk;
+                }
+                uint32_t* crow =
+                    reinterpret_cast<uint32_t*>(codes + t * (d / 2) + (b * K + row0) / 2);
+#pragma unroll
+                for (int qp = 0; qp < 4; qp += 2) {
+                    const uint32_t send = h ? v[qp] : v[qp + 1];
+                    const uint32_t recv =
+                        static_cast<uint32_t>(__shfl_xor(static_cast<int>(send), 32));
+                    const uint32_t word = h ? (recv | (v[qp + 1] << 16)) : (v[qp] | (recv << 16));
+                    if (valid) crow[qp + h] = word;
+                }
+            }
+        } else if constexpr (!QUANT) {
 #pragma unroll
             for (int sb = 0; sb < C::NSB; ++sb) {
                 uint32_t m = 0;
@@ -838,9 +966,10 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
     }
 }
 
-template <int K, int QM>
+template <int K, int QM, bool ASYM = false>
 hipError_t launch_tq_ring(const uint16_t* X, int64_t n, int64_t d, const uint16_t* T,
-                          uint8_t* codes, float* s_x, uint32_t* ws, hipStream_t stream) {
+                          uint8_t* codes, float* s_x, uint32_t* ws, hipStream_t stream,
+                          float* zmin_x = nullptr) {
     using C = TqRing<K>;
     int dev = 0, cus = 0;
     hipError_t err = hipGetDevice(&dev);
@@ -854,12 +983,12 @@ hipError_t launch_tq_ring(const uint16_t* X, int64_t n, int64_t d, const uint16_
     if (R > ntiles) R = ntiles;
     if (R < 1) R = 1;
     const int64_t grid = nbj * R;
-    hipLaunchKernelGGL((tq_ring_kernel<K, false, 7>), dim3(static_cast<uint32_t>(grid)),
-                       dim3(kTqThreads), 0, stream, X, T, n, d, R, ws, codes, s_x);
+    hipLaunchKernelGGL((tq_ring_kernel<K, false, 7, ASYM>), dim3(static_cast<uint32_t>(grid)),
+                       dim3(kTqThreads), 0, stream, X, T, n, d, R, ws, codes, s_x, zmin_x);
     err = hipGetLastError();
     if (err != hipSuccess) return err;
-    hipLaunchKernelGGL((tq_ring_kernel<K, true, QM>), dim3(static_cast<uint32_t>(grid)),
-                       dim3(kTqThreads), 0, stream, X, T, n, d, R, ws, codes, s_x);
+    hipLaunchKernelGGL((tq_ring_kernel<K, true, QM, ASYM>), dim3(static_cast<uint32_t>(grid)),
+                       dim3(kTqThreads), 0, stream, X, T, n, d, R, ws, codes, s_x, zmin_x);
     return hipGetLastError();
 }
 
@@ -1020,6 +1149,54 @@ hipError_t launch_transform_quant(const void* X, int x_bf16, int64_t n, int64_t 
         case 8: return launch_tq_qm<127>(X, x_bf16, n, d, T, t_bf16, k, codes, s_x, amax_ws, stream);
         default: return hipErrorInvalidValue;   // rejected by the caller
     }
+}
+
+template <typename XT, typename TT>
+static hipError_t launch_tq_generic_asym(const XT* X, int64_t n, int64_t d, const TT* T,
+                                         int64_t k, uint8_t* codes, float* s_x, float* zmin_x,
+                                         uint32_t* ws, hipStream_t stream) {
+    const int64_t units = n * (d / 2);
+    const int64_t grid = (units + kTqThreads - 1) / kTqThreads;
+    hipLaunchKernelGGL((tq_generic_minmax_kernel<XT, TT>), dim3(static_cast<uint32_t>(grid)),
+                       dim3(kTqThreads), 0, stream, X, T, n, d, k, ws);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL((tq_generic_quant_asym_kernel<XT, TT>), dim3(static_cast<uint32_t>(grid)),
+                       dim3(kTqThreads), 0, stream, X, T, n, d, k, ws, codes, s_x, zmin_x);
+    return hipGetLastError();
+}
+
+// Asymmetric INT4: two passes (row max and min keys, then codes), on the
+// ring kernels for bf16 with k in {128, 256, 512}, else the vector ALU.
+hipError_t launch_transform_quant_asym(const void* X, int x_bf16, int64_t n, int64_t d,
+                                       const void* T, int t_bf16, int64_t k, uint8_t* codes,
+                                       float* s_x, float* zmin_x, uint32_t* ws,
+                                       hipStream_t stream) {
+    hipLaunchKernelGGL(fill_zero_u32_kernel, dim3(static_cast<uint32_t>((2 * n + 255) / 256)),
+                       dim3(256), 0, stream, ws, 2 * n);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    if (x_bf16 && t_bf16) {
+        const uint16_t* Xb = static_cast<const uint16_t*>(X);
+        const uint16_t* Tb = static_cast<const uint16_t*>(T);
+        switch (k) {
+            case 128: return launch_tq_ring<128, 7, true>(Xb, n, d, Tb, codes, s_x, ws, stream, zmin_x);
+            case 256: return launch_tq_ring<256, 7, true>(Xb, n, d, Tb, codes, s_x, ws, stream, zmin_x);
+            case 512: return launch_tq_ring<512, 7, true>(Xb, n, d, Tb, codes, s_x, ws, stream, zmin_x);
+            default:
+                return launch_tq_generic_asym(Xb, n, d, Tb, k, codes, s_x, zmin_x, ws, stream);
+        }
+    }
+    if (x_bf16)
+        return launch_tq_generic_asym(static_cast<const uint16_t*>(X), n, d,
+                                      static_cast<const float*>(T), k, codes, s_x, zmin_x, ws,
+                                      stream);
+    if (t_bf16)
+        return launch_tq_generic_asym(static_cast<const float*>(X), n, d,
+                                      static_cast<const uint16_t*>(T), k, codes, s_x, zmin_x, ws,
+                                      stream);
+    return launch_tq_generic_asym(static_cast<const float*>(X), n, d,
+                                  static_cast<const float*>(T), k, codes, s_x, zmin_x, ws, stream);
 }
 
 }  // namespace catk

@@ -129,12 +129,18 @@ typedef float GemmScales[kScaleSlots][kBM + kBN];
 // MFMA as they are; otherwise packed INT4 (rows of d_in / 2 bytes), widened
 // to 16 * code in registers.  A K step is 64 bytes of a row either way:
 // 128 INT4 codes (4 MFMA sub-steps) or 64 int8 codes (2).
-template <bool I8>
+// ASYM (INT4 only): asymmetric activations stored as q - 8 with the row
+// minimum zmin_x, weights with row code sums rsum_w: the epilogue adds
+// 8 R_o back (int32, exact) and forms
+// y = fl(fl(fl(acc) s_x) + fl(zmin fl(R_o))) s_w.
+template <bool I8, bool ASYM>
 __device__ __forceinline__ void gemm_body(
     const uint8_t* __restrict__ qx, const float* __restrict__ s_x,
     const uint8_t* __restrict__ qw, const float* __restrict__ s_w, int64_t n, int64_t d_in,
     int64_t d_out, float* __restrict__ y, int32_t* __restrict__ acc_out, GemmRing& ring,
-    GemmScales& sscale) {
+    GemmScales& sscale, const float* __restrict__ zmin_x, const int32_t* __restrict__ rsum_w,
+    GemmScales* sasym) {
+    static_assert(!(I8 && ASYM), "asymmetric codes are INT4");
     const int64_t row_bytes = I8 ? d_in : d_in / 2;
     const int nk = static_cast<int>((row_bytes + kKBP - 1) / kKBP);
 
@@ -196,6 +202,15 @@ __device__ __forceinline__ void gemm_body(
         const int64_t r = (grp == 0 ? tl.m0 : tl.n0) + 64 * w4 + lane;
         dma4(grp == 0 ? s_x : s_w, static_cast<uint32_t>((r < src_rows ? r : src_rows - 1) * 4),
              lds_addr(&sscale[slot][grp * kBM + 64 * w4]));
+        if constexpr (ASYM) {
+            // the rows' minima (group 0) and the outputs' weight code sums
+            // (group 1), staged like the scales; older than the step's
+            // loads, so the step's wait covers them too
+            const void* a = grp == 0 ? static_cast<const void*>(zmin_x)
+                                     : static_cast<const void*>(rsum_w);
+            dma4(a, static_cast<uint32_t>((r < src_rows ? r : src_rows - 1) * 4),
+                 lds_addr(&(*sasym)[slot][grp * kBM + 64 * w4]));
+        }
     };
     // A units of a ragged last step past d_in: zeroed by the threads that loaded them
     auto clear_ragged = [&](int kt, int st) {
@@ -289,14 +304,27 @@ __device__ __forceinline__ void gemm_body(
 #pragma unroll
             for (int j = 0; j < 2; ++j)
                 voff[j] = static_cast<uint32_t>(4 * h) * dout + static_cast<uint32_t>(wn * 64 + j * 32 + l32);
+            int rs[2] = {0, 0};
+            const float* za = ASYM ? (*sasym)[slot] : nullptr;
+            if constexpr (ASYM) {
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    rs[j] = __float_as_int(za[kBM + wn * 64 + j * 32 + l32]);
+            }
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                float sx[16];
+                float sx[16], zm[16];
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
                     const f32x4 v = *reinterpret_cast<const f32x4*>(sc + wm * 128 + i * 32 + 8 * q + 4 * h);
 #pragma unroll
                     for (int e = 0; e < 4; ++e) sx[4 * q + e] = v[e];
+                    if constexpr (ASYM) {
+                        const f32x4 z = *reinterpret_cast<const f32x4*>(
+                            za + wm * 128 + i * 32 + 8 * q + 4 * h);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) zm[4 * q + e] = z[e];
+                    }
                 }
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
@@ -304,7 +332,13 @@ __device__ __forceinline__ void gemm_body(
 #pragma unroll
                     for (int j = 0; j < 2; ++j) {
                         const int v = acc[i][j][r] >> kShift;
-                        __builtin_nontemporal_store((static_cast<float>(v) * sx[r]) * sw[j], yr + voff[j]);
+                        if constexpr (ASYM) {
+                            const float t1 = static_cast<float>(v + 8 * rs[j]) * sx[r];
+                            const float t2 = zm[r] * static_cast<float>(rs[j]);
+                            __builtin_nontemporal_store((t1 + t2) * sw[j], yr + voff[j]);
+                        } else {
+                            __builtin_nontemporal_store((static_cast<float>(v) * sx[r]) * sw[j], yr + voff[j]);
+                        }
                     }
                 }
             }
@@ -324,13 +358,22 @@ __device__ __forceinline__ void gemm_body(
             for (int j = 0; j < 2; ++j) {
                 const int col = wn * 64 + j * 32 + l32;
                 if (col >= cols_left) continue;
+                const int rsj = ASYM ? __float_as_int((*sasym)[slot][kBM + col]) : 0;
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int row = rb + 8 * (r >> 2) + (r & 3);
                     if (row >= rows_left) continue;
                     const int64_t off = static_cast<int64_t>(row) * d_out + col;
-                    const int v = acc[i][j][r] >> kShift;
-                    const float yv = (static_cast<float>(v) * sx[r]) * sw[j];
+                    int v = acc[i][j][r] >> kShift;
+                    float yv;
+                    if constexpr (ASYM) {
+                        v += 8 * rsj;
+                        const float t1 = static_cast<float>(v) * sx[r];
+                        const float t2 = (*sasym)[slot][row] * static_cast<float>(rsj);
+                        yv = (t1 + t2) * sw[j];
+                    } else {
+                        yv = (static_cast<float>(v) * sx[r]) * sw[j];
+                    }
                     __builtin_nontemporal_store(yv, yt + off);
                     if (at) at[off] = v;
                 }
@@ -445,7 +488,8 @@ __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
     int64_t d_out, float* __restrict__ y, int32_t* __restrict__ acc_out) {
     __shared__ __attribute__((aligned(16))) GemmRing ring;
     __shared__ __attribute__((aligned(16))) GemmScales sscale;
-    gemm_body<false>(qx, s_x, qw, s_w, n, d_in, d_out, y, acc_out, ring, sscale);
+    gemm_body<false, false>(qx, s_x, qw, s_w, n, d_in, d_out, y, acc_out, ring, sscale, nullptr,
+                            nullptr, nullptr);
 }
 
 __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void int8_gemm_kernel(
@@ -454,12 +498,27 @@ __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void int8_gemm_kernel(
     int64_t d_out, float* __restrict__ y, int32_t* __restrict__ acc_out) {
     __shared__ __attribute__((aligned(16))) GemmRing ring;
     __shared__ __attribute__((aligned(16))) GemmScales sscale;
-    gemm_body<true>(qx, s_x, qw, s_w, n, d_in, d_out, y, acc_out, ring, sscale);
+    gemm_body<true, false>(qx, s_x, qw, s_w, n, d_in, d_out, y, acc_out, ring, sscale, nullptr,
+                           nullptr, nullptr);
+}
+
+__global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_asym_gemm_kernel(
+    const uint8_t* __restrict__ qx, const float* __restrict__ s_x,
+    const uint8_t* __restrict__ qw, const float* __restrict__ s_w, int64_t n, int64_t d_in,
+    int64_t d_out, float* __restrict__ y, int32_t* __restrict__ acc_out,
+    const float* __restrict__ zmin_x, const int32_t* __restrict__ rsum_w) {
+    __shared__ __attribute__((aligned(16))) GemmRing ring;
+    __shared__ __attribute__((aligned(16))) GemmScales sscale;
+    // zmin of a tile's rows and the code sums of its outputs, slots as sscale
+    __shared__ __attribute__((aligned(16))) GemmScales sasym;
+    gemm_body<false, true>(qx, s_x, qw, s_w, n, d_in, d_out, y, acc_out, ring, sscale, zmin_x,
+                           rsum_w, &sasym);
 }
 
 static hipError_t launch_gemm(bool i8, const uint8_t* codes_x, const float* s_x,
                               const uint8_t* codes_w, const float* s_w, int64_t n, int64_t d_in,
-                              int64_t d_out, float* y, int32_t* acc_out, hipStream_t stream) {
+                              int64_t d_out, float* y, int32_t* acc_out, hipStream_t stream,
+                              const float* zmin_x = nullptr, const int32_t* rsum_w = nullptr) {
     int dev = 0, cus = 0;
     hipError_t err = hipGetDevice(&dev);
     if (err != hipSuccess) return err;
@@ -471,9 +530,14 @@ static hipError_t launch_gemm(bool i8, const uint8_t* codes_x, const float* s_x,
     const int64_t t_pad = ((T + kXcd - 1) / kXcd) * kXcd;
     if (grid > t_pad) grid = t_pad;
     if (grid < kXcd) grid = kXcd;
-    hipLaunchKernelGGL(i8 ? int8_gemm_kernel : w4a4_gemm_kernel, dim3(static_cast<uint32_t>(grid)),
-                       dim3(kGemmThreads), 0, stream, codes_x, s_x, codes_w, s_w, n, d_in, d_out, y,
-                       acc_out);
+    if (zmin_x)
+        hipLaunchKernelGGL(w4a4_asym_gemm_kernel, dim3(static_cast<uint32_t>(grid)),
+                           dim3(kGemmThreads), 0, stream, codes_x, s_x, codes_w, s_w, n, d_in,
+                           d_out, y, acc_out, zmin_x, rsum_w);
+    else
+        hipLaunchKernelGGL(i8 ? int8_gemm_kernel : w4a4_gemm_kernel,
+                           dim3(static_cast<uint32_t>(grid)), dim3(kGemmThreads), 0, stream,
+                           codes_x, s_x, codes_w, s_w, n, d_in, d_out, y, acc_out);
     return hipGetLastError();
 }
 
@@ -481,6 +545,14 @@ hipError_t launch_w4a4_linear(const uint8_t* codes_x, const float* s_x, const ui
                               const float* s_w, int64_t n, int64_t d_in, int64_t d_out, float* y,
                               int32_t* acc_out, hipStream_t stream) {
     return launch_gemm(false, codes_x, s_x, codes_w, s_w, n, d_in, d_out, y, acc_out, stream);
+}
+
+hipError_t launch_w4a4_linear_asym(const uint8_t* codes_x, const float* s_x, const float* zmin_x,
+                                   const uint8_t* codes_w, const float* s_w,
+                                   const int32_t* rsum_w, int64_t n, int64_t d_in, int64_t d_out,
+                                   float* y, int32_t* acc_out, hipStream_t stream) {
+    return launch_gemm(false, codes_x, s_x, codes_w, s_w, n, d_in, d_out, y, acc_out, stream,
+                       zmin_x, rsum_w);
 }
 
 hipError_t launch_int8_linear(const int8_t* codes_x, const float* s_x, const int8_t* codes_w,

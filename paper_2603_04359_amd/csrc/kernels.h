@@ -28,10 +28,23 @@ hipError_t launch_transform_quant(const void* X, int x_bf16, int64_t n, int64_t 
                                   uint8_t* codes, float* s_x, uint32_t* amax_ws,
                                   hipStream_t stream);
 
+// Asymmetric INT4 activations: codes q - 8 packed as INT4, s_x and the
+// row minimum zmin_x per token; amax_ws as above (2 n words used).
+hipError_t launch_transform_quant_asym(const void* X, int x_bf16, int64_t n, int64_t d,
+                                       const void* T, int t_bf16, int64_t k, uint8_t* codes,
+                                       float* s_x, float* zmin_x, uint32_t* amax_ws,
+                                       hipStream_t stream);
+
 // ---- integer GEMM: packed INT4 codes (w4a4) or one int8 per code (int8)
 hipError_t launch_w4a4_linear(const uint8_t* codes_x, const float* s_x, const uint8_t* codes_w,
                               const float* s_w, int64_t n, int64_t d_in, int64_t d_out,
                               float* y, int32_t* acc_out, hipStream_t stream);
+// Asymmetric INT4 activations (codes q - 8, scale s_x, minimum zmin_x) by
+// symmetric INT4 weights with row code sums rsum_w.
+hipError_t launch_w4a4_linear_asym(const uint8_t* codes_x, const float* s_x, const float* zmin_x,
+                                   const uint8_t* codes_w, const float* s_w,
+                                   const int32_t* rsum_w, int64_t n, int64_t d_in, int64_t d_out,
+                                   float* y, int32_t* acc_out, hipStream_t stream);
 hipError_t launch_int8_linear(const int8_t* codes_x, const float* s_x, const int8_t* codes_w,
                               const float* s_w, int64_t n, int64_t d_in, int64_t d_out,
                               float* y, int32_t* acc_out, hipStream_t stream);

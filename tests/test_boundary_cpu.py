@@ -127,3 +127,20 @@ def test_binding_rejects_cpu_tensors():
     acc = torch.zeros(64, 64)
     with pytest.raises(ValueError):
         cat.cat_cov_accumulate(x, acc)
+
+
+def test_asymmetric_entry_points_invalid_args():
+    L = cat.lib()
+    ws = L.cat_transform_quant_workspace_bytes(8, 64, 16)
+    f = L.cat_transform_quant_asym
+    assert f(P, 1, 8, 64, P, 1, 16, P, P, None, P, ws, None) == B.CAT_ERR_INVALID_ARG
+    assert f(P, 1, 8, 64, P, 1, 12, P, P, P, P, ws, None) == B.CAT_ERR_INVALID_ARG
+    assert f(P, 1, 8, 64, P, 1, 16, P, P, P + 4, P, ws, None) == B.CAT_ERR_INVALID_ARG
+    assert f(P, 1, 8, 64, P, 1, 16, P, P, P, P, ws - 1, None) == B.CAT_ERR_WORKSPACE
+    g = L.cat_w4a4_linear_asym
+    assert g(P, P, None, P, P, P, 4, 64, 8, P, None, None) == B.CAT_ERR_INVALID_ARG
+    assert g(P, P, P, P, P, None, 4, 64, 8, P, None, None) == B.CAT_ERR_INVALID_ARG
+    assert g(P, P, P, P, P, P + 4, 4, 64, 8, P, None, None) == B.CAT_ERR_INVALID_ARG
+    assert g(P, P, P, P, P, P, 4, 48, 8, P, None, None) == B.CAT_ERR_INVALID_ARG
+    assert L.cat_weight_code_sums(None, 4, 8, P) == B.CAT_ERR_INVALID_ARG
+    assert L.cat_weight_code_sums(P, 4, 7, P) == B.CAT_ERR_INVALID_ARG

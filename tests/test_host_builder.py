@@ -113,3 +113,12 @@ def test_quantize_weights_matches_oracle_bit_exact(bits):
     assert np.array_equal(codes, o.pack_int4(q_or) if bits == 4 else q_or)
     assert np.array_equal(s_w, s_or)
     assert s_w[3] == 0 and not codes[3].any()
+
+
+def test_weight_code_sums_match_unpacked_codes():
+    qw = wl.random_codes(37, 96, seed=41)
+    qw[0] = -8 + 1                                 # all -7
+    qw[1] = 7
+    rs = cat.cat_weight_code_sums(o.pack_int4(qw))
+    assert rs.dtype == np.int32
+    assert np.array_equal(rs, qw.astype(np.int64).sum(axis=1))

@@ -331,6 +331,21 @@ def main():
             "linear_tokens_per_s": n / ((tq_ms + g_ms) * 1e-3)}
         log(f"[bench] W{bits}A{bits}: transform_quant {tq_ms:.4f} ms, int8_linear {g_ms:.4f} ms "
             f"({g_tops:.0f} TOP/s), SQNR {wide[f'W{bits}A{bits}']['sqnr_db']:.2f} dB")
+    # ---------------- the Theorem 2.4 decomposition of the W4A4 layer from
+    # device results (per-token scales, the batch's block second-moment
+    # sums, sum y^2), after the timed steps
+    cat.cat_transform_quant(Xs[0], T_dev, k, codes, s_x, ws_q)
+    cat.cat_w4a4_linear(codes, s_x, codes_w, s_w, y_t)
+    cat.cat_sqnr(Ys[0], y_t, ws_s, out)
+    acc_e = torch.zeros((d_in // k, k, k), dtype=torch.float32, device=dev)
+    cat.cat_cov_accumulate(Xs[0], acc_e, B.CAT_COV_BLOCK_DIAG, k)
+    torch.cuda.synchronize()
+    res = out.cpu().numpy()
+    terms = cat.cat_sqnr_terms(s_x.cpu().numpy(), 4, acc_e.double().cpu().numpy(), T_host, tdt,
+                               Wp, 4, float(res[0]))
+    terms["measured_db"] = float(res[2])
+    rec["theorem_2_4"] = terms
+    log(f"[bench] Theorem 2.4: predicted {terms['sqnr_pred_db']:.2f} dB, measured {res[2]:.2f} dB")
     del Wp
     rec["wide_codes"] = wide
 

@@ -279,6 +279,27 @@ int cat_build_transform(const double* sigma_x_blocks, const float* W,
 int cat_quantize_weights(const double* W_prime, int64_t d_out, int64_t d_in,
                          int bits, uint8_t* codes_w_out, float* s_w_out);
 
+/* The Theorem 2.4 decomposition of a quantized layer (Sec. 2: Lemmas 2.2,
+ * 2.3, Theorem 2.4) from what the device calls produce, host side:
+ *   C(x')  = E||x'||^2 / E[r(x')^2], x' = T x, r = 2 max|x'_i| = 2 qmax s_x
+ *   C(W')  = sum_o ||w'_o||^2 / sum_o r(w'_o)^2
+ *   A      = E||W' x'||^2 / (||W'||_F^2 E||x'||^2), E||W'x'||^2 = sum_y2 / n
+ *   SQNR  ~= 12 (N(b_x)^2 C(x') || N(b_w)^2 C(W')) A,  N(b) = 2 qmax
+ * with E||x'||^2 = (1/n) sum_b tr(T_b S_b T_b^T).
+ * s_x              host fp32 [n]: cat_transform_quant's scales at bits_x.
+ * sigma_sum_blocks host fp64 [d_in/k x k x k]: block sums X_b^T X_b over the
+ *                  same n tokens (cat_cov_accumulate, BLOCK_DIAG, not
+ *                  divided by n).
+ * T                host [d_in/k x k x k] in t_dtype (bf16 as uint16 bits).
+ * W_prime          host fp64 [d_out x d_in].
+ * sum_y2           sum of y^2 over the batch (cat_sqnr's out[0]).
+ * out              host fp64 [5]: C(x'), C(W'), A, predicted SQNR, in dB.
+ * bits_x, bits_w in [2, 8]. */
+int cat_sqnr_terms(const float* s_x, int64_t n, int bits_x,
+                   const double* sigma_sum_blocks, int64_t d_in, int64_t k,
+                   const void* T, int t_dtype, const double* W_prime,
+                   int64_t d_out, int bits_w, double sum_y2, double* out);
+
 /* Thread-local message describing the last non-OK return on this thread. */
 const char* cat_last_error(void);
 

@@ -43,7 +43,7 @@ EXPORTED = (
     "cat_cov_workspace_bytes", "cat_cov_accumulate", "cat_transform_quant_workspace_bytes",
     "cat_transform_quant",
     "cat_w4a4_linear", "cat_int8_linear", "cat_transform_quant_asym", "cat_w4a4_linear_asym",
-    "cat_weight_code_sums", "cat_sqnr_workspace_bytes", "cat_sqnr", "cat_build_transform",
+    "cat_weight_code_sums", "cat_sqnr_terms", "cat_sqnr_workspace_bytes", "cat_sqnr", "cat_build_transform",
     "cat_quantize_weights", "cat_last_error", "cat_version",
 )
 
@@ -93,6 +93,9 @@ def lib() -> ctypes.CDLL:
     L.cat_w4a4_linear_asym.restype = _int
     L.cat_weight_code_sums.argtypes = [_vp, _i64, _i64, _vp]
     L.cat_weight_code_sums.restype = _int
+    L.cat_sqnr_terms.argtypes = [_vp, _i64, _int, _vp, _i64, _i64, _vp, _int, _vp, _i64, _int,
+                                 ctypes.c_double, _vp]
+    L.cat_sqnr_terms.restype = _int
     L.cat_sqnr_workspace_bytes.argtypes = [_i64]
     L.cat_sqnr_workspace_bytes.restype = _sz
     L.cat_sqnr.argtypes = [_vp, _vp, _i64, _vp, _sz, _vp, _vp]
@@ -299,6 +302,22 @@ def cat_weight_code_sums(codes_w):
     out = np.empty(d_out, dtype=np.int32)
     _check("cat_weight_code_sums", lib().cat_weight_code_sums(pc, d_out, 2 * half, out.ctypes.data))
     return out
+
+
+def cat_sqnr_terms(s_x, bits_x: int, sigma_sum_blocks, T, t_dtype: int, W_prime, bits_w: int,
+                   sum_y2: float):
+    """Host Theorem 2.4 terms: returns dict C_x, C_w, A, sqnr_pred, sqnr_pred_db."""
+    sx, psx = _host(s_x, np.float32, "s_x")
+    S, pS = _host(sigma_sum_blocks, np.float64, "sigma_sum_blocks")
+    Tn, pT = _host(T, np.uint16 if t_dtype == CAT_BF16 else np.float32, "T")
+    Wp, pW = _host(W_prime, np.float64, "W_prime")
+    nb, k, _ = S.shape
+    d_out, d_in = Wp.shape
+    out = np.empty(5, dtype=np.float64)
+    _check("cat_sqnr_terms", lib().cat_sqnr_terms(psx, sx.shape[0], bits_x, pS, d_in, k, pT,
+                                                  t_dtype, pW, d_out, bits_w, float(sum_y2),
+                                                  out.ctypes.data))
+    return dict(zip(("C_x", "C_w", "A", "sqnr_pred", "sqnr_pred_db"), out.tolist()))
 
 
 def cat_sqnr_workspace_bytes(count: int) -> int:

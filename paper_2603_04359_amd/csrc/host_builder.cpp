@@ -409,3 +409,69 @@ extern "C" int cat_weight_code_sums(const uint8_t* codes_w, int64_t d_out, int64
     }
     return CAT_OK;
 }
+
+extern "C" int cat_sqnr_terms(const float* s_x, int64_t n, int bits_x, const double* sigma_sum_blocks,
+                              int64_t d_in, int64_t k, const void* T, int t_dtype,
+                              const double* W_prime, int64_t d_out, int bits_w, double sum_y2,
+                              double* out) {
+    using cat::fail;
+    if (!s_x || !sigma_sum_blocks || !T || !W_prime || !out)
+        return fail(CAT_ERR_INVALID_ARG, "cat_sqnr_terms: NULL pointer");
+    if (n < 1 || d_out < 1 || d_in < 1 || !cat::is_pow2(k) || k > CAT_MAX_BLOCK || d_in % k)
+        return fail(CAT_ERR_INVALID_ARG, "cat_sqnr_terms: bad sizes");
+    if (t_dtype != CAT_F32 && t_dtype != CAT_BF16)
+        return fail(CAT_ERR_INVALID_ARG, "cat_sqnr_terms: bad t_dtype");
+    if (bits_x < 2 || bits_x > 8 || bits_w < 2 || bits_w > 8)
+        return fail(CAT_ERR_INVALID_ARG, "cat_sqnr_terms: bits must lie in [2, 8]");
+    const double qx = static_cast<double>((1 << (bits_x - 1)) - 1);
+    const double qw = static_cast<double>((1 << (bits_w - 1)) - 1);
+    // E||x'||^2 = (1/n) sum_b tr(T_b S_b T_b^T), S_b the block's second-moment sum
+    double tr_sum = 0.0;
+    std::vector<double> tb(static_cast<size_t>(k * k));
+    for (int64_t b = 0; b < d_in / k; ++b) {
+        for (int64_t e = 0; e < k * k; ++e)
+            tb[e] = t_dtype == CAT_BF16
+                        ? bf16_bits_to_double(static_cast<const uint16_t*>(T)[b * k * k + e])
+                        : static_cast<double>(static_cast<const float*>(T)[b * k * k + e]);
+        const double* S = sigma_sum_blocks + b * k * k;
+        for (int64_t j = 0; j < k; ++j)           // row j of T_b: t_j^T S t_j
+            for (int64_t a = 0; a < k; ++a) {
+                const double ta = tb[j * k + a];
+                if (ta == 0.0) continue;
+                double acc = 0.0;
+                for (int64_t c = 0; c < k; ++c) acc += S[a * k + c] * tb[j * k + c];
+                tr_sum += ta * acc;
+            }
+    }
+    const double ex2 = tr_sum / static_cast<double>(n);
+    // E[r(x')^2] with r = 2 amax = 2 qmax s_x (the per-token scale)
+    double er2 = 0.0;
+    for (int64_t t = 0; t < n; ++t) {
+        const double r = 2.0 * qx * static_cast<double>(s_x[t]);
+        er2 += r * r;
+    }
+    er2 /= static_cast<double>(n);
+    // C(W') and ||W'||_F^2 over output rows
+    double wf2 = 0.0, wr2 = 0.0;
+    for (int64_t o = 0; o < d_out; ++o) {
+        double amax = 0.0;
+        for (int64_t j = 0; j < d_in; ++j) {
+            const double v = W_prime[o * d_in + j];
+            wf2 += v * v;
+            amax = std::max(amax, std::fabs(v));
+        }
+        wr2 += 4.0 * amax * amax;
+    }
+    const double cx = ex2 / er2;
+    const double cw = wf2 / wr2;
+    const double a = (sum_y2 / static_cast<double>(n)) / (wf2 * ex2);   // E||W'x'||^2 = E||Wx||^2
+    const double nx = 2.0 * qx, nw = 2.0 * qw;
+    const double px = nx * nx * cx, pw = nw * nw * cw;
+    const double pred = 12.0 * (1.0 / (1.0 / px + 1.0 / pw)) * a;
+    out[0] = cx;
+    out[1] = cw;
+    out[2] = a;
+    out[3] = pred;
+    out[4] = 10.0 * std::log10(pred);
+    return CAT_OK;
+}

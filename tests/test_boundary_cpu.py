@@ -144,3 +144,12 @@ def test_asymmetric_entry_points_invalid_args():
     assert g(P, P, P, P, P, P, 4, 48, 8, P, None, None) == B.CAT_ERR_INVALID_ARG
     assert L.cat_weight_code_sums(None, 4, 8, P) == B.CAT_ERR_INVALID_ARG
     assert L.cat_weight_code_sums(P, 4, 7, P) == B.CAT_ERR_INVALID_ARG
+
+
+def test_sqnr_terms_invalid_args():
+    L = cat.lib()
+    f = L.cat_sqnr_terms
+    assert f(None, 4, 4, P, 64, 16, P, 1, P, 8, 4, 1.0, P) == B.CAT_ERR_INVALID_ARG
+    assert f(P, 4, 4, P, 64, 12, P, 1, P, 8, 4, 1.0, P) == B.CAT_ERR_INVALID_ARG
+    assert f(P, 4, 9, P, 64, 16, P, 1, P, 8, 4, 1.0, P) == B.CAT_ERR_INVALID_ARG
+    assert f(P, 4, 4, P, 64, 16, P, 7, P, 8, 4, 1.0, P) == B.CAT_ERR_INVALID_ARG

@@ -122,3 +122,30 @@ def test_weight_code_sums_match_unpacked_codes():
     rs = cat.cat_weight_code_sums(o.pack_int4(qw))
     assert rs.dtype == np.int32
     assert np.array_equal(rs, qw.astype(np.int64).sum(axis=1))
+
+
+@pytest.mark.parametrize("t_dtype", ["f32", "bf16"])
+def test_sqnr_terms_match_oracle_decomposition(t_dtype):
+    # Theorem 2.4's terms from a batch's block second-moment sums, the
+    # per-token scales and sum y^2, against the oracle's concentration,
+    # alignment and prediction computed from the transformed rows directly
+    cfg = wl.get_config("tiny")
+    lay = wl.make_layer(cfg, seed=3)
+    X, W, k = lay["X"].astype(np.float64), lay["W"].astype(np.float64), cfg.k
+    T = o.round_storage(o.cat_transform(o.second_moment(lay["X_cal"]), W, k), t_dtype)
+    Wp = o.transform_weights(W, T)
+    Z = o.transform_rows(X, T)
+    _, s_x = o.transform_quant(X, T, 4)
+    S = np.stack([X[:, b * k:(b + 1) * k].T @ X[:, b * k:(b + 1) * k] for b in range(cfg.d_in // k)])
+    Y = X @ W.T
+    if t_dtype == "bf16":
+        Tc = (T.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+        tcode = cat.CAT_BF16
+    else:
+        Tc, tcode = T.astype(np.float32), cat.CAT_F32
+    r = cat.cat_sqnr_terms(s_x, 4, S, Tc, tcode, Wp, 4, float(np.sum(Y * Y)))
+    assert r["C_x"] == pytest.approx(o.concentration_act(Z), rel=1e-6)
+    assert r["C_w"] == pytest.approx(o.concentration_weight(Wp), rel=1e-12)
+    assert r["A"] == pytest.approx(o.alignment(Z, Wp), rel=1e-9)
+    assert r["sqnr_pred"] == pytest.approx(o.theorem_2_4(Z, Wp, 4, 4), rel=1e-6)
+    assert r["sqnr_pred_db"] == pytest.approx(10 * np.log10(r["sqnr_pred"]))

@@ -166,3 +166,49 @@ def test_end_to_end_asym_vs_sym_sqnr():
     assert abs(asym_db - or_asym) <= 0.05
     assert abs(sym_db - or_sym) <= 0.05
     assert asym_db > sym_db
+
+
+def test_asym_pair_graph_replays_match_eager():
+    # the asymmetric pair (key clear, two transform+quant passes, GEMM)
+    # captured once and replayed with new activations, against eager calls
+    torch = torch_mod()
+    n, d, d_out, k = 300, 1024, 384, 128
+    say("asymmetric pair under graph capture: 3 replays vs eager")
+    rng = np.random.default_rng(71)
+    T = o.round_storage(rng.standard_normal((d // k, k, k)) / np.sqrt(k), "bf16")
+    dT = dev(T, "bf16")
+    qw = wl.random_codes(d_out, d, seed=72)
+    pw = o.pack_int4(qw)
+    dqw, drs = dev(pw, "u8"), dev(cat.cat_weight_code_sums(pw), "i32")
+    dsw = dev(rng.uniform(0.01, 1.0, d_out).astype(np.float32), "f32")
+    Xs = [o.round_storage((rng.standard_normal((n, d)) + 1.0).astype(np.float32), "bf16")
+          for _ in range(3)]
+
+    def buffers():
+        return dict(codes=torch.empty((n, d // 2), dtype=torch.uint8, device="cuda"),
+                    s_x=torch.empty(n, dtype=torch.float32, device="cuda"),
+                    zmin=torch.empty(n, dtype=torch.float32, device="cuda"),
+                    yt=torch.empty((n, d_out), dtype=torch.float32, device="cuda"),
+                    ws=torch.empty(cat.cat_transform_quant_workspace_bytes(n, d, k),
+                                   dtype=torch.uint8, device="cuda"))
+
+    def pair(dX, b):
+        cat.cat_transform_quant_asym(dX, dT, k, b["codes"], b["s_x"], b["zmin"], b["ws"])
+        cat.cat_w4a4_linear_asym(b["codes"], b["s_x"], b["zmin"], dqw, dsw, drs, b["yt"])
+
+    dX = dev(Xs[0], "bf16")
+    g_b, e_b = buffers(), buffers()
+    pair(dX, g_b)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=torch.cuda.Stream()):
+        pair(dX, g_b)
+    for i, X in enumerate(Xs):
+        dX.copy_(dev(X, "bf16"))
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        pair(dX, e_b)
+        torch.cuda.synchronize()
+        for key in ("codes", "s_x", "zmin", "yt"):
+            assert torch.equal(g_b[key], e_b[key]), f"replay {i}: {key}"

@@ -48,6 +48,12 @@ Function -> passage -> what pins it (tests/test_oracle_*.py):
   linear_asym        Sec. 3, eq. 5 with asymmetric activations
                                                 -> brute-force loops,
                      dequantize-then-multiply product
+  hadamard_order, paley2_hadamard, full_hadamard_mix, transform_quant_full
+                     Sec. 4 (T = H M, H full-dimension), Sec. 5 (rotations)
+                                                -> H H^T = m I and +-1
+                     entries (orders 1 .. 112, incl. 28 = Paley II q = 13),
+                     Sylvester = scipy.linalg.hadamard, mix of H_k blocks =
+                     kron(H_m, H_k) / sqrt(d), function preservation
   pack_int4          storage layout (no passage) -> hand-computed bytes
   w4a4_linear        Sec. 3, eq. 5 (Q(W T^-1) Q(T x))
                                                 -> brute-force loops,
@@ -183,6 +189,64 @@ def hadamard(k: int) -> np.ndarray:
     while H.shape[0] < k:
         H = np.block([[H, H], [H, -H]])
     return H / np.sqrt(k)
+
+
+def paley2_hadamard(q: int) -> np.ndarray:
+    """Unnormalised Hadamard matrix of order 2 (q + 1) by Paley's second
+    construction, q a prime with q = 1 (mod 4): the symmetric conference
+    matrix C = [[0, 1^T], [1, Q]] (Q_ij = Legendre symbol of i - j mod q)
+    gives H = C (x) [[1, 1], [1, -1]] + I (x) [[1, -1], [-1, -1]]."""
+    if q % 4 != 1 or any(q % p == 0 for p in range(2, int(q ** 0.5) + 1)):
+        raise ValueError("q must be a prime = 1 mod 4")
+    squares = {(x * x) % q for x in range(1, q)}
+    chi = np.array([0] + [1 if a in squares else -1 for a in range(1, q)])
+    Q = np.array([[chi[(i - j) % q] for j in range(q)] for i in range(q)])
+    C = np.zeros((q + 1, q + 1), dtype=np.int64)
+    C[0, 1:] = 1
+    C[1:, 0] = 1
+    C[1:, 1:] = Q
+    return np.kron(C, np.array([[1, 1], [1, -1]])) + \
+        np.kron(np.eye(q + 1, dtype=np.int64), np.array([[1, -1], [-1, -1]]))
+
+
+def hadamard_order(m: int) -> np.ndarray:
+    """Unnormalised Hadamard matrix of order m for the full-dimension
+    transform: Sylvester when m is a power of two, else H_28 (Paley II,
+    q = 13) (x) Sylvester_(m/28) (the widths 28 2^a, e.g. 14336 / 128 =
+    112).  The row index is b = b1 m / 28 + b2 for the Kronecker factor."""
+    if m >= 1 and not (m & (m - 1)):
+        return np.rint(hadamard(m) * np.sqrt(m)).astype(np.int64)
+    if m % 28 == 0 and not ((m // 28) & (m // 28 - 1)):
+        return np.kron(paley2_hadamard(13), hadamard_order(m // 28))
+    raise ValueError(f"no Hadamard order {m} here")
+
+
+def full_hadamard_mix(Z, k: int) -> np.ndarray:
+    """Cross-block part of T = H_d M_block with H_d = H_m (x) H_k
+    (Sec. 4, T = H M with a full-dimension H; Sec. 5, QuaRot-style
+    rotations): z'_(b, j) = sum_b' H_m[b, b'] z_(b', j) / sqrt(m), fp64."""
+    Z = np.asarray(Z, dtype=np.float64)
+    n, d = Z.shape
+    m = d // k
+    H = hadamard_order(m).astype(np.float64) / np.sqrt(m)
+    return np.einsum("ab,nbj->naj", H, Z.reshape(n, m, k)).reshape(n, d)
+
+
+def transform_quant_full(X, T_blocks, bits: int = 4):
+    """Q(H_d M x): the block transform T_b = H_k M_b, the cross-block
+    Hadamard, one rounding to fp32, then the per-token quantizer."""
+    k = T_blocks.shape[1]
+    Z32 = full_hadamard_mix(transform_rows(X, T_blocks), k).astype(np.float32)
+    return quantize_rows(Z32, bits)
+
+
+def transform_weights_full(W, T_blocks) -> np.ndarray:
+    """W'' = W T_full^-1 = (W blockdiag(T_b)^-1) (H_m (x) I_k)^T / sqrt(m),
+    so that W'' T_full x = W x."""
+    Wp = transform_weights(W, T_blocks)
+    k = T_blocks.shape[1]
+    # row times (H_m (x) I_k)^T / sqrt(m) is the same mix applied to the row
+    return full_hadamard_mix(Wp, k)
 
 
 def cat_transform(sigma_x, W, k: int, use_hadamard: bool = True,

@@ -547,3 +547,39 @@ def test_linear_asym_brute_force_loops_and_fake_quant():
     X = qx * sx[:, None].astype(np.float64) + mx[:, None]
     Wq = qw * sw[:, None].astype(np.float64)
     np.testing.assert_allclose(y, X @ Wq.T, rtol=1e-6, atol=1e-6)
+
+
+# ------------------------------------------- full-dimension Hadamard
+@pytest.mark.parametrize("m", [1, 2, 8, 32, 28, 56, 112])
+def test_hadamard_orders_are_hadamard(m):
+    H = o.hadamard_order(m)
+    assert set(np.unique(H)) <= {-1, 1}
+    assert np.array_equal(H @ H.T, m * np.eye(m, dtype=np.int64))
+    if not (m & (m - 1)):
+        assert np.array_equal(H, sla.hadamard(m))
+
+
+def test_full_mix_of_hadamard_blocks_is_the_kronecker_hadamard():
+    # with M = I every block is H_k / sqrt(k); block transform then mix is
+    # x -> kron(H_m, H_k) x / sqrt(d)
+    rng = np.random.default_rng(51)
+    for m, k in ((4, 8), (28, 4)):
+        d = m * k
+        X = rng.standard_normal((6, d))
+        Tb = np.stack([o.hadamard(k)] * m)
+        Z = o.full_hadamard_mix(o.transform_rows(X, Tb), k)
+        K = np.kron(o.hadamard_order(m), o.hadamard_order(k)) / np.sqrt(d)
+        np.testing.assert_allclose(Z, X @ K.T, atol=1e-12)
+        np.testing.assert_allclose(K @ K.T, np.eye(d), atol=1e-12)
+
+
+def test_full_transform_preserves_function():
+    rng = np.random.default_rng(52)
+    d, k = 28 * 8, 8
+    X = rng.standard_normal((10, d))
+    W = rng.standard_normal((12, d))
+    S = X.T @ X / 10 + np.eye(d)
+    T = o.cat_transform(S, W, k)
+    Wpp = o.transform_weights_full(W, T)
+    Z = o.full_hadamard_mix(o.transform_rows(X, T), k)
+    np.testing.assert_allclose(Z @ Wpp.T, X @ W.T, atol=1e-9 * np.abs(X @ W.T).max())

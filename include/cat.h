@@ -279,6 +279,32 @@ int cat_build_transform(const double* sigma_x_blocks, const float* W,
 int cat_quantize_weights(const double* W_prime, int64_t d_out, int64_t d_in,
                          int bits, uint8_t* codes_w_out, float* s_w_out);
 
+/* ------------------------------------------------------------------
+ * Full-dimension Hadamard (Sec. 4: T = H M with H over all d channels;
+ * Sec. 5: QuaRot-style rotations).  H_d = H_m (x) H_k with m = d / k, so
+ *   T = (H_m (x) I_k) / sqrt(m) . blockdiag(T_b),  T_b = H_k M_b / sqrt(k)
+ * (the blocks cat_build_transform returns with CAT_BUILD_HADAMARD).  H_m is
+ * Sylvester for m a power of two, else H_28 (x) Sylvester_(m/28), H_28 from
+ * Paley's second construction with q = 13, rows split r = r1 (m/28) + r2.
+ *
+ * cat_transform_quant_full: z = blockdiag(T_b) x in fp32, z' =
+ *   (H_m (x) I_k) z / sqrt(m) in fp32, then the per-token INT4 quantizer of
+ *   cat_transform_quant on z'.  bf16 X and T, k = 128 or 256, m in {2, 4,
+ *   8, 16, 32, 64, 28, 56, 112} (else CAT_ERR_UNSUPPORTED).  workspace:
+ *   cat_transform_quant_full_workspace_bytes(n, d, k) bytes (z, fp32).
+ *   Other arguments and errors as cat_transform_quant.
+ * cat_full_hadamard_weights: host; W_full = W' (H_m (x) I_k)^T / sqrt(m)
+ *   for W' = W blockdiag(T_b)^-1 (cat_build_transform's W_prime), so that
+ *   W_full z' = W x.  fp64 [d_out x d_in] in and out (may not alias).
+ */
+size_t cat_transform_quant_full_workspace_bytes(int64_t n, int64_t d, int64_t k);
+int cat_transform_quant_full(const void* X, int x_dtype, int64_t n, int64_t d,
+                             const void* T, int t_dtype, int64_t k,
+                             uint8_t* codes, float* s_x, void* workspace,
+                             size_t workspace_bytes, void* stream);
+int cat_full_hadamard_weights(const double* W_prime, int64_t d_out,
+                              int64_t d_in, int64_t k, double* W_full_out);
+
 /* The Theorem 2.4 decomposition of a quantized layer (Sec. 2: Lemmas 2.2,
  * 2.3, Theorem 2.4) from what the device calls produce, host side:
  *   C(x')  = E||x'||^2 / E[r(x')^2], x' = T x, r = 2 max|x'_i| = 2 qmax s_x

@@ -43,7 +43,8 @@ EXPORTED = (
     "cat_cov_workspace_bytes", "cat_cov_accumulate", "cat_transform_quant_workspace_bytes",
     "cat_transform_quant",
     "cat_w4a4_linear", "cat_int8_linear", "cat_transform_quant_asym", "cat_w4a4_linear_asym",
-    "cat_weight_code_sums", "cat_sqnr_terms", "cat_sqnr_workspace_bytes", "cat_sqnr", "cat_build_transform",
+    "cat_weight_code_sums", "cat_sqnr_terms", "cat_transform_quant_full_workspace_bytes",
+    "cat_transform_quant_full", "cat_full_hadamard_weights", "cat_sqnr_workspace_bytes", "cat_sqnr", "cat_build_transform",
     "cat_quantize_weights", "cat_last_error", "cat_version",
 )
 
@@ -96,6 +97,13 @@ def lib() -> ctypes.CDLL:
     L.cat_sqnr_terms.argtypes = [_vp, _i64, _int, _vp, _i64, _i64, _vp, _int, _vp, _i64, _int,
                                  ctypes.c_double, _vp]
     L.cat_sqnr_terms.restype = _int
+    L.cat_transform_quant_full_workspace_bytes.argtypes = [_i64, _i64, _i64]
+    L.cat_transform_quant_full_workspace_bytes.restype = _sz
+    L.cat_transform_quant_full.argtypes = [_vp, _int, _i64, _i64, _vp, _int, _i64, _vp, _vp, _vp,
+                                           _sz, _vp]
+    L.cat_transform_quant_full.restype = _int
+    L.cat_full_hadamard_weights.argtypes = [_vp, _i64, _i64, _i64, _vp]
+    L.cat_full_hadamard_weights.restype = _int
     L.cat_sqnr_workspace_bytes.argtypes = [_i64]
     L.cat_sqnr_workspace_bytes.restype = _sz
     L.cat_sqnr.argtypes = [_vp, _vp, _i64, _vp, _sz, _vp, _vp]
@@ -318,6 +326,38 @@ def cat_sqnr_terms(s_x, bits_x: int, sigma_sum_blocks, T, t_dtype: int, W_prime,
                                                   t_dtype, pW, d_out, bits_w, float(sum_y2),
                                                   out.ctypes.data))
     return dict(zip(("C_x", "C_w", "A", "sqnr_pred", "sqnr_pred_db"), out.tolist()))
+
+
+def cat_transform_quant_full_workspace_bytes(n: int, d: int, k: int) -> int:
+    return int(lib().cat_transform_quant_full_workspace_bytes(n, d, k))
+
+
+def cat_transform_quant_full(X, T, k: int, codes, s_x, workspace, stream=None):
+    """Full-dimension Hadamard transform + INT4: codes uint8 [n, d/2] and
+    s_x [n] fp32 from X [n, d] bf16 and the blocks T [d/k, k, k] bf16."""
+    torch = _torch()
+    px = _dev_ptr(X, "X", (torch.bfloat16,))
+    pt = _dev_ptr(T, "T", (torch.bfloat16,))
+    pc = _dev_ptr(codes, "codes", (torch.uint8,))
+    ps = _dev_ptr(s_x, "s_x", (torch.float32,))
+    pw = _dev_ptr(workspace, "workspace")
+    n, d = X.shape
+    if tuple(codes.shape) != (n, d // 2):
+        raise ValueError(f"codes must be [{n}, {d // 2}]")
+    wbytes = workspace.numel() * workspace.element_size()
+    _check("cat_transform_quant_full",
+           lib().cat_transform_quant_full(px, CAT_BF16, n, d, pt, CAT_BF16, k, pc, ps, pw, wbytes,
+                                          _stream_ptr(stream)))
+
+
+def cat_full_hadamard_weights(W_prime, k: int):
+    """Host: W_full = W' (H_m (x) I_k)^T / sqrt(m), fp64."""
+    Wp, pw = _host(W_prime, np.float64, "W_prime")
+    d_out, d_in = Wp.shape
+    out = np.empty_like(Wp)
+    _check("cat_full_hadamard_weights",
+           lib().cat_full_hadamard_weights(pw, d_out, d_in, k, out.ctypes.data))
+    return out
 
 
 def cat_sqnr_workspace_bytes(count: int) -> int:

@@ -157,6 +157,44 @@ extern "C" int cat_transform_quant_asym(const void* X, int x_dtype, int64_t n, i
     }
 }
 
+extern "C" size_t cat_transform_quant_full_workspace_bytes(int64_t n, int64_t d, int64_t k) {
+    if (n < 1 || d < 1 || k < 1) return 0;
+    return catk::tq_full_workspace_bytes(n, d);
+}
+
+extern "C" int cat_transform_quant_full(const void* X, int x_dtype, int64_t n, int64_t d,
+                                        const void* T, int t_dtype, int64_t k, uint8_t* codes,
+                                        float* s_x, void* workspace, size_t workspace_bytes,
+                                        void* stream) {
+    const char* fn = "cat_transform_quant_full";
+    try {
+        if (!X || !T || !codes || !s_x)
+            return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": NULL pointer");
+        if (!valid_dtype(x_dtype) || !valid_dtype(t_dtype))
+            return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": bad dtype");
+        if (n < 1 || d < 2 || !cat::is_pow2(k) || k > CAT_MAX_BLOCK || d % k)
+            return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": bad sizes");
+        if (!catk::tq_full_supported(x_dtype == CAT_BF16, t_dtype == CAT_BF16, d, k))
+            return fail(CAT_ERR_UNSUPPORTED, std::string(fn) +
+                        ": needs bf16 X and T, k 128 or 256, d/k in {2..64 powers of two, 28, 56, 112}");
+        if (!cat::aligned16(X) || !cat::aligned16(T) || !cat::aligned16(codes) || !cat::aligned16(s_x))
+            return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": pointers must be 16-byte aligned");
+        if (!workspace || workspace_bytes < catk::tq_full_workspace_bytes(n, d))
+            return fail(CAT_ERR_WORKSPACE, std::string(fn) + ": workspace missing or too small");
+        if (!cat::aligned16(workspace))
+            return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": workspace must be 16-byte aligned");
+        if (int rc = require_device(fn)) return rc;
+        const hipError_t err = catk::launch_transform_quant_full(
+            X, n, d, T, k, codes, s_x, static_cast<float*>(workspace), static_cast<hipStream_t>(stream));
+        if (err != hipSuccess) return hip_fail(fn, err);
+        return CAT_OK;
+    } catch (const std::exception& e) {
+        return fail(CAT_ERR_INTERNAL, std::string(fn) + ": " + e.what());
+    } catch (...) {
+        return fail(CAT_ERR_INTERNAL, std::string(fn) + ": unknown error");
+    }
+}
+
 namespace {
 
 // Shared checks and launch of the two integer GEMM entry points.

@@ -475,3 +475,57 @@ extern "C" int cat_sqnr_terms(const float* s_x, int64_t n, int bits_x, const dou
     out[4] = 10.0 * std::log10(pred);
     return CAT_OK;
 }
+
+namespace {
+// Entry (r, c) of the unnormalised Hadamard matrix H_m of the
+// full-dimension transform: Sylvester for m a power of two, else
+// H_28 (x) Sylvester_(m/28) with H_28 from Paley's second construction
+// (q = 13), rows split as r = r1 (m/28) + r2.
+int legendre13_h(int a) {
+    a = ((a % 13) + 13) % 13;
+    return a == 0 ? 0 : (a == 1 || a == 3 || a == 4 || a == 9 || a == 10 || a == 12) ? 1 : -1;
+}
+int paley28_h(int r, int c) {
+    const int i = r / 2, j = c / 2, ri = r % 2, cj = c % 2;
+    const int conf = (i == 0 && j == 0) ? 0 : (i == 0 || j == 0) ? 1 : legendre13_h(i - j);
+    const int a = (ri == 1 && cj == 1) ? -1 : 1;
+    const int b = (ri == 0 && cj == 0) ? 1 : -1;
+    return conf * a + (i == j ? b : 0);
+}
+int hadamard_entry(int64_t m, int64_t r, int64_t c) {
+    if ((m & (m - 1)) == 0) return (__builtin_popcountll(r & c) & 1) ? -1 : 1;
+    const int64_t m2 = m / 28;
+    const int syl = (__builtin_popcountll((r % m2) & (c % m2)) & 1) ? -1 : 1;
+    return paley28_h(static_cast<int>(r / m2), static_cast<int>(c / m2)) * syl;
+}
+}  // namespace
+
+extern "C" int cat_full_hadamard_weights(const double* W_prime, int64_t d_out, int64_t d_in,
+                                         int64_t k, double* W_full_out) {
+    using cat::fail;
+    if (!W_prime || !W_full_out) return fail(CAT_ERR_INVALID_ARG, "cat_full_hadamard_weights: NULL pointer");
+    if (d_out < 1 || k < 1 || d_in < k || d_in % k)
+        return fail(CAT_ERR_INVALID_ARG, "cat_full_hadamard_weights: bad sizes");
+    const int64_t m = d_in / k;
+    const bool pow2 = (m & (m - 1)) == 0;
+    const bool p28 = m % 28 == 0 && ((m / 28) & (m / 28 - 1)) == 0;
+    if (!pow2 && !p28) return fail(CAT_ERR_UNSUPPORTED, "cat_full_hadamard_weights: d_in/k has no Hadamard order here");
+    std::vector<double> H(static_cast<size_t>(m * m));
+    const double norm = 1.0 / std::sqrt(static_cast<double>(m));
+    for (int64_t r = 0; r < m; ++r)
+        for (int64_t c = 0; c < m; ++c) H[r * m + c] = hadamard_entry(m, r, c) * norm;
+    std::vector<double> v(static_cast<size_t>(m));
+    for (int64_t o = 0; o < d_out; ++o) {
+        const double* src = W_prime + o * d_in;
+        double* dst = W_full_out + o * d_in;
+        for (int64_t j = 0; j < k; ++j) {
+            for (int64_t b = 0; b < m; ++b) v[b] = src[b * k + j];
+            for (int64_t a = 0; a < m; ++a) {
+                double acc = 0.0;
+                for (int64_t b = 0; b < m; ++b) acc += H[a * m + b] * v[b];
+                dst[a * k + j] = acc;
+            }
+        }
+    }
+    return CAT_OK;
+}

@@ -28,6 +28,7 @@
 // packed 4 per lane, joined to 8 per dword with one lane swap.
 // fp32 (or small-k) path: plain fp32 FMA chains on the vector ALU.
 #include <atomic>
+#include <type_traits>
 
 #include "device_common.h"
 #include "kernels.h"
@@ -509,6 +510,19 @@ __global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
                     const uint32_t word = h ? (recv | (v[qp + 1] << 16)) : (v[qp] | (recv << 16));
                     if (valid) crow[qp + h] = word;
                 }
+            }
+        } else if constexpr (QUANT && QM == 0) {
+            // z itself, fp32 (the full-dimension Hadamard path mixes it
+            // across blocks afterwards): codes is an [n x d] fp32 buffer
+#pragma unroll
+            for (int sb = 0; sb < C::NSB; ++sb) {
+                const int64_t t = tile * C::TT + sb * 32 + l32;
+                if (t >= n) continue;
+                float* zrow = reinterpret_cast<float*>(codes) + t * d + b * K + row0;
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    *reinterpret_cast<f32x4*>(zrow + 8 * q + 4 * h) =
+                        f32x4{acc[sb][4 * q], acc[sb][4 * q + 1], acc[sb][4 * q + 2], acc[sb][4 * q + 3]};
             }
         } else if constexpr (!QUANT) {
 #pragma unroll
@@ -1197,6 +1211,150 @@ hipError_t launch_transform_quant_asym(const void* X, int x_bf16, int64_t n, int
                                       stream);
     return launch_tq_generic_asym(static_cast<const float*>(X), n, d,
                                   static_cast<const float*>(T), k, codes, s_x, zmin_x, ws, stream);
+}
+
+// ------------------------------------------ full-dimension Hadamard
+// T = H_d blockdiag(M_b) with H_d = H_m (x) H_k (m = d / k blocks): the
+// block transform T_b = H_k M_b as above, then z' = (H_m (x) I_k) z /
+// sqrt(m) across blocks (Sec. 4, T = H M with a full-dimension H), then the
+// per-token INT4 quantizer.  H_m is Sylvester for m a power of two, else
+// H_28 (x) Sylvester_(m/28), with H_28 from Paley's second construction
+// (q = 13): the conference matrix C = [[0, 1^T], [1, Q]], Q_ij = Legendre
+// symbol of (i - j) mod 13, and H = C (x) [[1, 1], [1, -1]] + I (x)
+// [[1, -1], [-1, -1]].  Row b of H_m splits as b = b1 (m / 28) + b2.
+constexpr int legendre13(int a) {
+    a = ((a % 13) + 13) % 13;
+    return a == 0 ? 0 : (a == 1 || a == 3 || a == 4 || a == 9 || a == 10 || a == 12) ? 1 : -1;
+}
+constexpr int paley28(int r, int c) {
+    const int i = r / 2, j = c / 2, ri = r % 2, cj = c % 2;
+    const int conf = (i == 0 && j == 0) ? 0 : (i == 0 || j == 0) ? 1 : legendre13((i - 1) - (j - 1));
+    const int a = (ri == 1 && cj == 1) ? -1 : 1;                 // [[1, 1], [1, -1]]
+    const int bb = (ri == 0 && cj == 0) ? 1 : -1;                // [[1, -1], [-1, -1]]
+    return conf * a + (i == j ? bb : 0);
+}
+
+// One workgroup per token, k threads; thread j holds channel j of every
+// block (M values), mixes them, and the workgroup reduces the row maximum.
+template <int M>
+__global__ __launch_bounds__(256) void tq_mix_quant_kernel(const float* __restrict__ z, int64_t n,
+                                                          int64_t d, int64_t k,
+                                                          uint8_t* __restrict__ codes,
+                                                          float* __restrict__ s_x) {
+    constexpr bool P28 = (M % 28) == 0;
+    constexpr int M2 = P28 ? M / 28 : M;      // Sylvester factor
+    __shared__ uint32_t red[4];
+    const int64_t t = blockIdx.x;
+    const int j = threadIdx.x;
+    float v[M];
+#pragma unroll
+    for (int b = 0; b < M; ++b) v[b] = z[t * d + b * k + j];
+    // Sylvester factor over b2 inside each b1 group
+#pragma unroll
+    for (int hstep = 1; hstep < M2; hstep <<= 1)
+#pragma unroll
+        for (int b = 0; b < M; ++b)
+            if (((b % M2) & hstep) == 0) {
+                const float x = v[b], y = v[b + hstep];
+                v[b] = x + y;
+                v[b + hstep] = x - y;
+            }
+    if constexpr (P28) {
+        // H_28 over b1 for every b2
+#pragma unroll
+        for (int b2 = 0; b2 < M2; ++b2) {
+            float o[28];
+#pragma unroll
+            for (int a1 = 0; a1 < 28; ++a1) {
+                float acc = 0.0f;
+#pragma unroll
+                for (int b1 = 0; b1 < 28; ++b1) {
+                    const int sgn = paley28(a1, b1);
+                    acc = sgn > 0 ? acc + v[b1 * M2 + b2] : acc - v[b1 * M2 + b2];
+                }
+                o[a1] = acc;
+            }
+#pragma unroll
+            for (int a1 = 0; a1 < 28; ++a1) v[a1 * M2 + b2] = o[a1];
+        }
+    }
+    const float norm = 1.0f / __builtin_sqrtf(static_cast<float>(M));
+    uint32_t m = 0;
+#pragma unroll
+    for (int b = 0; b < M; ++b) {
+        v[b] *= norm;
+        m = max(m, abs_bits(v[b]));
+    }
+#pragma unroll
+    for (int x = 1; x < kWave; x <<= 1)
+        m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), x)));
+    if ((j & (kWave - 1)) == 0) red[j / kWave] = m;
+    __syncthreads();
+    const int nw = static_cast<int>(k / kWave);
+    m = red[0];
+    for (int w = 1; w < nw; ++w) m = max(m, red[w]);
+    const float amax = __uint_as_float(m);
+    if (j == 0) s_x[t] = __fdiv_rn(amax, kQmax4);
+    const float inv = amax > 0.0f ? __fdiv_rn(kQmax4, amax) : 0.0f;
+#pragma unroll
+    for (int b = 0; b < M; ++b) {
+        const int c = amax > 0.0f ? quant_code<7>(v[b], inv) : 0;
+        const int other = __shfl_xor(c, 1);
+        if ((j & 1) == 0)
+            codes[t * (d / 2) + (b * k + j) / 2] = static_cast<uint8_t>((c & 0xF) | ((other & 0xF) << 4));
+    }
+}
+
+static bool tq_full_supported_m(int64_t m) {
+    switch (m) {
+        case 2: case 4: case 8: case 16: case 32: case 64: case 28: case 56: case 112: return true;
+        default: return false;
+    }
+}
+
+bool tq_full_supported(int x_bf16, int t_bf16, int64_t d, int64_t k) {
+    return x_bf16 && t_bf16 && (k == 128 || k == 256) && d % k == 0 && tq_full_supported_m(d / k);
+}
+
+size_t tq_full_workspace_bytes(int64_t n, int64_t d) {
+    return static_cast<size_t>(n) * static_cast<size_t>(d) * sizeof(float);
+}
+
+hipError_t launch_transform_quant_full(const void* X, int64_t n, int64_t d, const void* T,
+                                       int64_t k, uint8_t* codes, float* s_x, float* zbuf,
+                                       hipStream_t stream) {
+    const uint16_t* Xb = static_cast<const uint16_t*>(X);
+    const uint16_t* Tb = static_cast<const uint16_t*>(T);
+    uint8_t* zb = reinterpret_cast<uint8_t*>(zbuf);
+    int dev = 0, cus = 0;
+    hipError_t err = hipGetDevice(&dev);
+    if (err != hipSuccess) return err;
+    err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (err != hipSuccess) return err;
+    auto zpass = [&](auto kc) -> hipError_t {
+        constexpr int K = decltype(kc)::value;
+        using C = TqRing<K>;
+        const int64_t ntiles = (n + C::TT - 1) / C::TT;
+        const int64_t nbj = (d / K) * C::NCHUNK;
+        int64_t R = (2 * static_cast<int64_t>(cus) + nbj - 1) / nbj;
+        if (R > ntiles) R = ntiles;
+        if (R < 1) R = 1;
+        hipLaunchKernelGGL((tq_ring_kernel<K, true, 0, false>), dim3(static_cast<uint32_t>(nbj * R)),
+                           dim3(kTqThreads), 0, stream, Xb, Tb, n, d, R, nullptr, zb, nullptr,
+                           nullptr);
+        return hipGetLastError();
+    };
+    err = k == 128 ? zpass(std::integral_constant<int, 128>{})
+                   : zpass(std::integral_constant<int, 256>{});
+    if (err != hipSuccess) return err;
+    const dim3 grid(static_cast<uint32_t>(n)), block(static_cast<uint32_t>(k));
+    switch (d / k) {
+#define CAT_MIX(MM) case MM: hipLaunchKernelGGL(tq_mix_quant_kernel<MM>, grid, block, 0, stream, zbuf, n, d, k, codes, s_x); break;
+        CAT_MIX(2) CAT_MIX(4) CAT_MIX(8) CAT_MIX(16) CAT_MIX(32) CAT_MIX(64) CAT_MIX(28) CAT_MIX(56) CAT_MIX(112)
+#undef CAT_MIX
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
 }
 
 }  // namespace catk

@@ -35,6 +35,15 @@ hipError_t launch_transform_quant_asym(const void* X, int x_bf16, int64_t n, int
                                        float* s_x, float* zmin_x, uint32_t* amax_ws,
                                        hipStream_t stream);
 
+// Full-dimension Hadamard: block transform to fp32 z in zbuf
+// (tq_full_workspace_bytes), then the cross-block Hadamard and the
+// per-token INT4 quantizer.  Only where tq_full_supported().
+bool tq_full_supported(int x_bf16, int t_bf16, int64_t d, int64_t k);
+size_t tq_full_workspace_bytes(int64_t n, int64_t d);
+hipError_t launch_transform_quant_full(const void* X, int64_t n, int64_t d, const void* T,
+                                       int64_t k, uint8_t* codes, float* s_x, float* zbuf,
+                                       hipStream_t stream);
+
 // ---- integer GEMM: packed INT4 codes (w4a4) or one int8 per code (int8)
 hipError_t launch_w4a4_linear(const uint8_t* codes_x, const float* s_x, const uint8_t* codes_w,
                               const float* s_w, int64_t n, int64_t d_in, int64_t d_out,

@@ -153,3 +153,18 @@ def test_sqnr_terms_invalid_args():
     assert f(P, 4, 4, P, 64, 12, P, 1, P, 8, 4, 1.0, P) == B.CAT_ERR_INVALID_ARG
     assert f(P, 4, 9, P, 64, 16, P, 1, P, 8, 4, 1.0, P) == B.CAT_ERR_INVALID_ARG
     assert f(P, 4, 4, P, 64, 16, P, 7, P, 8, 4, 1.0, P) == B.CAT_ERR_INVALID_ARG
+
+
+def test_full_hadamard_invalid_args():
+    L = cat.lib()
+    ws = L.cat_transform_quant_full_workspace_bytes(8, 1024, 128)
+    assert ws == 8 * 1024 * 4
+    f = L.cat_transform_quant_full
+    assert f(None, 1, 8, 1024, P, 1, 128, P, P, P, ws, None) == B.CAT_ERR_INVALID_ARG
+    assert f(P, 0, 8, 1024, P, 1, 128, P, P, P, ws, None) == B.CAT_ERR_UNSUPPORTED      # fp32 X
+    assert f(P, 1, 8, 1024, P, 1, 64, P, P, P, ws, None) == B.CAT_ERR_UNSUPPORTED       # k = 64
+    assert f(P, 1, 8, 384, P, 1, 128, P, P, P, ws, None) == B.CAT_ERR_UNSUPPORTED       # m = 3
+    assert f(P, 1, 8, 1024, P, 1, 128, P, P, P, ws - 1, None) == B.CAT_ERR_WORKSPACE
+    g = L.cat_full_hadamard_weights
+    assert g(None, 4, 64, 8, P) == B.CAT_ERR_INVALID_ARG
+    assert g(P, 4, 24, 8, P) == B.CAT_ERR_UNSUPPORTED                                   # m = 3

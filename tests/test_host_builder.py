@@ -149,3 +149,13 @@ def test_sqnr_terms_match_oracle_decomposition(t_dtype):
     assert r["A"] == pytest.approx(o.alignment(Z, Wp), rel=1e-9)
     assert r["sqnr_pred"] == pytest.approx(o.theorem_2_4(Z, Wp, 4, 4), rel=1e-6)
     assert r["sqnr_pred_db"] == pytest.approx(10 * np.log10(r["sqnr_pred"]))
+
+
+@pytest.mark.parametrize("m,k", [(8, 16), (28, 8), (56, 4), (112, 2)])
+def test_full_hadamard_weights_match_oracle(m, k):
+    rng = np.random.default_rng(m + k)
+    Wp = rng.standard_normal((9, m * k))
+    Tb = np.stack([np.eye(k)] * m)
+    ref = o.transform_weights_full(Wp, Tb)          # W' itself when T_b = I
+    got = cat.cat_full_hadamard_weights(Wp, k)
+    np.testing.assert_allclose(got, ref, atol=1e-12 * np.abs(ref).max())

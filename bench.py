@@ -346,8 +346,38 @@ def main():
     terms["measured_db"] = float(res[2])
     rec["theorem_2_4"] = terms
     log(f"[bench] Theorem 2.4: predicted {terms['sqnr_pred_db']:.2f} dB, measured {res[2]:.2f} dB")
+
+    # ---------------- full-dimension Hadamard T = H_d blockdiag(M_b), INT4,
+    # after the timed steps
+    if cat.cat_transform_quant_full_workspace_bytes(n, d_in, k) and tdt == B.CAT_BF16 and \
+            k in (128, 256):
+        cw_h, sw_h = cat.cat_quantize_weights(cat.cat_full_hadamard_weights(Wp, k), 4)
+        cw, sw = torch.from_numpy(cw_h).to(dev), torch.from_numpy(sw_h).to(dev)
+        ws_f = torch.empty(cat.cat_transform_quant_full_workspace_bytes(n, d_in, k),
+                           dtype=torch.uint8, device=dev)
+        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)]
+              for _ in range(args.wide_steps)]
+        for i in range(2 + args.wide_steps):
+            e = ev[i - 2] if i >= 2 else None
+            if e: e[0].record()
+            cat.cat_transform_quant_full(Xs[i % 2], T_dev, k, codes, s_x, ws_f)
+            if e: e[1].record()
+            cat.cat_w4a4_linear(codes, s_x, cw, sw, y_t)
+            if e: e[2].record()
+        cat.cat_sqnr(Ys[(1 + args.wide_steps) % 2], y_t, ws_s, out)
+        torch.cuda.synchronize()
+        tq_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+        g_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+        rec_full = {"sqnr_db": float(out[2].item()), "transform_quant_full_ms": tq_ms,
+                    "w4a4_linear_ms": g_ms, "linear_tokens_per_s": n / ((tq_ms + g_ms) * 1e-3)}
+        log(f"[bench] full-dimension Hadamard: transform_quant {tq_ms:.4f} ms, SQNR "
+            f"{rec_full['sqnr_db']:.2f} dB")
+        del ws_f
+    else:
+        rec_full = None
     del Wp
     rec["wide_codes"] = wide
+    rec["full_hadamard"] = rec_full
 
     # ---------------- asymmetric per-token activations (the paper's own
     # activation set-up), INT4, after the timed steps

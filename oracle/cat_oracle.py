@@ -74,6 +74,13 @@ the design notes):
     fl((2^b - 1) / r))), 0, 2^b - 1); dequantized as s q + min (no integer
     zero point: the minimum is kept in fp32).  A constant row gets s = 0.
     The product's fp32 order: fl(fl(fl(acc) s_x) + fl(min fl(R))) s_w.
+  * Full-dimension Hadamard (the variant of T = H M with H over all d
+    channels): H_d = H_m (x) H_k with m = d / k; H_m Sylvester for m a
+    power of two, else H_28 (Paley II, q = 13) (x) Sylvester_(m/28).  So
+    T = (H_m (x) I_k) / sqrt(m) blockdiag(H_k M_b / sqrt(k)), and the
+    weights take the same cross-block mix.
+  * Quantization widths 6 and 8 bits store one int8 per code; their tie
+    bar is the INT4 one scaled by qmax / 7.
   * Symmetric integer grid: codes in [-qmax, qmax], qmax = 2^(b-1)-1, so
     the grid has N(b) = 2^b - 2 intervals (the paper's N(b) is "the number
     of quantization intervals"; its 2^b - 1 counts a 2^b-level grid).

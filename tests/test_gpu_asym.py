@@ -212,3 +212,31 @@ def test_asym_pair_graph_replays_match_eager():
         torch.cuda.synchronize()
         for key in ("codes", "s_x", "zmin", "yt"):
             assert torch.equal(g_b[key], e_b[key]), f"replay {i}: {key}"
+
+
+def test_asym_mlp_up_full_size():
+    # 8192 x 4096 activations (transform+quant over every token) and the
+    # 4096 -> 14336 product checked on a 64 x 64 sample of rows and columns
+    torch = torch_mod()
+    n, d, d_out, k = 8192, 4096, 14336, 128
+    say(f"asym full size {n} x {d} -> {d_out}")
+    cfg = wl.get_config("mlp_up", n=n, n_cal=16)
+    X = wl.make_layer(cfg, seed=3, with_cal=False, with_weights=False)["X"].astype(np.float64)
+    rng = np.random.default_rng(81)
+    T = o.round_storage(rng.standard_normal((d // k, k, k)) / np.sqrt(k), "bf16")
+    q, s, m = _tq_asym(X, T, k, "bf16", "bf16")
+    _check_asym(q, s, m, X, T, "mlp_up asym")
+    qw = wl.random_codes(d_out, d, seed=82)
+    sw = rng.uniform(0.01, 1.0, d_out).astype(np.float32)
+    pw = o.pack_int4(qw)
+    y = torch.empty((n, d_out), dtype=torch.float32, device="cuda")
+    acc = torch.empty((n, d_out), dtype=torch.int32, device="cuda")
+    cat.cat_w4a4_linear_asym(dev(o.pack_int4(q - 8), "u8"), dev(s, "f32"), dev(m, "f32"),
+                             dev(pw, "u8"), dev(sw, "f32"), dev(cat.cat_weight_code_sums(pw), "i32"),
+                             y, acc)
+    rows = np.unique(np.concatenate([rng.choice(n, 62, replace=False), [0, n - 1]]))
+    cols = np.unique(np.concatenate([rng.choice(d_out, 62, replace=False), [0, d_out - 1]]))
+    acc_or, y_or = o.linear_asym(q[rows], s[rows], m[rows], qw[cols], sw[cols])
+    ri, ci = torch.from_numpy(rows).cuda(), torch.from_numpy(cols).cuda()
+    assert np.array_equal(host(acc[ri][:, ci]), acc_or)
+    assert np.array_equal(host(y[ri][:, ci]), y_or)

@@ -47,7 +47,7 @@ def _check_full(q, s, X, T, k, label):
 
 @pytest.mark.parametrize("d,k,n", [(1024, 128, 257), (4096, 128, 130), (3584, 128, 70),
                                    (7168, 256, 33), (14336, 128, 17), (14336, 256, 40),
-                                   (256, 128, 5)])
+                                   (256, 128, 5), (4096, 128, 8192)])
 def test_transform_quant_full_matches_oracle(d, k, n):
     say(f"tq full Hadamard d={d} k={k} (m={d // k}) n={n}")
     rng = np.random.default_rng(d + k + n)

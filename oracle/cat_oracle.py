@@ -15,6 +15,14 @@ Paper: "Dissecting Quantization Error: A Concentration-Alignment
 Perspective" (Federici, van Breugel, Whatmough, Nagel).
 
 Function -> passage -> what pins it (tests/test_oracle_*.py):
+  round_bf16         storage precision of T and X (no passage)
+                                                -> hand-worked values with
+                     exact ties both ways, brute-force nearest-neighbour
+                     search, torch's float32 -> bfloat16 cast
+  spd_power floor    (reading below; the paper is silent)
+                                                -> closed forms on singular
+                     and rotated-singular matrices, dead-channel closed
+                     form of M through the floor
   second_moment      Sec. 4 (autocorrelation E[x x^T] used by eq. 7),
                      Sec. 6 "Calibration"       -> numpy.cov identity,
                      batch-split invariance, basis-vector case, PSD
@@ -60,6 +68,10 @@ Function -> passage -> what pins it (tests/test_oracle_*.py):
                      fake-quant product, K-permutation invariance
   sqnr               Sec. 2, eq. 1               -> hand-computed values,
                      uniform-noise closed form on Gaussian data
+  alignment_from_moments
+                     Sec. 2 Lemma 2.2 (A written with second moments)
+                                                -> equals the sample
+                     alignment, isotropic 1/d and rank-one cos^2 closed forms
   concentration_*, alignment, theorem_2_4, parallel
                      Sec. 2 Lemmas 2.1-2.3, Theorem 2.4; Sec. 2.1
                                                 -> paper's printed minimum

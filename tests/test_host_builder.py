@@ -159,3 +159,42 @@ def test_full_hadamard_weights_match_oracle(m, k):
     ref = o.transform_weights_full(Wp, Tb)          # W' itself when T_b = I
     got = cat.cat_full_hadamard_weights(Wp, k)
     np.testing.assert_allclose(got, ref, atol=1e-12 * np.abs(ref).max())
+
+
+def test_build_transform_rounds_exact_bf16_ties_to_even():
+    # k = 1 makes each block the scalar m_i = (sum_j W_ji^2 / E[x_i^2])^(1/4)
+    # (eq. 7).  With E[x_i^2] = 1 and one weight row W_0i = m_i^2, every
+    # intermediate is exact, so T_i = m_i; the m_i below sit exactly on
+    # bf16 rounding boundaries (spacing 2^-7 on [1, 2)) and on either side.
+    m = np.array([1 + 2.0 ** -8,              # tie: down to 1.0 (even)
+                  1 + 3 * 2.0 ** -8,          # tie: up to 1 + 2^-6 (even)
+                  1 + 2.0 ** -7,              # exact
+                  1.5,                        # exact
+                  1 + 5 * 2.0 ** -8,          # tie: down to 1 + 2^-6 (even)
+                  1 + 7 * 2.0 ** -8])         # tie: up to 1 + 2^-5
+    # neighbours of 1 + (2j+1) 2^-8 are 1 + j 2^-7 and 1 + (j+1) 2^-7;
+    # the even one has the even multiple of 2^-7
+    expected = []
+    for v in m:
+        j = np.floor((v - 1.0) / 2.0 ** -7)
+        lo, hi = 1.0 + j * 2.0 ** -7, 1.0 + (j + 1) * 2.0 ** -7
+        if v - lo < hi - v:
+            expected.append(lo)
+        elif v - lo > hi - v:
+            expected.append(hi)
+        else:
+            expected.append(lo if j % 2 == 0 else hi)
+    expected = np.array(expected)
+    np.testing.assert_array_equal(expected, [1.0, 1 + 2.0 ** -6, 1 + 2.0 ** -7, 1.5,
+                                             1 + 2.0 ** -6, 1 + 2.0 ** -5])
+    d = m.size
+    W = (m ** 2).astype(np.float32)[None, :]
+    assert np.array_equal(W[0].astype(np.float64), m ** 2)
+    sx = np.ones((d, 1, 1))
+    T, Te, _ = cat.cat_build_transform(sx, W, 1, B.CAT_BUILD_ALIGN, B.CAT_BF16, want_exact=True)
+    np.testing.assert_array_equal(Te.reshape(-1), m)
+    np.testing.assert_array_equal(wl.bf16_bits_to_f32(T).reshape(-1).astype(np.float64), expected)
+    # the oracle's T and its storage rounding land on the same values
+    T_or = o.cat_transform(np.eye(d), W, 1, use_hadamard=False)
+    np.testing.assert_array_equal(T_or.reshape(-1), m)
+    np.testing.assert_array_equal(o.round_storage(T_or, "bf16").reshape(-1), expected)

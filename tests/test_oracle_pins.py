@@ -583,3 +583,132 @@ def test_full_transform_preserves_function():
     Wpp = o.transform_weights_full(W, T)
     Z = o.full_hadamard_mix(o.transform_rows(X, T), k)
     np.testing.assert_allclose(Z @ Wpp.T, X @ W.T, atol=1e-9 * np.abs(X @ W.T).max())
+
+
+# ------------------------------------------------- bf16 storage rounding
+# bf16 keeps 8 significant bits, so the spacing just above 1.0 is 2^-7 and
+# 1 + 2^-8 sits exactly halfway between two neighbours.
+@pytest.mark.parametrize("x,expected", [
+    (1.0, 1.0),                                   # exact
+    (1 + 2.0 ** -8, 1.0),                         # tie, 1.0 has the even last bit
+    (1 + 3 * 2.0 ** -8, 1 + 2.0 ** -6),           # tie, rounds up to the even neighbour
+    (1 + 2.0 ** -8 + 2.0 ** -20, 1 + 2.0 ** -7),  # just above the tie
+    (1 + 2.0 ** -8 - 2.0 ** -20, 1.0),            # just below the tie
+    (-(1 + 3 * 2.0 ** -8), -(1 + 2.0 ** -6)),     # sign is symmetric
+    (-(1 + 2.0 ** -8), -1.0),
+    (2 - 2.0 ** -8, 2.0),                         # tie across a binade: up to 2.0 (even)
+    (2 - 3 * 2.0 ** -8, 2 - 2.0 ** -6),           # tie inside [1, 2): down to the even neighbour
+    (3 * 2.0 ** 100 + 2.0 ** 93, 3 * 2.0 ** 100),  # tie at a large exponent (even below)
+    (2.0 ** -149, 0.0),                           # smallest fp32 subnormal flushes to +0
+    (2.0 ** -134, 0.0),                           # subnormal tie, 0 is even
+    (1.5 * 2.0 ** -133, 2.0 ** -132),             # subnormal tie, rounds up to the even one
+    (2.0 ** -133, 2.0 ** -133),                   # exact subnormal
+])
+def test_round_bf16_hand_values_and_ties(x, expected):
+    # every input is exact in fp32; the expected values are worked out by
+    # hand from the 8-bit significand and ties-to-even
+    assert np.float64(np.float32(x)) == x
+    got = o.round_bf16(np.array([x]))[0]
+    assert got == expected and np.signbit(got) == np.signbit(expected)
+
+
+def test_round_bf16_is_nearest_with_even_ties_brute_force():
+    # Independent of the bit manipulation: for each fp32 value take its two
+    # bf16 neighbours (truncation and the next representable value above in
+    # magnitude), choose the nearer by exact fp64 distance, and on a tie the
+    # one whose significand is even.  Half of the inputs are exact ties.
+    rng = np.random.default_rng(81)
+    bits = rng.integers(0x00800000, 0x7F000000, size=20000, dtype=np.uint32)
+    bits[::2] = (bits[::2] & 0xFFFF0000) | 0x8000           # ties
+    bits[1::4] |= 0x80000000                                # negatives
+    x32 = bits.view(np.float32)
+    got = o.round_bf16(x32)
+    mag = np.abs(x32.astype(np.float64))
+    lo_bits = (np.abs(x32).view(np.uint32) & 0xFFFF0000)
+    lo = lo_bits.view(np.float32).astype(np.float64)
+    hi = (lo_bits + 0x10000).view(np.float32).astype(np.float64)
+    d_lo, d_hi = mag - lo, hi - mag
+    lo_even = ((lo_bits >> 16) & 1) == 0
+    pick_lo = (d_lo < d_hi) | ((d_lo == d_hi) & lo_even)
+    ref = np.where(pick_lo, lo, hi) * np.sign(x32.astype(np.float64))
+    assert np.array_equal(got, ref)
+    assert (d_lo == d_hi).sum() >= 10000
+
+
+def test_round_bf16_matches_torch_conversion():
+    # torch's float32 -> bfloat16 cast rounds to nearest, ties to even
+    import torch
+    rng = np.random.default_rng(82)
+    x = (rng.standard_normal(50000) * np.exp(rng.uniform(-30, 30, 50000))).astype(np.float32)
+    x[:2000] = (x[:2000].view(np.uint32) & 0xFFFF0000 | 0x8000).view(np.float32)
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(o.round_bf16(x), ref)
+
+
+# ------------------------------------------------------ eigenvalue floor
+def test_eigenvalue_floor_closed_forms():
+    # Eigenvalues below 1e-12 lambda_max are raised to that value before a
+    # power is taken, so the powers stay finite on singular blocks.
+    np.testing.assert_allclose(o.spd_power(np.diag([1.0, 1e-20]), -0.5),
+                               np.diag([1.0, 1e6]), rtol=1e-12, atol=0)
+    np.testing.assert_allclose(o.spd_power(np.diag([1.0, 0.0]), 0.5),
+                               np.diag([1.0, 1e-6]), rtol=1e-12, atol=0)
+    # a rotated singular matrix: Q diag(4, 1e-30) Q^T to the power -1/2 is
+    # Q diag(1/2, (4e-12)^-1/2) Q^T
+    c, s = np.cos(0.3), np.sin(0.3)
+    Q = np.array([[c, -s], [s, c]])
+    S = Q @ np.diag([4.0, 1e-30]) @ Q.T
+    ref = Q @ np.diag([0.5, (4e-12) ** -0.5]) @ Q.T
+    np.testing.assert_allclose(o.spd_power(S, -0.5), ref, rtol=1e-9, atol=1e-9 * 5e5)
+    # eigenvalues above the floor are left alone
+    np.testing.assert_allclose(o.spd_power(np.diag([1.0, 1e-11]), -0.5),
+                               np.diag([1.0, 1e-11 ** -0.5]), rtol=1e-12)
+    with pytest.raises(ValueError):
+        o.spd_power(np.zeros((2, 2)), 0.5)
+
+
+def test_eigenvalue_floor_keeps_the_transform_finite_on_a_dead_channel():
+    # A channel that is zero on every calibration token makes its Sigma_x
+    # block singular.  With the floor, the block's M has the floored
+    # eigenvalue's closed form on that channel: for a diagonal block,
+    # m_i = (sum_j W_ji^2 / max(E[x_i^2], 1e-12 lambda_max))^(1/4).
+    k = 4
+    Sx = np.diag([2.0, 0.5, 0.0, 1.0])
+    w = np.array([[1.0, 2.0, 3.0, 0.5]])
+    # rank-one Sigma_w: the block transform stays finite
+    T = o.cat_transform(Sx, w.astype(np.float32), k, use_hadamard=False)[0]
+    assert np.all(np.isfinite(T))
+    # diagonal Sigma_w commutes with Sigma_x, so M is diagonal with the
+    # closed form above; lambda_max = 2 sets the floor 2e-12 on channel 2
+    cw = (w.astype(np.float32).astype(np.float64) ** 2)[0]
+    ex = np.maximum(np.diag(Sx), 1e-12 * 2.0)
+    Tdiag = o.optimal_alignment(Sx, np.diag(cw))
+    np.testing.assert_allclose(np.diag(Tdiag), (cw / ex) ** 0.25, rtol=1e-9)
+    np.testing.assert_allclose(Tdiag - np.diag(np.diag(Tdiag)), 0.0, atol=1e-12)
+
+
+# ---------------------------------------------- alignment from moments
+def test_alignment_from_moments_equals_sample_alignment():
+    # Tr(W^T W X^T X) = ||X W^T||_F^2, so the moment form with Sigma_x =
+    # X^T X / n and Sigma_w = W^T W equals the sample form of Lemma 2.2
+    rng = np.random.default_rng(83)
+    X, W = _act(rng, 400, 24), rng.standard_normal((10, 24))
+    a_mom = o.alignment_from_moments(o.second_moment(X), W.T @ W)
+    assert a_mom == pytest.approx(o.alignment(X, W), rel=1e-12)
+
+
+def test_alignment_from_moments_closed_forms():
+    rng = np.random.default_rng(84)
+    d = 16
+    Sw = _rand_spd(rng, d)
+    # isotropic inputs: A = Tr(Sigma_w) / (Tr(Sigma_w) d) = 1 / d
+    assert o.alignment_from_moments(np.eye(d), Sw) == pytest.approx(1.0 / d, rel=1e-14)
+    # one input direction v and one weight row w: A = cos^2(v, w)
+    v, w = rng.standard_normal(d), rng.standard_normal(d)
+    cos2 = np.dot(v, w) ** 2 / (np.dot(v, v) * np.dot(w, w))
+    assert o.alignment_from_moments(np.outer(v, v), np.outer(w, w)) == pytest.approx(cos2,
+                                                                                      rel=1e-12)
+    # orthogonal directions give zero alignment
+    u = np.zeros(d); u[0] = 1.0
+    t = np.zeros(d); t[1] = 1.0
+    assert o.alignment_from_moments(np.outer(u, u), np.outer(t, t)) == 0.0

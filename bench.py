@@ -14,8 +14,15 @@ between steps so the 256 MiB last-level cache never holds a step's
 activations when its transform_quant starts (the sqnr pass of the previous
 step streams ~900 MiB in between).
 
-Printed: one JSON line (rank 0) with the throughput, per-kernel times,
-the roofline of the dominant kernel and the CPU oracle baseline.
+The chain (calibration on the GPU, host transform construction, the four
+device calls, the fp64 reference output y) is paper_2603_04359_amd.pipeline,
+the same code the full-size layer tests check against the oracle.
+
+Printed: one JSON line with the throughput, per-kernel times (mean, median,
+min), the roofline of the dominant kernel, the CPU oracle baseline, and,
+after the timed steps, the widened paths and a report over the other layer
+configurations (tiny: SQNR per transform; attention and MLP-down: kernel
+times and SQNR; stress: block-size sweep and 4/6/8-bit widths).
 """
 from __future__ import annotations
 
@@ -24,9 +31,15 @@ import hashlib
 import json
 import os
 import sys
+import threading
 import time
 
-import numpy as np
+# explicit thread counts for the CPU oracle's BLAS (the host's share of cores)
+_CORES = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+for _v in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS"):
+    os.environ.setdefault(_v, str(_CORES))
+
+import numpy as np  # noqa: E402
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
@@ -47,10 +60,12 @@ def parse():
     p.add_argument("--config", default="mlp_up")
     p.add_argument("--seed", type=int, default=0)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-report", action="store_true",
+                   help="skip the widened paths and the other configurations after the steps")
     p.add_argument("--wide-steps", type=int, default=10,
-                   help="timed iterations of each 6- and 8-bit comparison pair")
+                   help="timed iterations of each pair measured after the steps")
     p.add_argument("--cpu-seconds", type=float, default=10.0,
-                   help="minimum CPU time of the oracle sample")
+                   help="minimum oracle time of each CPU baseline sample")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                    help="only run a plain device-to-device copy of MIB MiB (5 launches): "
                         "the known-size kernel that scales HBM byte counters")
@@ -90,40 +105,79 @@ def measured_traffic(kernel: str):
     return None if ent is None else ent.get("hbm_bytes_per_launch")
 
 
+def stats(ms):
+    ms = np.asarray(ms, dtype=np.float64)
+    return {"mean": float(ms.mean()), "median": float(np.median(ms)), "min": float(ms.min()),
+            "max": float(ms.max())}
+
+
+# ------------------------------------------------------------ CPU baseline
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
 def cpu_baseline(lay, T_vals, codes_w, s_w, n_tokens, min_seconds):
     """The CPU oracle (test infrastructure, never the product path) timed on
     this host on a bounded sample of the same workload: 512-token chunks
-    of the step's batch run through the oracle's Sigma_x, transform+quant,
-    integer GEMM and SQNR, cycling over the batch, until at least
-    `min_seconds` of oracle time have passed (and at most 4 passes)."""
+    of the step's batch through the oracle's Sigma_x, transform+quant,
+    integer GEMM and SQNR (each timed), cycling over the batch, until at
+    least `min_seconds` of oracle time have passed (at most 4 passes).
+    Run twice: with every core of this process's affinity set, then with
+    the BLAS pools limited to one thread."""
     from oracle import cat_oracle as o
-    try:
-        import threadpoolctl
-        threads = max(i["num_threads"] for i in threadpoolctl.threadpool_info()) \
-            if threadpoolctl.threadpool_info() else 1
-    except Exception:  # pragma: no cover
-        threads = os.cpu_count()
+    import threadpoolctl
+
     X = lay["X"]
-    W32 = lay["W"]
+    W64 = lay["W"].astype(np.float64)
     T = np.asarray(T_vals, dtype=np.float64)
     qw = o.unpack_int4(codes_w)
-    chunk, done, t_total = 512, 0, 0.0
-    while done < 4 * n_tokens and (t_total < min_seconds or done == 0):
-        a = done % n_tokens
-        xs = X[a:a + chunk].astype(np.float64)
-        y = xs.astype(np.float32) @ W32.T   # signal: input of the SQNR step, not timed
-        t0 = time.perf_counter()
-        o.second_moment_sum(xs)
-        qx, sx = o.transform_quant(xs, T)
-        _, yt = o.w4a4_linear(qx, sx, qw, s_w)
-        o.sqnr(y, yt)
-        t_total += time.perf_counter() - t0
-        done += xs.shape[0]
-    return {"value": done / t_total, "unit": "tokens/s", "cores": int(threads),
-            "kind": "oracle",
+
+    def sample(limit):
+        chunk, done, info = 512, 0, []
+        part = {"second_moment": 0.0, "transform_quant": 0.0, "w4a4_linear": 0.0, "sqnr": 0.0}
+        while done < 4 * n_tokens and (sum(part.values()) < min_seconds or done == 0):
+            a = done % n_tokens
+            xs = X[a:a + chunk].astype(np.float64)
+            y = xs @ W64.T          # signal: input of the SQNR step, not timed
+            with threadpoolctl.threadpool_limits(limits=limit):
+                info = threadpoolctl.threadpool_info()
+                t0 = time.perf_counter()
+                o.second_moment_sum(xs)
+                t1 = time.perf_counter()
+                qx, sx = o.transform_quant(xs, T)
+                t2 = time.perf_counter()
+                _, yt = o.w4a4_linear(qx, sx, qw, s_w)
+                t3 = time.perf_counter()
+                o.sqnr(y, yt)
+                t4 = time.perf_counter()
+            for key, dt in zip(part, (t1 - t0, t2 - t1, t3 - t2, t4 - t3)):
+                part[key] += dt
+            done += xs.shape[0]
+        total = sum(part.values())
+        threads = max([i.get("num_threads", 1) for i in info] or [1])
+        return done, total, part, threads, info
+
+    done, total, part, threads, info = sample(None)
+    d1, t1, p1, _, _ = sample(1)
+    blas = [{k: i.get(k) for k in ("internal_api", "version", "num_threads", "threading_layer")}
+            for i in info]
+    return {"value": done / total, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{done} tokens ({done / n_tokens:.2f} passes over one step's "
-                      f"{n_tokens}-token batch) in 512-token chunks, {t_total:.1f} s of "
-                      f"oracle time (fp64 numpy, os.cpu_count()={os.cpu_count()})"}
+                      f"{n_tokens}-token batch) in 512-token chunks, {total:.1f} s of oracle "
+                      f"time (fp64 numpy); one-thread run: {d1} tokens in {t1:.1f} s",
+            "seconds_per_part": part,
+            "one_thread": {"value": d1 / t1, "unit": "tokens/s", "cores": 1,
+                           "seconds_per_part": p1},
+            "host": {"cpu_model": _cpu_model(), "os_cpu_count": os.cpu_count(),
+                     "affinity_cores": _CORES, "blas": blas,
+                     "env": {v: os.environ.get(v) for v in
+                             ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS")}}}
 
 
 def copy_calibration(mib):
@@ -140,6 +194,206 @@ def copy_calibration(mib):
     print(json.dumps({"copy_calibration_bytes": mib << 20, "launches": 5}), flush=True)
 
 
+# ------------------------------------------------------------ GPU clocks
+class ClockSampler:
+    """Samples the graphics and memory clocks of this process's GPU through
+    amd-smi (matched by PCI address) every 2 ms on a side thread.  Reports
+    nothing if the monitoring library is unavailable."""
+
+    def __init__(self, torch):
+        self.samples, self.handle, self.smi = [], None, None
+        try:
+            import amdsmi
+            amdsmi.amdsmi_init()
+            props = torch.cuda.get_device_properties(0)
+            want = f"{props.pci_domain_id:04x}:{props.pci_bus_id:02x}:{props.pci_device_id:02x}"
+            for h in amdsmi.amdsmi_get_processor_handles():
+                if amdsmi.amdsmi_get_gpu_device_bdf(h).lower().startswith(want):
+                    self.handle = h
+            self.smi = amdsmi
+        except Exception:  # monitoring is optional
+            self.handle = None
+
+    def _read(self):
+        gfx = self.smi.amdsmi_get_clock_info(self.handle, self.smi.AmdSmiClkType.GFX)
+        mem = self.smi.amdsmi_get_clock_info(self.handle, self.smi.AmdSmiClkType.MEM)
+        return gfx.get("clk"), mem.get("clk")
+
+    def __enter__(self):
+        self._stop = threading.Event()
+        if self.handle is not None:
+            def run():
+                while not self._stop.is_set():
+                    try:
+                        self.samples.append(self._read())
+                    except Exception:
+                        return
+                    time.sleep(0.002)
+            self._thr = threading.Thread(target=run, daemon=True)
+            self._thr.start()
+        return self
+
+    def __exit__(self, *a):
+        self._stop.set()
+        if self.handle is not None:
+            self._thr.join(timeout=1.0)
+
+    def summary(self):
+        s = [x for x in self.samples if x[0] is not None]
+        if not s:
+            return None
+        g = np.array([x[0] for x in s], dtype=np.float64)
+        m = np.array([x[1] for x in s], dtype=np.float64)
+        return {"samples": len(s), "gfx_MHz": {"median": float(np.median(g)), "min": float(g.min()),
+                                               "max": float(g.max())},
+                "mem_MHz": {"median": float(np.median(m)), "min": float(m.min()),
+                            "max": float(m.max())}}
+
+
+# ------------------------------------------------------------ helpers
+def timed_pairs(torch, calls, iters):
+    """Run `calls` (a list of callables) `iters` + 2 times; returns per-call
+    event-timed ms of the last `iters` iterations."""
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(calls) + 1)]
+          for _ in range(iters)]
+    for i in range(2 + iters):
+        e = ev[i - 2] if i >= 2 else None
+        for j, c in enumerate(calls):
+            if e:
+                e[j].record()
+            c(i)
+        if e:
+            e[-1].record()
+    torch.cuda.synchronize()
+    return [[e[j].elapsed_time(e[j + 1]) for e in ev] for j in range(len(calls))]
+
+
+def tq_bytes_of(n, d_in, k, x_bytes=2, t_bytes=2, code_bytes=0.5):
+    return n * d_in * x_bytes + n * d_in * code_bytes + n * 4 + d_in * k * t_bytes
+
+
+def gemm_ops_of(n, d_in, d_out):
+    return 2.0 * n * d_in * d_out
+
+
+def kernel_line(ms, work, unit, peak):
+    """Event-timed ms statistics of one kernel and its rate at the median
+    time in `unit` (GB/s, TOP/s or TFLOP/s), with the fraction of `peak`."""
+    st = stats(ms)
+    scale = 1e9 if unit == "GB/s" else 1e12
+    rate = work / (st["median"] * 1e-3) / scale
+    return {"ms": st, "rate": rate, "unit": unit, "frac_peak": rate / peak}
+
+
+# --------------------------------------------- report: other configurations
+def report_tiny(torch, cat, B, P, wl, seed):
+    """Tiny fp32 layer: SQNR of the whole GPU chain for T = I, the block
+    Hadamard H_32, the full Hadamard H_256 (one 256-block) and CAT (k = 32),
+    at 4, 6 and 8 bits."""
+    cfg = wl.get_config("tiny")
+    lay = wl.make_layer(cfg, seed=seed)
+    dev = torch.device("cuda:0")
+    Xc = P.to_device(lay["X_cal"], "f32")
+    X = P.to_device(lay["X"], "f32")
+    y = P.reference_output(X, lay["W"])
+    out = {}
+    for label, k, flags in (("I", 32, 0), ("H_32 block", 32, B.CAT_BUILD_HADAMARD),
+                            ("H_256 full", 256, B.CAT_BUILD_HADAMARD),
+                            ("CAT_32", 32, B.CAT_BUILD_CAT)):
+        sig = P.calibrate_blocks(Xc, k) if flags & B.CAT_BUILD_ALIGN else None
+        layer = P.build_layer(sig, lay["W"], k, B.CAT_F32, flags=flags, bits=(4, 6, 8), device=dev)
+        run = P.LayerRunner(layer, cfg.n, cfg.d_in, cfg.d_out, device=dev)
+        for bits in (4, 6, 8):
+            out.setdefault(f"W{bits}A{bits}", {})[label] = float(run.run(X, y, bits)[2])
+    return {"workload": "tiny: 256->256 fp32, 2048 calibration / 512 eval tokens, seed "
+                        f"{seed}", "sqnr_db": out}
+
+
+def report_layer(torch, cat, B, P, wl, name, k, seed, iters):
+    """A layer's four kernels at its full size: median event-timed ms and
+    rate of transform+quant, the W4A4 GEMM, SQNR and the full Sigma_x of the
+    batch, plus the chain's SQNR."""
+    cfg = wl.get_config(name, k=k)
+    n, d_in, d_out = cfg.n, cfg.d_in, cfg.d_out
+    lay = wl.make_layer(cfg, seed=seed)
+    Xc = P.to_device(lay["X_cal"], "bf16")
+    sig = P.calibrate_blocks(Xc, k)
+    del Xc, lay["X_cal"]
+    torch.cuda.empty_cache()
+    layer = P.build_layer(sig, lay["W"], k, B.CAT_BF16)
+    X0 = P.to_device(lay["X"], "bf16")
+    Xs = [X0, torch.roll(X0, shifts=1, dims=0).contiguous()]
+    Ys = [P.reference_output(Xi, lay["W"]) for Xi in Xs]
+    run = P.LayerRunner(layer, n, d_in, d_out)
+    sigma = torch.zeros((d_in, d_in), dtype=torch.float32, device="cuda")
+    ws_c = torch.empty(max(16, cat.cat_cov_workspace_bytes(B.CAT_BF16, n, d_in, B.CAT_COV_FULL,
+                                                           1)), dtype=torch.uint8, device="cuda")
+    ms = timed_pairs(torch, [lambda i: run.transform_quant(Xs[i % 2]), lambda i: run.linear(),
+                             lambda i: run.sqnr(Ys[i % 2]),
+                             lambda i: cat.cat_cov_accumulate(Xs[i % 2], sigma, B.CAT_COV_FULL,
+                                                              1, ws_c)], iters)
+    db = float(run.run(X0, Ys[0])[2])
+    res = {"workload": f"{name}: {d_in}->{d_out}, block {k}, {n} tokens, "
+                       f"{cfg.n_cal} calibration tokens, seed {seed}",
+           "sqnr_db": db,
+           "transform_quant": kernel_line(ms[0], tq_bytes_of(n, d_in, k), "GB/s",
+                                          PEAK["hbm_GBps"]),
+           "w4a4_linear": kernel_line(ms[1], gemm_ops_of(n, d_in, d_out), "TOP/s",
+                                      PEAK["int8_TOPS"]),
+           "sqnr": kernel_line(ms[2], 8.0 * n * d_out, "GB/s", PEAK["hbm_GBps"]),
+           "cov_accumulate_full": kernel_line(ms[3], float(n) * d_in * (d_in + 1), "TFLOP/s",
+                                              PEAK["bf16_TFLOPS"])}
+    res["linear_tokens_per_s"] = n / ((res["transform_quant"]["ms"]["median"] +
+                                       res["w4a4_linear"]["ms"]["median"]) * 1e-3)
+    return res
+
+
+def report_stress(torch, cat, B, P, wl, seed, iters):
+    """Stress layer (8192 -> 28672, 16384 tokens): transform+quant time and
+    the chain's SQNR for every block size of the sweep, the GEMM time, and
+    the 4/6/8-bit widths at k = 128."""
+    cfg = wl.get_config("stress")
+    n, d_in, d_out = cfg.n, cfg.d_in, cfg.d_out
+    lay = wl.make_layer(cfg, seed=seed)
+    Xc = P.to_device(lay["X_cal"], "bf16")
+    del lay["X_cal"]
+    X0 = P.to_device(lay["X"], "bf16")
+    Xs = [X0, torch.roll(X0, shifts=1, dims=0).contiguous()]
+    y0 = P.reference_output(X0, lay["W"])
+    sweep, widths, gemm = {}, {}, None
+    for k in cfg.k_sweep:
+        t0 = time.perf_counter()
+        sig = P.calibrate_blocks(Xc, k)
+        bits = (4, 6, 8) if k == 128 else (4,)
+        layer = P.build_layer(sig, lay["W"], k, B.CAT_BF16, bits=bits)
+        t_build = time.perf_counter() - t0
+        run = P.LayerRunner(layer, n, d_in, d_out)
+        ms = timed_pairs(torch, [lambda i: run.transform_quant(Xs[i % 2])], iters)
+        db = float(run.run(X0, y0)[2])
+        sweep[str(k)] = {"sqnr_db": db, "host_build_s": t_build,
+                         "transform_quant": kernel_line(ms[0], tq_bytes_of(n, d_in, k), "GB/s",
+                                                        PEAK["hbm_GBps"])}
+        if k == 128:
+            ms = timed_pairs(torch, [lambda i: run.linear()], iters)
+            gemm = kernel_line(ms[0], gemm_ops_of(n, d_in, d_out), "TOP/s", PEAK["int8_TOPS"])
+            widths["W4A4"] = {"sqnr_db": db}
+            for b in (6, 8):
+                ms = timed_pairs(torch, [lambda i, b=b: run.transform_quant(Xs[i % 2], b),
+                                         lambda i, b=b: run.linear(b)], iters)
+                widths[f"W{b}A{b}"] = {
+                    "sqnr_db": float(run.run(X0, y0, b)[2]),
+                    "transform_quant": kernel_line(ms[0], tq_bytes_of(n, d_in, k, code_bytes=1),
+                                                   "GB/s", PEAK["hbm_GBps"]),
+                    "int8_linear": kernel_line(ms[1], gemm_ops_of(n, d_in, d_out), "TOP/s",
+                                               PEAK["int8_TOPS"])}
+        del run, layer
+        torch.cuda.empty_cache()
+    return {"workload": f"stress: {d_in}->{d_out}, {n} tokens, {cfg.n_cal} calibration tokens, "
+                        f"seed {seed}", "k_sweep": sweep, "w4a4_linear_k128": gemm,
+            "widths_k128": widths}
+
+
+# ------------------------------------------------------------------ main
 def main():
     args = parse()
     if args.copy_calibration:
@@ -152,6 +406,7 @@ def main():
     import torch
     import paper_2603_04359_amd as cat
     from paper_2603_04359_amd import binding as B
+    from paper_2603_04359_amd import pipeline as P
     import workloads as wl
 
     if not torch.cuda.is_available():
@@ -162,48 +417,27 @@ def main():
     cfg = wl.get_config(args.config)
     d_in, d_out, k, n = cfg.d_in, cfg.d_out, cfg.k, cfg.n
     xdt = torch.bfloat16 if cfg.dtype == "bf16" else torch.float32
+    tdt = B.CAT_BF16 if cfg.dtype == "bf16" else B.CAT_F32
     log(f"[bench] generating {cfg.name} layer (seed {args.seed})")
     lay = wl.make_layer(cfg, seed=args.seed)
 
     # ---------------- calibration + transform construction (untimed set-up)
     log("[bench] calibration: block-diagonal Sigma_x on the GPU")
-    Xc = torch.from_numpy(lay["X_cal"]).to(dev).to(xdt)
-    acc_blk = torch.zeros((d_in // k, k, k), dtype=torch.float32, device=dev)
-    for a in range(0, cfg.n_cal, 8192):
-        cat.cat_cov_accumulate(Xc[a:a + 8192], acc_blk, B.CAT_COV_BLOCK_DIAG, k)
-    torch.cuda.synchronize()
+    Xc = P.to_device(lay["X_cal"], cfg.dtype)
+    sig = P.calibrate_blocks(Xc, k)
     del Xc
-    sx_blocks = acc_blk.double().cpu().numpy() / cfg.n_cal
     log("[bench] host transform construction")
     t0 = time.perf_counter()
-    tdt = B.CAT_BF16 if cfg.dtype == "bf16" else B.CAT_F32
-    T_host, _, Wp = cat.cat_build_transform(sx_blocks, lay["W"], k, B.CAT_BUILD_CAT, tdt)
-    codes_w_h, s_w_h = cat.cat_quantize_weights(Wp, 4)
+    layer = P.build_layer(sig, lay["W"], k, tdt, bits=(4, 6, 8))
     t_build = time.perf_counter() - t0
 
     # ---------------- device-resident inputs (two alternating sets)
-    X0 = torch.from_numpy(lay["X"]).to(dev).to(xdt)
-    if tdt == B.CAT_BF16:
-        T_dev = torch.from_numpy(T_host.view(np.int16)).to(dev).view(torch.bfloat16)
-    else:
-        T_dev = torch.from_numpy(T_host).to(dev)
-    W_dev = torch.from_numpy(lay["W"]).to(dev)
-    # y: the unquantized layer output (the SQNR signal), an input of the
-    # sqnr step synthesised once here in fp32
+    X0 = P.to_device(lay["X"], cfg.dtype)
     Xs = [X0, torch.roll(X0, shifts=1, dims=0).contiguous()]
-    Ys = []
-    for Xi in Xs:
-        Ys.append(torch.matmul(Xi.float(), W_dev.t()).contiguous())
-    del W_dev
-    codes_w = torch.from_numpy(codes_w_h).to(dev)
-    s_w = torch.from_numpy(s_w_h).to(dev)
-    codes = torch.empty((n, d_in // 2), dtype=torch.uint8, device=dev)
-    s_x = torch.empty(n, dtype=torch.float32, device=dev)
-    ws_q = torch.empty(cat.cat_transform_quant_workspace_bytes(n, d_in, k), dtype=torch.uint8,
-                       device=dev)
-    y_t = torch.empty((n, d_out), dtype=torch.float32, device=dev)
-    ws_s = torch.empty(cat.cat_sqnr_workspace_bytes(n * d_out), dtype=torch.uint8, device=dev)
-    out = torch.empty(3, dtype=torch.float64, device=dev)
+    # y: the unquantized layer output (the SQNR signal), fp64 on the device
+    # and stored as fp32; an input of the sqnr step, formed once here
+    Ys = [P.reference_output(Xi, lay["W"]) for Xi in Xs]
+    run = P.LayerRunner(layer, n, d_in, d_out)
     sigma = torch.zeros((d_in, d_in), dtype=torch.float32, device=dev)
     ws_c = torch.empty(max(16, cat.cat_cov_workspace_bytes(
         B.CAT_BF16 if xdt == torch.bfloat16 else B.CAT_F32, n, d_in, B.CAT_COV_FULL, k)),
@@ -212,11 +446,11 @@ def main():
     def step(i, ev=None):
         Xi, Yi = Xs[i % 2], Ys[i % 2]
         if ev: ev[0].record()
-        cat.cat_transform_quant(Xi, T_dev, k, codes, s_x, ws_q)
+        run.transform_quant(Xi)
         if ev: ev[1].record()
-        cat.cat_w4a4_linear(codes, s_x, codes_w, s_w, y_t)
+        run.linear()
         if ev: ev[2].record()
-        cat.cat_sqnr(Yi, y_t, ws_s, out)
+        run.sqnr(Yi)
         if ev: ev[3].record()
         cat.cat_cov_accumulate(Xi, sigma, B.CAT_COV_FULL, k, ws_c)
         if ev: ev[4].record()
@@ -225,28 +459,39 @@ def main():
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
-    sqnr_db = float(out[2].item())
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     log(f"[bench] timing {args.steps} steps")
+    clocks = ClockSampler(torch)
     torch.cuda.synchronize()
-    t_start.record()
-    for i in range(args.steps):
-        step(args.warmup + i, evs[i])
-    t_end.record()
-    torch.cuda.synchronize()
+    with clocks:
+        t_start.record()
+        for i in range(args.steps):
+            step(args.warmup + i, evs[i])
+        t_end.record()
+        torch.cuda.synchronize()
+        # a sustained GEMM window after the steps, so the clock sampler sees
+        # the power state of the dominant kernel over ~0.5 s
+        if clocks.handle is not None:
+            for _ in range(max(1, int(500 / 0.4))):
+                run.linear()
+            torch.cuda.synchronize()
     ms_step = t_start.elapsed_time(t_end) / args.steps
     names = ["transform_quant", "w4a4_linear", "sqnr", "cov_accumulate"]
-    per = {nm: float(np.mean([e[j].elapsed_time(e[j + 1]) for e in evs]))
-           for j, nm in enumerate(names)}
-    log("[bench] per-call ms: " + ", ".join(f"{k_}={v:.4f}" for k_, v in per.items()))
+    per_ms = {nm: [e[j].elapsed_time(e[j + 1]) for e in evs] for j, nm in enumerate(names)}
+    per = {nm: float(np.mean(v)) for nm, v in per_ms.items()}
+    log("[bench] per-call ms (mean): " + ", ".join(f"{k_}={v:.4f}" for k_, v in per.items()))
+
+    # the chain's SQNR on the first input set (the value the full-size layer
+    # test compares with the oracle's chain)
+    sqnr_db = float(run.run(X0, Ys[0])[2])
 
     # ---------------- algorithmic work per launch
-    gemm_ops = 2.0 * n * d_in * d_out
+    gemm_ops = gemm_ops_of(n, d_in, d_out)
     gemm_bytes = n * d_in / 2 + n * 4 + d_out * d_in / 2 + d_out * 4 + n * d_out * 4
-    tq_bytes = n * d_in * (2 if xdt == torch.bfloat16 else 4) + n * d_in / 2 + n * 4 + \
-        d_in * k * (2 if tdt == B.CAT_BF16 else 4)
+    tq_bytes = tq_bytes_of(n, d_in, k, 2 if xdt == torch.bfloat16 else 4,
+                           2 if tdt == B.CAT_BF16 else 4)
     sq_bytes = 8.0 * n * d_out
     cov_flop = float(n) * d_in * (d_in + 1)
     t_g = per["w4a4_linear"] * 1e-3
@@ -255,15 +500,19 @@ def main():
     t_c = per["cov_accumulate"] * 1e-3
     gemm_tops = gemm_ops / t_g / 1e12
     kernels = {
-        "w4a4_linear": {"ms": per["w4a4_linear"], "TOPS": gemm_tops,
-                        "frac_int8_peak": gemm_tops / PEAK["int8_TOPS"],
+        "w4a4_linear": {"ms": per["w4a4_linear"], "ms_stats": stats(per_ms["w4a4_linear"]),
+                        "TOPS": gemm_tops, "frac_int8_peak": gemm_tops / PEAK["int8_TOPS"],
                         "tokens_per_s": n / t_g},
-        "transform_quant": {"ms": per["transform_quant"], "GBps": tq_bytes / t_q / 1e9,
+        "transform_quant": {"ms": per["transform_quant"],
+                            "ms_stats": stats(per_ms["transform_quant"]),
+                            "GBps": tq_bytes / t_q / 1e9,
                             "frac_hbm_peak": tq_bytes / t_q / 1e9 / PEAK["hbm_GBps"],
                             "algorithmic_bytes": tq_bytes},
-        "sqnr": {"ms": per["sqnr"], "GBps": sq_bytes / t_s / 1e9,
+        "sqnr": {"ms": per["sqnr"], "ms_stats": stats(per_ms["sqnr"]),
+                 "GBps": sq_bytes / t_s / 1e9,
                  "frac_hbm_peak": sq_bytes / t_s / 1e9 / PEAK["hbm_GBps"]},
-        "cov_accumulate": {"ms": per["cov_accumulate"], "TFLOPS": cov_flop / t_c / 1e12,
+        "cov_accumulate": {"ms": per["cov_accumulate"], "ms_stats": stats(per_ms["cov_accumulate"]),
+                           "TFLOPS": cov_flop / t_c / 1e12,
                            "frac_bf16_peak": cov_flop / t_c / 1e12 / PEAK["bf16_TFLOPS"]},
     }
     traffic = measured_traffic("w4a4_linear")
@@ -284,7 +533,8 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "int8",
-        "dtypes": {"transform_quant": "bf16 MFMA -> int4", "w4a4_linear": "int4 codes on int8 MFMA -> int32 -> f32",
+        "dtypes": {"transform_quant": "bf16 MFMA -> int4",
+                   "w4a4_linear": "int4 codes on int8 MFMA -> int32 -> f32",
                    "sqnr": "f32 -> f64", "cov_accumulate": "bf16 MFMA -> f32"},
         "data": "synthetic",
         "config": {"workload": f"{cfg.name}: CAT W4A4 linear {d_in}->{d_out}, block {k}, "
@@ -298,117 +548,121 @@ def main():
         "sqnr_db": sqnr_db,
         "kernels": kernels,
         "roofline": roofline,
+        "clocks": clocks.summary(),
         "host_transform_build_s": t_build,
     }
-    # ---------------- the W6A6 / W8A8 comparison widths (after the timed
-    # steps; not part of the step): the same layer and tokens through
-    # transform+quant at 6 or 8 bits and the int8-code GEMM
-    wide = {"W4A4": {"sqnr_db": sqnr_db}}
-    codes8 = torch.empty((n, d_in), dtype=torch.int8, device=dev)
+
+    if not args.no_report:
+        widened(rec, torch, cat, B, P, layer, run, Xs, Ys, lay, n, d_in, d_out, k, tdt,
+                tq_bytes, gemm_ops, args.wide_steps)
+        # free the metric layer before the other configurations
+        del run, Xs, Ys, X0, sigma, ws_c
+        torch.cuda.empty_cache()
+        rep = {}
+        log("[bench] report: tiny layer transforms")
+        rep["tiny"] = report_tiny(torch, cat, B, P, wl, args.seed)
+        for name, kk in (("attn4096", 128), ("mlp_down", 256)):
+            log(f"[bench] report: {name}")
+            rep[name] = report_layer(torch, cat, B, P, wl, name, kk, args.seed, args.wide_steps)
+            torch.cuda.empty_cache()
+        log("[bench] report: stress block-size sweep and widths")
+        rep["stress"] = report_stress(torch, cat, B, P, wl, args.seed, args.wide_steps)
+        rec["configs_report"] = rep
+
+    if not args.no_cpu_baseline:
+        log("[bench] CPU oracle baseline (all cores, then one thread)")
+        T_vals = wl.bf16_bits_to_f32(layer["T_host"]) if tdt == B.CAT_BF16 else layer["T_host"]
+        rec["cpu_baseline"] = cpu_baseline(lay, T_vals, layer["weights"][4]["codes_host"],
+                                           layer["weights"][4]["s_host"], n, args.cpu_seconds)
+    print(json.dumps(rec), flush=True)
+
+
+def widened(rec, torch, cat, B, P, layer, run, Xs, Ys, lay, n, d_in, d_out, k, tdt, tq_bytes,
+            gemm_ops, iters):
+    """After the timed steps (same layer and batch, not part of the step):
+    the W6A6 / W8A8 widths, the Theorem 2.4 terms, the full-dimension
+    Hadamard and asymmetric activations."""
+    T_dev, Wp = layer["T"], layer["W_prime"]
+    wide = {"W4A4": {"sqnr_db": rec["sqnr_db"]}}
     for bits in (6, 8):
-        cw_h, sw_h = cat.cat_quantize_weights(Wp, bits)
-        cw, sw = torch.from_numpy(cw_h).to(dev), torch.from_numpy(sw_h).to(dev)
-        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)]
-              for _ in range(args.wide_steps)]
-        for i in range(2 + args.wide_steps):
-            e = ev[i - 2] if i >= 2 else None
-            if e: e[0].record()
-            cat.cat_transform_quant(Xs[i % 2], T_dev, k, codes8, s_x, ws_q, bits=bits)
-            if e: e[1].record()
-            cat.cat_int8_linear(codes8, s_x, cw, sw, y_t)
-            if e: e[2].record()
-        cat.cat_sqnr(Ys[(1 + args.wide_steps) % 2], y_t, ws_s, out)
-        torch.cuda.synchronize()
-        tq_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
-        g_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+        ms = timed_pairs(torch, [lambda i, b=bits: run.transform_quant(Xs[i % 2], b),
+                                 lambda i, b=bits: run.linear(b)], iters)
+        db = float(run.run(Xs[0], Ys[0], bits)[2])
+        tq_ms, g_ms = float(np.mean(ms[0])), float(np.mean(ms[1]))
         tq_b = tq_bytes + n * d_in / 2          # one byte per code instead of half
         g_tops = gemm_ops / (g_ms * 1e-3) / 1e12
         wide[f"W{bits}A{bits}"] = {
-            "sqnr_db": float(out[2].item()),
-            "transform_quant": {"ms": tq_ms, "GBps": tq_b / (tq_ms * 1e-3) / 1e9,
+            "sqnr_db": db,
+            "transform_quant": {"ms": tq_ms, "ms_stats": stats(ms[0]),
+                                "GBps": tq_b / (tq_ms * 1e-3) / 1e9,
                                 "frac_hbm_peak": tq_b / (tq_ms * 1e-3) / 1e9 / PEAK["hbm_GBps"]},
-            "int8_linear": {"ms": g_ms, "TOPS": g_tops, "frac_int8_peak": g_tops / PEAK["int8_TOPS"]},
+            "int8_linear": {"ms": g_ms, "ms_stats": stats(ms[1]), "TOPS": g_tops,
+                            "frac_int8_peak": g_tops / PEAK["int8_TOPS"]},
             "linear_tokens_per_s": n / ((tq_ms + g_ms) * 1e-3)}
         log(f"[bench] W{bits}A{bits}: transform_quant {tq_ms:.4f} ms, int8_linear {g_ms:.4f} ms "
-            f"({g_tops:.0f} TOP/s), SQNR {wide[f'W{bits}A{bits}']['sqnr_db']:.2f} dB")
-    # ---------------- the Theorem 2.4 decomposition of the W4A4 layer from
-    # device results (per-token scales, the batch's block second-moment
-    # sums, sum y^2), after the timed steps
-    cat.cat_transform_quant(Xs[0], T_dev, k, codes, s_x, ws_q)
-    cat.cat_w4a4_linear(codes, s_x, codes_w, s_w, y_t)
-    cat.cat_sqnr(Ys[0], y_t, ws_s, out)
-    acc_e = torch.zeros((d_in // k, k, k), dtype=torch.float32, device=dev)
+            f"({g_tops:.0f} TOP/s), SQNR {db:.2f} dB")
+    rec["wide_codes"] = wide
+
+    # the Theorem 2.4 decomposition of the W4A4 layer from device results
+    # (per-token scales, the batch's block second-moment sums, sum y^2)
+    res = run.run(Xs[0], Ys[0], 4)
+    acc_e = torch.zeros((d_in // k, k, k), dtype=torch.float32, device="cuda")
     cat.cat_cov_accumulate(Xs[0], acc_e, B.CAT_COV_BLOCK_DIAG, k)
     torch.cuda.synchronize()
-    res = out.cpu().numpy()
-    terms = cat.cat_sqnr_terms(s_x.cpu().numpy(), 4, acc_e.double().cpu().numpy(), T_host, tdt,
-                               Wp, 4, float(res[0]))
+    terms = cat.cat_sqnr_terms(run.s_x.cpu().numpy(), 4, acc_e.double().cpu().numpy(),
+                               layer["T_host"], tdt, Wp, 4, float(res[0]))
     terms["measured_db"] = float(res[2])
     rec["theorem_2_4"] = terms
     log(f"[bench] Theorem 2.4: predicted {terms['sqnr_pred_db']:.2f} dB, measured {res[2]:.2f} dB")
 
-    # ---------------- full-dimension Hadamard T = H_d blockdiag(M_b), INT4,
-    # after the timed steps
+    # full-dimension Hadamard T = H_d blockdiag(M_b), INT4
+    rec_full = None
     if cat.cat_transform_quant_full_workspace_bytes(n, d_in, k) and tdt == B.CAT_BF16 and \
             k in (128, 256):
         cw_h, sw_h = cat.cat_quantize_weights(cat.cat_full_hadamard_weights(Wp, k), 4)
-        cw, sw = torch.from_numpy(cw_h).to(dev), torch.from_numpy(sw_h).to(dev)
+        cw, sw = torch.from_numpy(cw_h).cuda(), torch.from_numpy(sw_h).cuda()
         ws_f = torch.empty(cat.cat_transform_quant_full_workspace_bytes(n, d_in, k),
-                           dtype=torch.uint8, device=dev)
-        ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)]
-              for _ in range(args.wide_steps)]
-        for i in range(2 + args.wide_steps):
-            e = ev[i - 2] if i >= 2 else None
-            if e: e[0].record()
-            cat.cat_transform_quant_full(Xs[i % 2], T_dev, k, codes, s_x, ws_f)
-            if e: e[1].record()
-            cat.cat_w4a4_linear(codes, s_x, cw, sw, y_t)
-            if e: e[2].record()
-        cat.cat_sqnr(Ys[(1 + args.wide_steps) % 2], y_t, ws_s, out)
+                           dtype=torch.uint8, device="cuda")
+        ms = timed_pairs(torch, [
+            lambda i: cat.cat_transform_quant_full(Xs[i % 2], T_dev, k, run.codes4, run.s_x, ws_f),
+            lambda i: cat.cat_w4a4_linear(run.codes4, run.s_x, cw, sw, run.y_t)], iters)
+        cat.cat_transform_quant_full(Xs[0], T_dev, k, run.codes4, run.s_x, ws_f)
+        cat.cat_w4a4_linear(run.codes4, run.s_x, cw, sw, run.y_t)
+        run.sqnr(Ys[0])
         torch.cuda.synchronize()
-        tq_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
-        g_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
-        rec_full = {"sqnr_db": float(out[2].item()), "transform_quant_full_ms": tq_ms,
+        tq_ms, g_ms = float(np.mean(ms[0])), float(np.mean(ms[1]))
+        rec_full = {"sqnr_db": float(run.out[2].item()), "transform_quant_full_ms": tq_ms,
+                    "transform_quant_full_ms_stats": stats(ms[0]),
                     "w4a4_linear_ms": g_ms, "linear_tokens_per_s": n / ((tq_ms + g_ms) * 1e-3)}
         log(f"[bench] full-dimension Hadamard: transform_quant {tq_ms:.4f} ms, SQNR "
             f"{rec_full['sqnr_db']:.2f} dB")
         del ws_f
-    else:
-        rec_full = None
-    del Wp
-    rec["wide_codes"] = wide
     rec["full_hadamard"] = rec_full
 
-    # ---------------- asymmetric per-token activations (the paper's own
-    # activation set-up), INT4, after the timed steps
-    zmin = torch.empty(n, dtype=torch.float32, device=dev)
-    rsum = torch.from_numpy(cat.cat_weight_code_sums(codes_w_h)).to(dev)
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.wide_steps)]
-    for i in range(2 + args.wide_steps):
-        e = ev[i - 2] if i >= 2 else None
-        if e: e[0].record()
-        cat.cat_transform_quant_asym(Xs[i % 2], T_dev, k, codes, s_x, zmin, ws_q)
-        if e: e[1].record()
-        cat.cat_w4a4_linear_asym(codes, s_x, zmin, codes_w, s_w, rsum, y_t)
-        if e: e[2].record()
-    cat.cat_sqnr(Ys[(1 + args.wide_steps) % 2], y_t, ws_s, out)
+    # asymmetric per-token activations (the paper's own activation set-up)
+    w4 = layer["weights"][4]
+    zmin = torch.empty(n, dtype=torch.float32, device="cuda")
+    rsum = torch.from_numpy(cat.cat_weight_code_sums(w4["codes_host"])).cuda()
+    ms = timed_pairs(torch, [
+        lambda i: cat.cat_transform_quant_asym(Xs[i % 2], T_dev, k, run.codes4, run.s_x, zmin,
+                                               run.ws_q),
+        lambda i: cat.cat_w4a4_linear_asym(run.codes4, run.s_x, zmin, w4["codes"], w4["s"], rsum,
+                                           run.y_t)], iters)
+    cat.cat_transform_quant_asym(Xs[0], T_dev, k, run.codes4, run.s_x, zmin, run.ws_q)
+    cat.cat_w4a4_linear_asym(run.codes4, run.s_x, zmin, w4["codes"], w4["s"], rsum, run.y_t)
+    run.sqnr(Ys[0])
     torch.cuda.synchronize()
-    tq_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
-    g_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    tq_ms, g_ms = float(np.mean(ms[0])), float(np.mean(ms[1]))
     g_tops = gemm_ops / (g_ms * 1e-3) / 1e12
     rec["asymmetric_activations"] = {
-        "sqnr_db": float(out[2].item()), "sqnr_db_symmetric": sqnr_db,
-        "transform_quant": {"ms": tq_ms, "GBps": (tq_bytes + 4 * n) / (tq_ms * 1e-3) / 1e9},
-        "w4a4_linear": {"ms": g_ms, "TOPS": g_tops, "frac_int8_peak": g_tops / PEAK["int8_TOPS"]},
+        "sqnr_db": float(run.out[2].item()), "sqnr_db_symmetric": rec["sqnr_db"],
+        "transform_quant": {"ms": tq_ms, "ms_stats": stats(ms[0]),
+                            "GBps": (tq_bytes + 4 * n) / (tq_ms * 1e-3) / 1e9},
+        "w4a4_linear": {"ms": g_ms, "ms_stats": stats(ms[1]), "TOPS": g_tops,
+                        "frac_int8_peak": g_tops / PEAK["int8_TOPS"]},
         "linear_tokens_per_s": n / ((tq_ms + g_ms) * 1e-3)}
     log(f"[bench] asymmetric INT4: transform_quant {tq_ms:.4f} ms, w4a4_linear {g_ms:.4f} ms, "
         f"SQNR {rec['asymmetric_activations']['sqnr_db']:.2f} dB")
-
-    if not args.no_cpu_baseline:
-        log("[bench] CPU oracle baseline")
-        T_vals = wl.bf16_bits_to_f32(T_host) if tdt == B.CAT_BF16 else T_host
-        rec["cpu_baseline"] = cpu_baseline(lay, T_vals, codes_w_h, s_w_h, n, args.cpu_seconds)
-    print(json.dumps(rec), flush=True)
 
 
 if __name__ == "__main__":

@@ -164,6 +164,10 @@ int cat_transform_quant(const void* X, int x_dtype, int64_t n, int64_t d,
  * codes_x  device uint8 [n x d_in/2] packed INT4, s_x device fp32 [n].
  * codes_w  device uint8 [d_out x d_in/2] packed INT4, s_w device fp32 [d_out].
  * n, d_out >= 1; d_in a multiple of 32 and <= CAT_MAX_D_IN.
+ * Codes must lie in [-7, 7] (what cat_transform_quant and
+ * cat_quantize_weights produce at 4 bits): every int32 sum is then exact
+ * for d_in <= CAT_MAX_D_IN.  -8 is not checked; with -8 on both sides the
+ * widened sum reaches 256 * 64 * d_in, which is 2^31 at CAT_MAX_D_IN.
  * y_tilde  device fp32 [n x d_out] (written).
  * acc_out  device int32 [n x d_out] or NULL (written when non-NULL).
  */
@@ -173,7 +177,8 @@ int cat_w4a4_linear(const uint8_t* codes_x, const float* s_x,
                     int32_t* acc_out, void* stream);
 
 /* The same product for codes stored one int8 per element: the W6A6 and
- * W8A8 layers the paper compares W4A4 against (Sec. 5; Sec. 3, eq. 5 at
+ * W8A8 layers the paper compares W4A4 against (Sec. 4 "CAT Block
+ * Approximation" and the Fig. 6 caption; Sec. 3, eq. 5 at
  * those widths).  Same formula, arguments and errors as cat_w4a4_linear,
  * except:
  * codes_x  device int8 [n x d_in], s_x device fp32 [n].
@@ -281,7 +286,7 @@ int cat_quantize_weights(const double* W_prime, int64_t d_out, int64_t d_in,
 
 /* ------------------------------------------------------------------
  * Full-dimension Hadamard (Sec. 4: T = H M with H over all d channels;
- * Sec. 5: QuaRot-style rotations).  H_d = H_m (x) H_k with m = d / k, so
+ * Sec. 3: Hadamard rotations).  H_d = H_m (x) H_k with m = d / k, so
  *   T = (H_m (x) I_k) / sqrt(m) . blockdiag(T_b),  T_b = H_k M_b / sqrt(k)
  * (the blocks cat_build_transform returns with CAT_BUILD_HADAMARD).  H_m is
  * Sylvester for m a power of two, else H_28 (x) Sylvester_(m/28), H_28 from

@@ -57,7 +57,7 @@ Function -> passage -> what pins it (tests/test_oracle_*.py):
                                                 -> brute-force loops,
                      dequantize-then-multiply product
   hadamard_order, paley2_hadamard, full_hadamard_mix, transform_quant_full
-                     Sec. 4 (T = H M, H full-dimension), Sec. 5 (rotations)
+                     Sec. 4 (T = H M, H full-dimension), Sec. 3 (Hadamard rotations)
                                                 -> H H^T = m I and +-1
                      entries (orders 1 .. 112, incl. 28 = Paley II q = 13),
                      Sylvester = scipy.linalg.hadamard, mix of H_k blocks =
@@ -242,7 +242,7 @@ def hadamard_order(m: int) -> np.ndarray:
 
 def full_hadamard_mix(Z, k: int) -> np.ndarray:
     """Cross-block part of T = H_d M_block with H_d = H_m (x) H_k
-    (Sec. 4, T = H M with a full-dimension H; Sec. 5, QuaRot-style
+    (Sec. 4, T = H M with a full-dimension H; Sec. 3, Hadamard
     rotations): z'_(b, j) = sum_b' H_m[b, b'] z_(b', j) / sqrt(m), fp64."""
     Z = np.asarray(Z, dtype=np.float64)
     n, d = Z.shape

@@ -156,6 +156,25 @@ def _dev_ptr(t, name, dtypes=None, allow_none=False):
     return t.data_ptr()
 
 
+def _shape(t, shape, name):
+    """The C ABI takes bare pointers and cannot see buffer sizes, so every
+    buffer's shape is checked here, before the call: a short buffer would
+    otherwise be read or written past its end on the device."""
+    if tuple(t.shape) != tuple(int(v) for v in shape):
+        raise ValueError(f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+
+
+def _numel(t, count, name):
+    if t.numel() != int(count):
+        raise ValueError(f"{name} has {t.numel()} elements, expected {int(count)}")
+
+
+def _t_blocks(T, d, k, name="T"):
+    if k <= 0 or d % k:
+        raise ValueError(f"d={d} is not a multiple of the block size k={k}")
+    _numel(T, d * k, name)
+
+
 def _dtype_code(t):
     torch = _torch()
     if t.dtype == torch.bfloat16:
@@ -188,6 +207,14 @@ def cat_cov_accumulate(X, acc, mode: int = CAT_COV_FULL, k: int = 1, workspace=N
     if X.dim() != 2:
         raise ValueError("X must be [n, d]")
     n, d = X.shape
+    if mode == CAT_COV_FULL:
+        _numel(acc, d * d, "acc")
+    elif mode == CAT_COV_BLOCK_DIAG:
+        if k <= 0 or d % k:
+            raise ValueError(f"d={d} is not a multiple of the block size k={k}")
+        _numel(acc, d * k, "acc ([d/k, k, k])")
+    else:
+        raise ValueError(f"unknown mode {mode}")
     code = _dtype_code(X)
     if workspace is None:
         need = cat_cov_workspace_bytes(code, n, d, mode, k)
@@ -217,10 +244,29 @@ def cat_transform_quant(X, T, k: int, codes, s_x, workspace, bits: int = 4, stre
     n, d = X.shape
     if tuple(codes.shape) != (n, d // 2 if bits == 4 else d):
         raise ValueError(f"codes must be [{n}, {d // 2 if bits == 4 else d}] for bits={bits}")
+    _t_blocks(T, d, k)
+    _numel(s_x, n, "s_x")
     wbytes = workspace.numel() * workspace.element_size()
     _check("cat_transform_quant",
            lib().cat_transform_quant(px, _dtype_code(X), n, d, pt, _dtype_code(T), k, bits, pc, ps,
                                      pw, wbytes, _stream_ptr(stream)))
+
+
+def _gemm_shapes(codes_x, s_x, codes_w, s_w, y_tilde, acc_out):
+    """(n, row bytes, d_out) of a GEMM call after checking every buffer
+    against them."""
+    if codes_x.dim() != 2 or codes_w.dim() != 2:
+        raise ValueError("codes_x and codes_w must be 2-D")
+    n, row = codes_x.shape
+    d_out = codes_w.shape[0]
+    if codes_w.shape[1] != row:
+        raise ValueError("codes_x and codes_w disagree on d_in")
+    _numel(s_x, n, "s_x")
+    _numel(s_w, d_out, "s_w")
+    _shape(y_tilde, (n, d_out), "y_tilde")
+    if acc_out is not None:
+        _shape(acc_out, (n, d_out), "acc_out")
+    return n, row, d_out
 
 
 def cat_w4a4_linear(codes_x, s_x, codes_w, s_w, y_tilde, acc_out=None, stream=None):
@@ -232,10 +278,7 @@ def cat_w4a4_linear(codes_x, s_x, codes_w, s_w, y_tilde, acc_out=None, stream=No
     psw = _dev_ptr(s_w, "s_w", (torch.float32,))
     py = _dev_ptr(y_tilde, "y_tilde", (torch.float32,))
     pacc = _dev_ptr(acc_out, "acc_out", (torch.int32,), allow_none=True)
-    n, half = codes_x.shape
-    d_out = codes_w.shape[0]
-    if codes_w.shape[1] != half:
-        raise ValueError("codes_x and codes_w disagree on d_in")
+    n, half, d_out = _gemm_shapes(codes_x, s_x, codes_w, s_w, y_tilde, acc_out)
     _check("cat_w4a4_linear",
            lib().cat_w4a4_linear(pcx, psx, pcw, psw, n, 2 * half, d_out, py, pacc,
                                  _stream_ptr(stream)))
@@ -251,10 +294,7 @@ def cat_int8_linear(codes_x, s_x, codes_w, s_w, y_tilde, acc_out=None, stream=No
     psw = _dev_ptr(s_w, "s_w", (torch.float32,))
     py = _dev_ptr(y_tilde, "y_tilde", (torch.float32,))
     pacc = _dev_ptr(acc_out, "acc_out", (torch.int32,), allow_none=True)
-    n, d_in = codes_x.shape
-    d_out = codes_w.shape[0]
-    if codes_w.shape[1] != d_in:
-        raise ValueError("codes_x and codes_w disagree on d_in")
+    n, d_in, d_out = _gemm_shapes(codes_x, s_x, codes_w, s_w, y_tilde, acc_out)
     _check("cat_int8_linear",
            lib().cat_int8_linear(pcx, psx, pcw, psw, n, d_in, d_out, py, pacc,
                                  _stream_ptr(stream)))
@@ -275,6 +315,9 @@ def cat_transform_quant_asym(X, T, k: int, codes, s_x, zmin_x, workspace, stream
     n, d = X.shape
     if tuple(codes.shape) != (n, d // 2):
         raise ValueError(f"codes must be [{n}, {d // 2}]")
+    _t_blocks(T, d, k)
+    _numel(s_x, n, "s_x")
+    _numel(zmin_x, n, "zmin_x")
     wbytes = workspace.numel() * workspace.element_size()
     _check("cat_transform_quant_asym",
            lib().cat_transform_quant_asym(px, _dtype_code(X), n, d, pt, _dtype_code(T), k, pc, ps,
@@ -294,10 +337,9 @@ def cat_w4a4_linear_asym(codes_x, s_x, zmin_x, codes_w, s_w, rsum_w, y_tilde, ac
     prs = _dev_ptr(rsum_w, "rsum_w", (torch.int32,))
     py = _dev_ptr(y_tilde, "y_tilde", (torch.float32,))
     pacc = _dev_ptr(acc_out, "acc_out", (torch.int32,), allow_none=True)
-    n, half = codes_x.shape
-    d_out = codes_w.shape[0]
-    if codes_w.shape[1] != half:
-        raise ValueError("codes_x and codes_w disagree on d_in")
+    n, half, d_out = _gemm_shapes(codes_x, s_x, codes_w, s_w, y_tilde, acc_out)
+    _numel(zmin_x, n, "zmin_x")
+    _numel(rsum_w, d_out, "rsum_w")
     _check("cat_w4a4_linear_asym",
            lib().cat_w4a4_linear_asym(pcx, psx, pmx, pcw, psw, prs, n, 2 * half, d_out, py, pacc,
                                       _stream_ptr(stream)))
@@ -319,8 +361,12 @@ def cat_sqnr_terms(s_x, bits_x: int, sigma_sum_blocks, T, t_dtype: int, W_prime,
     S, pS = _host(sigma_sum_blocks, np.float64, "sigma_sum_blocks")
     Tn, pT = _host(T, np.uint16 if t_dtype == CAT_BF16 else np.float32, "T")
     Wp, pW = _host(W_prime, np.float64, "W_prime")
+    if S.ndim != 3 or S.shape[1] != S.shape[2]:
+        raise ValueError("sigma_sum_blocks must be [d_in/k, k, k]")
     nb, k, _ = S.shape
     d_out, d_in = Wp.shape
+    if nb * k != d_in or Tn.size != d_in * k:
+        raise ValueError("sigma_sum_blocks, T and W_prime disagree on d_in or k")
     out = np.empty(5, dtype=np.float64)
     _check("cat_sqnr_terms", lib().cat_sqnr_terms(psx, sx.shape[0], bits_x, pS, d_in, k, pT,
                                                   t_dtype, pW, d_out, bits_w, float(sum_y2),
@@ -341,9 +387,13 @@ def cat_transform_quant_full(X, T, k: int, codes, s_x, workspace, stream=None):
     pc = _dev_ptr(codes, "codes", (torch.uint8,))
     ps = _dev_ptr(s_x, "s_x", (torch.float32,))
     pw = _dev_ptr(workspace, "workspace")
+    if X.dim() != 2:
+        raise ValueError("X must be [n, d]")
     n, d = X.shape
     if tuple(codes.shape) != (n, d // 2):
         raise ValueError(f"codes must be [{n}, {d // 2}]")
+    _t_blocks(T, d, k)
+    _numel(s_x, n, "s_x")
     wbytes = workspace.numel() * workspace.element_size()
     _check("cat_transform_quant_full",
            lib().cat_transform_quant_full(px, CAT_BF16, n, d, pt, CAT_BF16, k, pc, ps, pw, wbytes,
@@ -373,6 +423,7 @@ def cat_sqnr(y, y_tilde, workspace, out, stream=None):
     po = _dev_ptr(out, "out", (torch.float64,))
     if y.numel() != y_tilde.numel():
         raise ValueError("y and y_tilde differ in size")
+    _numel(out, 3, "out")
     wbytes = workspace.numel() * workspace.element_size()
     _check("cat_sqnr", lib().cat_sqnr(py, pt, y.numel(), pw, wbytes, po, _stream_ptr(stream)))
 

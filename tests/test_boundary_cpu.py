@@ -168,3 +168,114 @@ def test_full_hadamard_invalid_args():
     g = L.cat_full_hadamard_weights
     assert g(None, 4, 64, 8, P) == B.CAT_ERR_INVALID_ARG
     assert g(P, 4, 24, 8, P) == B.CAT_ERR_UNSUPPORTED                                   # m = 3
+
+
+# ----------------------------------------------------------------------
+# Buffer-size checks in the binding.  The C ABI receives bare pointers and
+# cannot see how long a buffer is, so the binding compares every tensor's
+# shape with the sizes the call implies and raises ValueError before the
+# library is entered.  Here CPU tensors stand in for device tensors: the
+# pointer helper is replaced by one that accepts them, and the library by
+# a recorder, so a call that passes the checks is seen to reach the ABI and
+# a call that fails them is seen not to.
+class _Recorder:
+    def __init__(self):
+        self.calls = []
+
+    def __getattr__(self, name):
+        def call(*args):
+            self.calls.append(name)
+            return 0
+        return call
+
+
+@pytest.fixture
+def fake_abi(monkeypatch):
+    import torch
+    rec = _Recorder()
+
+    def ptr(t, name, dtypes=None, allow_none=False):
+        if t is None:
+            if allow_none:
+                return None
+            raise ValueError(f"{name} is required")
+        if dtypes is not None and t.dtype not in dtypes:
+            raise TypeError(name)
+        return 16
+
+    monkeypatch.setattr(B, "_dev_ptr", ptr)
+    monkeypatch.setattr(B, "lib", lambda: rec)
+    monkeypatch.setattr(B, "_stream_ptr", lambda s: None)
+    return torch, rec
+
+
+def test_binding_checks_gemm_buffer_sizes(fake_abi):
+    torch, rec = fake_abi
+    n, d_in, d_out = 8, 64, 16
+    cx = torch.zeros((n, d_in // 2), dtype=torch.uint8)
+    cw = torch.zeros((d_out, d_in // 2), dtype=torch.uint8)
+    sx, sw = torch.zeros(n), torch.zeros(d_out)
+    y = torch.zeros((n, d_out))
+    acc = torch.zeros((n, d_out), dtype=torch.int32)
+    B.cat_w4a4_linear(cx, sx, cw, sw, y, acc)
+    assert rec.calls == ["cat_w4a4_linear"]
+    bad = [dict(s_x=torch.zeros(n - 1)), dict(s_w=torch.zeros(d_out + 1)),
+           dict(y_tilde=torch.zeros((n, d_out - 1))), dict(y_tilde=torch.zeros((n * d_out,))),
+           dict(acc_out=torch.zeros((n - 1, d_out), dtype=torch.int32))]
+    for b in bad:
+        args = dict(codes_x=cx, s_x=sx, codes_w=cw, s_w=sw, y_tilde=y, acc_out=acc)
+        args.update(b)
+        with pytest.raises(ValueError):
+            B.cat_w4a4_linear(**args)
+    # int8 and asymmetric products share the checks
+    c8x = torch.zeros((n, d_in), dtype=torch.int8)
+    c8w = torch.zeros((d_out, d_in), dtype=torch.int8)
+    with pytest.raises(ValueError):
+        B.cat_int8_linear(c8x, sx, c8w, sw, torch.zeros((n + 1, d_out)))
+    zm, rs = torch.zeros(n), torch.zeros(d_out, dtype=torch.int32)
+    with pytest.raises(ValueError):
+        B.cat_w4a4_linear_asym(cx, sx, torch.zeros(n - 1), cw, sw, rs, y)
+    with pytest.raises(ValueError):
+        B.cat_w4a4_linear_asym(cx, sx, zm, cw, sw, torch.zeros(d_out - 1, dtype=torch.int32), y)
+    B.cat_w4a4_linear_asym(cx, sx, zm, cw, sw, rs, y)
+    assert rec.calls == ["cat_w4a4_linear", "cat_w4a4_linear_asym"]
+
+
+def test_binding_checks_transform_quant_buffer_sizes(fake_abi):
+    torch, rec = fake_abi
+    n, d, k = 8, 256, 32
+    X = torch.zeros((n, d), dtype=torch.bfloat16)
+    T = torch.zeros((d // k, k, k), dtype=torch.bfloat16)
+    codes = torch.zeros((n, d // 2), dtype=torch.uint8)
+    sx, ws = torch.zeros(n), torch.zeros(64, dtype=torch.uint8)
+    B.cat_transform_quant(X, T, k, codes, sx, ws)
+    with pytest.raises(ValueError):
+        B.cat_transform_quant(X, T[:-1], k, codes, sx, ws)
+    with pytest.raises(ValueError):
+        B.cat_transform_quant(X, T, k, codes, torch.zeros(n - 1), ws)
+    with pytest.raises(ValueError):
+        B.cat_transform_quant(X, T, 48, codes, sx, ws)
+    with pytest.raises(ValueError):
+        B.cat_transform_quant_asym(X, T, k, codes, sx, torch.zeros(n + 1), ws)
+    with pytest.raises(ValueError):
+        B.cat_transform_quant_full(X, T[:, :, :16].contiguous(), k, codes, sx, ws)
+    assert rec.calls == ["cat_transform_quant"]
+
+
+def test_binding_checks_cov_and_sqnr_buffer_sizes(fake_abi):
+    torch, rec = fake_abi
+    n, d, k = 8, 256, 32
+    X = torch.zeros((n, d), dtype=torch.bfloat16)
+    ws = torch.zeros(64, dtype=torch.uint8)
+    B.cat_cov_accumulate(X, torch.zeros((d, d)), B.CAT_COV_FULL, k, ws)
+    B.cat_cov_accumulate(X, torch.zeros((d // k, k, k)), B.CAT_COV_BLOCK_DIAG, k, ws)
+    # a block-diagonal accumulator passed in FULL mode would receive d*d floats
+    with pytest.raises(ValueError):
+        B.cat_cov_accumulate(X, torch.zeros((d // k, k, k)), B.CAT_COV_FULL, k, ws)
+    with pytest.raises(ValueError):
+        B.cat_cov_accumulate(X, torch.zeros((d, d)), B.CAT_COV_BLOCK_DIAG, k, ws)
+    y = torch.zeros(100)
+    B.cat_sqnr(y, y, ws, torch.zeros(3, dtype=torch.float64))
+    with pytest.raises(ValueError):
+        B.cat_sqnr(y, y, ws, torch.zeros(2, dtype=torch.float64))
+    assert rec.calls == ["cat_cov_accumulate", "cat_cov_accumulate", "cat_sqnr"]

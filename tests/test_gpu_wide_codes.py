@@ -1,5 +1,5 @@
 """Parity of the 6- and 8-bit widths (the W6A6 / W8A8 layers the paper
-compares CAT W4A4 against, Sec. 5) with the CPU oracle: transform+quant
+compares CAT W4A4 against, Sec. 4 "CAT Block Approximation" and the Fig. 6 caption) with the CPU oracle: transform+quant
 writing one int8 per code on every kernel path, the int8-code GEMM, and the
 whole chain's SQNR."""
 import numpy as np

@@ -7,7 +7,7 @@ benchmark and the smoke check take their inputs from here, so the two sides
 always see identical arrays.
 
 The five layer configurations stand in for the LLM linear layers the paper
-measures (Sec. 5, "Models"): shapes copy Llama-3-8B attention / MLP
+measures (Sec. 6, set-up; Sec. 3, layers of Llama and Qwen models): shapes copy Llama-3-8B attention / MLP
 projections and a 70B-class MLP, and the value structure copies what the
 paper describes for real activations -- heavy tails and outlier channels
 (Sec. 3, concentration analysis) and massive-activation tokens (Fig. 2

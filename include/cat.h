@@ -142,13 +142,22 @@ int cat_cov_accumulate(const void* X, int x_dtype, int64_t n, int64_t d,
  * Capture: the call may be captured into a HIP graph and replayed (it
  *          enqueues kernels only; a captured call also enqueues a one-thread
  *          kernel that renews the exchange tag for every replay).
- * The d = 4096, k = 128 bf16 path exchanges row maxima between
- * workgroups of the same launch with bounded waits.  If a wait ever runs
- * out (the launch's workgroups were kept from running together for
- * seconds), the tokens concerned get s_x = NaN and zero codes rather than a
- * wrong scale.
+ * The d = 4096, k = 128 bf16 path runs one persistent launch whose
+ * workgroups exchange row maxima through the workspace with bounded waits.
+ * Its grid never exceeds the device's resident capacity, so every wait ends
+ * once the launch has the device; work from other streams that holds CUs
+ * for seconds can still make a wait run out.  Then the tokens concerned get
+ * s_x = NaN and zero codes rather than a wrong scale, and the 32-bit word
+ * at byte offset cat_transform_quant_flag_offset(n, d, k) of the workspace
+ * is set to a non-zero value.  The library never clears that word: a
+ * caller that wants to check it zeroes it before the call and reads it
+ * after synchronising.
  */
 size_t cat_transform_quant_workspace_bytes(int64_t n, int64_t d, int64_t k);
+/* Byte offset, inside a workspace of cat_transform_quant_workspace_bytes
+ * (n, d, k) bytes, of the exchange timeout word described above (0 when the
+ * arguments are invalid). */
+size_t cat_transform_quant_flag_offset(int64_t n, int64_t d, int64_t k);
 int cat_transform_quant(const void* X, int x_dtype, int64_t n, int64_t d,
                         const void* T, int t_dtype, int64_t k, int bits,
                         uint8_t* codes, float* s_x, void* workspace,

@@ -41,7 +41,7 @@ CAT_MAX_BLOCK = 512
 # every symbol include/cat.h declares
 EXPORTED = (
     "cat_cov_workspace_bytes", "cat_cov_accumulate", "cat_transform_quant_workspace_bytes",
-    "cat_transform_quant",
+    "cat_transform_quant_flag_offset", "cat_transform_quant",
     "cat_w4a4_linear", "cat_int8_linear", "cat_transform_quant_asym", "cat_w4a4_linear_asym",
     "cat_weight_code_sums", "cat_sqnr_terms", "cat_transform_quant_full_workspace_bytes",
     "cat_transform_quant_full", "cat_full_hadamard_weights", "cat_sqnr_workspace_bytes", "cat_sqnr", "cat_build_transform",
@@ -79,6 +79,8 @@ def lib() -> ctypes.CDLL:
     L.cat_cov_accumulate.restype = _int
     L.cat_transform_quant_workspace_bytes.argtypes = [_i64, _i64, _i64]
     L.cat_transform_quant_workspace_bytes.restype = _sz
+    L.cat_transform_quant_flag_offset.argtypes = [_i64, _i64, _i64]
+    L.cat_transform_quant_flag_offset.restype = _sz
     L.cat_transform_quant.argtypes = [_vp, _int, _i64, _i64, _vp, _int, _i64, _int, _vp, _vp,
                                       _vp, _sz, _vp]
     L.cat_transform_quant.restype = _int
@@ -228,6 +230,11 @@ def cat_cov_accumulate(X, acc, mode: int = CAT_COV_FULL, k: int = 1, workspace=N
 
 def cat_transform_quant_workspace_bytes(n: int, d: int, k: int) -> int:
     return int(lib().cat_transform_quant_workspace_bytes(n, d, k))
+
+
+def cat_transform_quant_flag_offset(n: int, d: int, k: int) -> int:
+    """Byte offset of the exchange timeout word inside the workspace."""
+    return int(lib().cat_transform_quant_flag_offset(n, d, k))
 
 
 def cat_transform_quant(X, T, k: int, codes, s_x, workspace, bits: int = 4, stream=None):

@@ -86,6 +86,12 @@ extern "C" size_t cat_transform_quant_workspace_bytes(int64_t n, int64_t d, int6
     return catk::tq_workspace_bytes(n, d, k);
 }
 
+extern "C" size_t cat_transform_quant_flag_offset(int64_t n, int64_t d, int64_t k) {
+    (void)k;
+    if (n < 1 || d < 1) return 0;
+    return catk::tq_flag_offset_bytes(n, d);
+}
+
 extern "C" int cat_transform_quant(const void* X, int x_dtype, int64_t n, int64_t d, const void* T,
                                    int t_dtype, int64_t k, int bits, uint8_t* codes, float* s_x,
                                    void* workspace, size_t workspace_bytes, void* stream) {

@@ -612,7 +612,7 @@ __global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
 //              (held in registers) with tokens 32 (w % 2) .. + 31 of the
 //              tile, read from LDS;
 //   waves 4-5  copy: stream token tiles into an 8-stage LDS ring with
-//              global_load_lds_dwordx4, seven tiles ahead;
+//              global_load_lds_dwordx4, kFqAhead tiles ahead;
 //   wave 6     gather: reads the per-token maxima other workgroups published;
 //   wave 7     publish: writes this workgroup's per-token maxima.
 // Each wave issues one kind of vector-memory traffic only, so every wait is
@@ -628,9 +628,9 @@ __global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
 // per level instead of 16 KiB for all P words).  A word is
 // (call tag << 32) | maximum bits written with one store, so a reader sees
 // either an old word (another tag) or the whole new one and the workspace
-// needs no clearing between calls.  Tags have bit 31 set, which no
-// absolute-value float pattern has, so 32-bit maxima left by the two-pass
-// path never look published either.  Eager calls take the tag from a host
+// needs no clearing between calls.  Tags have bit 31 set; the two-pass
+// paths keep their words in a region of the workspace of their own, so
+// nothing they leave behind is read here.  Eager calls take the tag from a host
 // counter; a call captured into a graph takes it from a word a one-thread
 // kernel advances before every replay (see launch_tq_fused).  P(j, t) lives at
 // ((t / 16) * 32 + j) * 16 + t % 16 (16 tokens of a block fill one 128-byte
@@ -664,7 +664,15 @@ constexpr int kFqStage = kFqTT * kFqU;          // units per stage (16 KiB)
 constexpr int kFqCopyOps = kFqStage / (kFqCopy * kWave);   // copies per lane per tile
 constexpr int kFqBlocks = 32;                   // d / 128
 constexpr int kFqLag = 3;                       // tile s is quantized in step s + kFqLag
-static_assert(kFqCopyOps * (kFqStages - 2) < 64, "copies in flight must fit the vmcnt range");
+// Copies in flight per CU (kFqAhead tiles of 16 KiB).  Every load of this
+// CU, the exchange polls included, queues behind them: under a 6 TB/s
+// stream a store/poll round trip between two CUs of one XCD measures 3.1 us
+// with 16 KiB in flight per CU, 4.6 us with 32 KiB and 6 us with 64 KiB,
+// while the stream itself already reaches 5.9-6.1 TB/s at 16-32 KiB.  Three
+// tiles ahead (48 KiB) was 41.8 us per call against 43.6 us for seven.
+constexpr int kFqAhead = 3;
+static_assert(kFqCopyOps * kFqAhead < 64, "copies in flight must fit the vmcnt range");
+static_assert(kFqAhead < kFqStages, "a stage is refilled only after its tile is multiplied");
 static_assert(kFqTT == 2 * kFqBlocks, "each workgroup reduces two tokens of a tile");
 
 struct TqFusedWs {
@@ -894,15 +902,16 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
                 dma16(base, static_cast<uint32_t>((rr * d + u * 8) * 2), lds_addr(&ring[st][first]));
             }
         };
-        for (int64_t it = 0; it < nt && it < kFqStages - 1; ++it) issue(it);
+        for (int64_t it = 0; it < nt && it < kFqAhead; ++it) issue(it);
         for (int64_t it = 0; it < nsteps; ++it) {
             if (it < nt) {
-                const int64_t hi_t = nt - 1 < it + kFqStages - 2 ? nt - 1 : it + kFqStages - 2;
+                const int64_t hi_t = nt - 1 < it + kFqAhead - 1 ? nt - 1 : it + kFqAhead - 1;
                 fq_wait_copies(static_cast<int>(hi_t - it));
             }
             lds_barrier();                                            // A
-            // the stage of tile it + 7 held tile it - 1, read before A
-            if (it + kFqStages - 1 < nt) issue(it + kFqStages - 1);
+            // the stage of tile it + kFqAhead last held a tile multiplied
+            // before A
+            if (it + kFqAhead < nt) issue(it + kFqAhead);
             lds_barrier();                                            // F
         }
         return;
@@ -1006,19 +1015,25 @@ hipError_t launch_tq_ring(const uint16_t* X, int64_t n, int64_t d, const uint16_
     return hipGetLastError();
 }
 
-// Workspace layout (bytes): [0, P) per-token words (two-pass path: one
-// 32-bit running maximum per token; single-pass path: d/128 64-bit tagged
-// block maxima and one tagged row maximum per token, n rounded up to 16,
-// P = 8 n' (max(1, d / 128) + 1)), then a 256-byte tail: the 32-bit
-// timeout flag at +0 and the device-side tag of captured calls at +64.
+// Workspace layout (bytes): [0, P) the single-pass exchange words (d/128
+// 64-bit tagged block maxima and one tagged row maximum per token, n
+// rounded up to 16, P = 8 n' (max(1, d / 128) + 1)); then a 256-byte tail:
+// the 32-bit timeout flag at +0 and the device-side tag of captured calls
+// at +64; then 8 n bytes for the two-pass paths (one 32-bit running
+// maximum per token, or the asymmetric path's two 32-bit keys per token).
+// The two regions never overlap, so words one path leaves behind are never
+// read by the other: the asymmetric keys can have bit 31 set and could
+// otherwise pass for a tagged word.
 static int64_t tq_nbj_max(int64_t d) { return d / 128 > 1 ? d / 128 : 1; }
 static size_t tq_flag_offset(int64_t n, int64_t d) {
     return static_cast<size_t>((n + 15) / 16 * 16 * 8 * (tq_nbj_max(d) + 1));
 }
+static size_t tq_twopass_offset(int64_t n, int64_t d) { return tq_flag_offset(n, d) + 256; }
+size_t tq_flag_offset_bytes(int64_t n, int64_t d) { return tq_flag_offset(n, d); }
 size_t tq_workspace_bytes(int64_t n, int64_t d, int64_t k) {
     (void)k;
     if (n < 1) return 0;
-    return tq_flag_offset(n, d) + 256;
+    return tq_twopass_offset(n, d) + static_cast<size_t>(n) * 8;
 }
 
 static uint32_t next_tq_tag() {
@@ -1123,6 +1138,8 @@ static hipError_t launch_tq_qm(const void* X, int x_bf16, int64_t n, int64_t d, 
                                                  launched);
         if (e != hipSuccess || launched) return e;
     }
+    amax_ws = reinterpret_cast<uint32_t*>(reinterpret_cast<uint8_t*>(amax_ws) +
+                                          tq_twopass_offset(n, d));
     hipLaunchKernelGGL(fill_zero_u32_kernel, dim3(static_cast<uint32_t>((n + 255) / 256)),
                        dim3(256), 0, stream, amax_ws, n);
     hipError_t err = hipGetLastError();
@@ -1186,6 +1203,7 @@ hipError_t launch_transform_quant_asym(const void* X, int x_bf16, int64_t n, int
                                        const void* T, int t_bf16, int64_t k, uint8_t* codes,
                                        float* s_x, float* zmin_x, uint32_t* ws,
                                        hipStream_t stream) {
+    ws = reinterpret_cast<uint32_t*>(reinterpret_cast<uint8_t*>(ws) + tq_twopass_offset(n, d));
     hipLaunchKernelGGL(fill_zero_u32_kernel, dim3(static_cast<uint32_t>((2 * n + 255) / 256)),
                        dim3(256), 0, stream, ws, 2 * n);
     hipError_t err = hipGetLastError();

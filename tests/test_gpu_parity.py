@@ -286,6 +286,21 @@ def test_transform_quant_single_pass(n):
         assert s[n // 2] == 0 and not codes[n // 2].any()
 
 
+@pytest.mark.parametrize("d,n", [(128, 777), (1024, 65), (2048, 1000), (8192, 300), (8192, 4097)])
+def test_transform_quant_k128_other_widths(d, n):
+    # k = 128 at widths other than the single-pass one (two passes), from
+    # one 128-channel block to the stress layer's 8192
+    say(f"tq k=128 d={d} n={n}")
+    rng = np.random.default_rng(d + n)
+    X = o.round_storage(rng.standard_normal((n, d)) * np.exp(rng.standard_normal(d)), "bf16")
+    X[n // 3] = 0.0
+    T = _rand_T(d, 128, seed=d)
+    codes, s = _tq_gpu(X, T, 128, "bf16", "bf16")
+    _, _, s_or = check_codes(codes, X, T, label=f"k=128 d={d} n={n}")
+    _check_scales(s, s_or, f"k=128 d={d} n={n}")
+    assert s[n // 3] == 0 and not codes[n // 3].any()
+
+
 def test_transform_quant_single_pass_mlp_up_full_size():
     # 8192 tokens x 4096 channels, the shape and launch the benchmark times
     say("tq single pass mlp_up 8192 x 4096")
@@ -322,9 +337,10 @@ def test_transform_quant_workspace_reuse_across_paths():
         if i == 0:
             first = (c, s)
     assert np.array_equal(first[0], c) and np.array_equal(first[1], s)
-    # the single-pass kernel's bounded waits record a timeout in the first
-    # word of the workspace's last 256 bytes; none may have happened
-    assert int(host(ws[wsb - 256:wsb - 252].view(torch.int32))[0]) == 0
+    # the single-pass kernel's bounded waits record a timeout in the word at
+    # cat_transform_quant_flag_offset; none may have happened
+    fo = cat.cat_transform_quant_flag_offset(n, 4096, 128)
+    assert int(host(ws[fo:fo + 4].view(torch.int32))[0]) == 0
 
 
 def test_transform_quant_graph_replays_see_fresh_inputs():
@@ -342,7 +358,8 @@ def test_transform_quant_graph_replays_see_fresh_inputs():
     dX = dev(Xs[0], "bf16")
     wsb = cat.cat_transform_quant_workspace_bytes(n, d, k)
     ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
-    ws[wsb - 256:wsb - 252].zero_()   # only the timeout word, to read it afterwards
+    fo = cat.cat_transform_quant_flag_offset(n, d, k)
+    ws[fo:fo + 4].zero_()             # only the timeout word, to read it afterwards
     codes = torch.empty((n, d // 2), dtype=torch.uint8, device="cuda")
     s_x = torch.empty(n, dtype=torch.float32, device="cuda")
     cat.cat_transform_quant(dX, dT, k, codes, s_x, ws)      # eager warm-up
@@ -364,7 +381,7 @@ def test_transform_quant_graph_replays_see_fresh_inputs():
         cat.cat_transform_quant(dX, dT, k, codes_e, s_x_e, ws)   # eager, same workspace
         torch.cuda.synchronize()
         assert np.array_equal(host(codes_e), c) and np.array_equal(host(s_x_e), sx)
-    assert int(host(ws[wsb - 256:wsb - 252].view(torch.int32))[0]) == 0
+    assert int(host(ws[fo:fo + 4].view(torch.int32))[0]) == 0
 
 
 # ------------------------------------------------------- second moment

@@ -163,6 +163,25 @@ int cat_transform_quant(const void* X, int x_dtype, int64_t n, int64_t d,
                         uint8_t* codes, float* s_x, void* workspace,
                         size_t workspace_bytes, void* stream);
 
+/* Allocation-free cat_transform_quant, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  Same arguments, results and errors as
+ * cat_transform_quant without the workspace: its scratch is a fixed array
+ * of cat_transform_quant_noalloc_max_bytes() bytes (16 MiB) that the
+ * library holds on each device it runs on, from its first use there until
+ * the process ends.  The call allocates nothing and calls no allocating
+ * routine.  A call whose cat_transform_quant_workspace_bytes(n, d, k)
+ * exceeds that size returns CAT_ERR_UNSUPPORTED before touching the device
+ * (8192 x 14336 and 16384 x 8192 bf16 inputs fit).  All calls on one GPU
+ * share that GPU's array, which keeps the last call's contents; calls that
+ * overlap on one GPU (other streams, other threads) race and must not be
+ * issued.  The exchange timeout word lives in that array and is not
+ * reported (a timed-out wait still yields NaN scales). */
+size_t cat_transform_quant_noalloc_max_bytes(void);
+int cat_transform_quant_noalloc(const void* X, int x_dtype, int64_t n, int64_t d,
+                                const void* T, int t_dtype, int64_t k, int bits,
+                                uint8_t* codes, float* s_x, void* stream);
+
 /* ------------------------------------------------------------------ (3)
  * W4A4 integer GEMM with dequantization (Sec. 3, eq. 5:
  * Q(W T^-1) Q(T x)).

@@ -41,7 +41,8 @@ CAT_MAX_BLOCK = 512
 # every symbol include/cat.h declares
 EXPORTED = (
     "cat_cov_workspace_bytes", "cat_cov_accumulate", "cat_transform_quant_workspace_bytes",
-    "cat_transform_quant_flag_offset", "cat_transform_quant",
+    "cat_transform_quant_flag_offset", "cat_transform_quant", "cat_transform_quant_noalloc_max_bytes",
+    "cat_transform_quant_noalloc",
     "cat_w4a4_linear", "cat_int8_linear", "cat_transform_quant_asym", "cat_w4a4_linear_asym",
     "cat_weight_code_sums", "cat_sqnr_terms", "cat_transform_quant_full_workspace_bytes",
     "cat_transform_quant_full", "cat_full_hadamard_weights", "cat_sqnr_workspace_bytes", "cat_sqnr", "cat_build_transform",
@@ -84,6 +85,11 @@ def lib() -> ctypes.CDLL:
     L.cat_transform_quant.argtypes = [_vp, _int, _i64, _i64, _vp, _int, _i64, _int, _vp, _vp,
                                       _vp, _sz, _vp]
     L.cat_transform_quant.restype = _int
+    L.cat_transform_quant_noalloc_max_bytes.argtypes = []
+    L.cat_transform_quant_noalloc_max_bytes.restype = _sz
+    L.cat_transform_quant_noalloc.argtypes = [_vp, _int, _i64, _i64, _vp, _int, _i64, _int, _vp,
+                                              _vp, _vp]
+    L.cat_transform_quant_noalloc.restype = _int
     L.cat_w4a4_linear.argtypes = [_vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp]
     L.cat_w4a4_linear.restype = _int
     L.cat_int8_linear.argtypes = [_vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp]
@@ -274,6 +280,30 @@ def _gemm_shapes(codes_x, s_x, codes_w, s_w, y_tilde, acc_out):
     if acc_out is not None:
         _shape(acc_out, (n, d_out), "acc_out")
     return n, row, d_out
+
+
+def cat_transform_quant_noalloc_max_bytes() -> int:
+    return int(lib().cat_transform_quant_noalloc_max_bytes())
+
+
+def cat_transform_quant_noalloc(X, T, k: int, codes, s_x, bits: int = 4, stream=None):
+    """cat_transform_quant with the library's own per-device scratch instead
+    of a caller workspace (no allocation on the call)."""
+    torch = _torch()
+    px = _dev_ptr(X, "X", (torch.bfloat16, torch.float32))
+    pt = _dev_ptr(T, "T", (torch.bfloat16, torch.float32))
+    pc = _dev_ptr(codes, "codes", (torch.uint8,) if bits == 4 else (torch.int8,))
+    ps = _dev_ptr(s_x, "s_x", (torch.float32,))
+    if X.dim() != 2:
+        raise ValueError("X must be [n, d]")
+    n, d = X.shape
+    if tuple(codes.shape) != (n, d // 2 if bits == 4 else d):
+        raise ValueError(f"codes must be [{n}, {d // 2 if bits == 4 else d}] for bits={bits}")
+    _t_blocks(T, d, k)
+    _numel(s_x, n, "s_x")
+    _check("cat_transform_quant_noalloc",
+           lib().cat_transform_quant_noalloc(px, _dtype_code(X), n, d, pt, _dtype_code(T), k, bits,
+                                             pc, ps, _stream_ptr(stream)))
 
 
 def cat_w4a4_linear(codes_x, s_x, codes_w, s_w, y_tilde, acc_out=None, stream=None):

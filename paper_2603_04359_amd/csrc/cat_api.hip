@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <exception>
+#include <mutex>
 #include <string>
 
 #include "cat_internal.h"
@@ -121,6 +122,67 @@ extern "C" int cat_transform_quant(const void* X, int x_dtype, int64_t n, int64_
             static_cast<uint32_t*>(workspace), static_cast<hipStream_t>(stream));
         if (err != hipSuccess) return hip_fail(fn, err);
         return CAT_OK;
+    } catch (const std::exception& e) {
+        return fail(CAT_ERR_INTERNAL, std::string(fn) + ": " + e.what());
+    } catch (...) {
+        return fail(CAT_ERR_INTERNAL, std::string(fn) + ": unknown error");
+    }
+}
+
+// ------------------------------------------------ allocation-free variant
+// cat_transform_quant with its workspace in this file-scope device array,
+// for callers that cannot allocate (code under graph capture, serving
+// loops).  Each GPU holds its own copy until the process ends; its address
+// on a device is looked up once, with that device current, and kept, and
+// host code only ever hands that address on.  The transform+quant paths
+// clear what they need cleared with their own kernels (the two-pass maxima)
+// or need nothing cleared (the tagged single-pass words), so the contents a
+// previous call left are harmless; calls that overlap on one GPU race.
+constexpr size_t kScratchBytes = size_t{16} << 20;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int scratch_on_current_device(const char* where, void** out) {
+    int dev = 0;
+    hipError_t err = hipGetDevice(&dev);
+    if (err != hipSuccess) return hip_fail(where, err);
+    if (dev < 0 || dev >= kMaxDevices)
+        return fail(CAT_ERR_UNSUPPORTED, std::string(where) + ": device index out of range");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (err != hipSuccess) return hip_fail(where, err);
+        if (!p) return fail(CAT_ERR_HIP, std::string(where) + ": no scratch address");
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return CAT_OK;
+}
+}  // namespace
+
+extern "C" size_t cat_transform_quant_noalloc_max_bytes(void) { return kScratchBytes; }
+
+extern "C" int cat_transform_quant_noalloc(const void* X, int x_dtype, int64_t n, int64_t d,
+                                           const void* T, int t_dtype, int64_t k, int bits,
+                                           uint8_t* codes, float* s_x, void* stream) {
+    const char* fn = "cat_transform_quant_noalloc";
+    try {
+        const size_t need = cat_transform_quant_workspace_bytes(n, d, k);
+        if (need > kScratchBytes)
+            return fail(CAT_ERR_UNSUPPORTED,
+                        std::string(fn) + ": needs " + std::to_string(need) +
+                            " bytes of scratch, more than the " + std::to_string(kScratchBytes) +
+                            " the library holds per device");
+        if (int rc = require_device(fn)) return rc;
+        void* ws = nullptr;
+        if (int rc = scratch_on_current_device(fn, &ws)) return rc;
+        return cat_transform_quant(X, x_dtype, n, d, T, t_dtype, k, bits, codes, s_x, ws,
+                                   kScratchBytes, stream);
     } catch (const std::exception& e) {
         return fail(CAT_ERR_INTERNAL, std::string(fn) + ": " + e.what());
     } catch (...) {

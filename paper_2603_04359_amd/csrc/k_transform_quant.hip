@@ -391,11 +391,21 @@ __global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
     __shared__ __attribute__((aligned(16))) u32x4 ring[2][C::STAGE];
     __shared__ uint32_t red[ASYM ? 8 : 4][C::TT];
 
-    const int64_t nbj = (d / K) * C::NCHUNK;
-    const int64_t bj = blockIdx.x % nbj;
-    const int64_t r0 = blockIdx.x / nbj;
-    const int64_t b = bj / C::NCHUNK;
-    const int jc = static_cast<int>(bj % C::NCHUNK);
+    // workgroup -> (block, tile row) unit and 128-row chunk; the NCHUNK
+    // workgroups of a unit are 8 apart in launch order, so round-robin
+    // dispatch puts them on one XCD and the later reads of each X tile hit
+    // that XCD's L2
+    const int64_t nb = d / K;
+    int64_t unit = blockIdx.x;
+    int jc = 0;
+    if constexpr (C::NCHUNK > 1) {
+        const int64_t sq = blockIdx.x >> 3;
+        jc = static_cast<int>(sq % C::NCHUNK);
+        unit = (sq / C::NCHUNK) * 8 + (blockIdx.x & 7);
+    }
+    if (unit >= nb * R) return;
+    const int64_t b = unit % nb;
+    const int64_t r0 = unit / nb;
     const int64_t ntiles = (n + C::TT - 1) / C::TT;
     if (r0 >= ntiles) return;
 
@@ -989,23 +999,355 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
     }
 }
 
+// ------------------------------------------------ group two-pass path
+// bf16, k in {32, 64, 128, 256} with d a multiple of 256.  One persistent
+// workgroup per CU owns a group of 256 channels (one or more whole blocks)
+// for the token tiles r, r + R, ...  (The structure also takes 256-row
+// halves of a 512-block, the two halves of a block 8 apart in launch order
+// so that they share an XCD's L2; at k = 512 the 32 rows x 512 columns of
+// T a wave holds do not fit the registers that three waves per SIMD leave,
+// so that case runs on the ring kernels.)  Ten waves with fixed roles:
+//   waves 0-7  compute: wave w holds 32 rows of T (channels 32 w .. + 31 of
+//              the group, in the fq_row order, so each lane ends up with 16
+//              consecutive output channels) in registers and multiplies
+//              them with every token of the tile, read from LDS;
+//   waves 8-9  copy: stream 32 KiB token tiles (64 tokens x 256 channels,
+//              or 32 x 512) into a 4-stage LDS ring, three tiles ahead,
+//              and in pass 2 the tile's finished row maxima beside them.
+// The copy waves issue nothing but copies, so their vmcnt waits are exact
+// while the compute waves' stores and atomics stay out of the count.
+// Pass 1 folds per-token maxima of all eight waves with LDS atomics; the
+// tile's maxima go to the global per-token words one step later (after the
+// next barrier), which needs no barrier of its own.
+constexpr int kTgCompute = 8;
+constexpr int kTgCopy = 2;
+constexpr int kTgThreads = (kTgCompute + kTgCopy) * kWave;
+constexpr int kTgStages = 4;
+constexpr int kTgAhead = kTgStages - 1;     // tiles in flight ahead of the one multiplied
+
+template <int K>
+struct TqGroup {
+    static constexpr int COLS = K > 256 ? K : 256;     // X channels per tile row
+    static constexpr int U = COLS / 8;                 // 16-byte units per token row
+    static constexpr int TT = K > 256 ? 32 : 64;       // tokens per tile
+    static constexpr int NSB = TT / 32;                // 32-token MFMA subtiles
+    static constexpr int STAGE = TT * U;               // 16-byte units per stage (32 KiB)
+    static constexpr int NS = K / 16;                  // 16-deep MFMA steps
+    static constexpr int NCHUNK = K > 256 ? K / 256 : 1;   // workgroups per column group
+    static constexpr int COPY_OPS = STAGE / (kTgCopy * kWave);
+    static_assert(STAGE % (kTgCopy * kWave) == 0, "copies split evenly");
+    static_assert(U >= 32, "swizzle spans 32 units");
+};
+
+// tile it has landed once at most `later` tiles issued after it are in flight
+template <int OPS>
+__device__ __forceinline__ void tg_wait_copies(int later) {
+    static_assert((kTgAhead - 1) * OPS < 64, "copies in flight must fit the vmcnt range");
+    if (later >= 2) wait_vmcnt<2 * OPS>();
+    else if (later == 1) wait_vmcnt<OPS>();
+    else wait_vmcnt<0>();
+}
+
+// Asymmetric INT4 codes of 16 consecutive channels: q = rint(clamp(fl(fl(z -
+// zmin) * inv), 0, 15)) (clamping first gives the same integer, as both
+// bounds are integers), stored as q - 8 = q ^ 8, channel 2m in the low
+// nibble of byte m.
+__device__ __forceinline__ u32x2 fq_quant16_asym(const f32x16& z, float zmin, float inv) {
+    uint32_t w[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        float u = (z[r] - zmin) * inv;
+        u = __builtin_amdgcn_fmed3f(u, 0.0f, 15.0f);
+        w[r] = __float_as_uint(u + 12582912.0f) ^ 8u;
+    }
+    u32x2 out;
+#pragma unroll
+    for (int hw = 0; hw < 2; ++hw) {
+        const uint32_t* v = w + 8 * hw;
+        const uint32_t ev = fq_bytes(v[0], v[2], v[4], v[6]);
+        const uint32_t od = fq_bytes(v[1], v[3], v[5], v[7]);
+        out[hw] = (ev & 0x0F0F0F0Fu) | ((od << 4) & 0xF0F0F0F0u);
+    }
+    return out;
+}
+
+// QUANT false: pass 1 (row maxima into ws[t], or for ASYM the max key into
+// ws[t] and the complemented min key into ws[n + t]).  QUANT true: pass 2
+// (codes and s_x from the finished words; for ASYM also zmin_x), or with
+// QM = 0 the transformed rows z themselves, fp32, into `codes` read as an
+// [n x d] float array (no pass 1 then).
+template <int K, bool QUANT, int QM, bool ASYM>
+__global__ __launch_bounds__(kTgThreads, 1) void tq_group_kernel(
+    const uint16_t* __restrict__ X, const uint16_t* __restrict__ T, int64_t n, int64_t d,
+    int64_t R, int64_t nunits, uint32_t* __restrict__ ws, uint8_t* __restrict__ codes,
+    float* __restrict__ s_x, float* __restrict__ zmin_x) {
+    using C = TqGroup<K>;
+    constexpr bool kWordsIn = QUANT && QM != 0;         // pass 2 reads the row words
+    constexpr int OPS = C::COPY_OPS + (kWordsIn ? 1 : 0);
+    __shared__ __attribute__((aligned(16))) u32x4 ring[kTgStages][C::STAGE];
+    __shared__ uint32_t words[kWordsIn ? kTgStages : 1][128];
+    __shared__ uint32_t red[QUANT ? 1 : 2][ASYM ? 2 : 1][C::TT];
+
+    // workgroup -> (unit, chunk); the NCHUNK workgroups of a unit are 8
+    // apart in launch order, so round-robin dispatch puts them on one XCD
+    int64_t unit = blockIdx.x;
+    int chunk = 0;
+    if constexpr (C::NCHUNK > 1) {
+        const int64_t s = blockIdx.x >> 3;
+        chunk = static_cast<int>(s % C::NCHUNK);
+        unit = (s / C::NCHUNK) * 8 + (blockIdx.x & 7);
+    }
+    if (unit >= nunits) return;
+    const int64_t ngroups = d / C::COLS;
+    const int64_t gb = unit % ngroups;                  // column group
+    const int64_t r0 = unit / ngroups;                  // first token tile
+    const int64_t ntiles = (n + C::TT - 1) / C::TT;
+    if (r0 >= ntiles) return;
+    const int64_t nt = (ntiles - r0 + R - 1) / R;       // tiles of this workgroup
+    const int64_t cb = gb * C::COLS;                    // first channel of the group
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wave = threadIdx.x / kWave;
+    auto tile0 = [&](int64_t it) { return (r0 + it * R) * C::TT; };
+
+    if (wave >= kTgCompute) {
+        // ---------------------------------------------------- copy waves
+        const int cw = wave - kTgCompute;
+        auto issue = [&](int64_t it) {
+            const int64_t t0 = tile0(it);
+            const uint16_t* base = X + t0 * d + cb;
+            const int64_t last = n - 1 - t0;            // rows past the end: never used
+            const int st = static_cast<int>(it % kTgStages);
+#pragma unroll
+            for (int q = 0; q < C::COPY_OPS; ++q) {
+                const int first = (q * kTgCopy + cw) * kWave;
+                const int sl = first + lane;
+                int rr = sl / C::U;
+                const int u = (sl % C::U) ^ (rr & 31);
+                rr = rr <= last ? rr : static_cast<int>(last);
+                dma16(base, static_cast<uint32_t>((rr * d + u * 8) * 2), lds_addr(&ring[st][first]));
+            }
+            if constexpr (kWordsIn) {
+                // symmetric: wave cw brings tokens 32 cw + (lane % 32) (64-token
+                // tiles); asymmetric: wave 0 the max keys, wave 1 the min keys
+                int j = ASYM ? lane : cw * 32 + (lane & 31);
+                if (j >= C::TT) j &= 31;
+                j = j <= last ? j : static_cast<int>(last);
+                const uint32_t* src = ws + (ASYM && cw ? n : 0) + t0;
+                dma4(src, static_cast<uint32_t>(j * 4), lds_addr(&words[st][cw * 64]));
+            }
+        };
+        for (int64_t it = 0; it < nt && it < kTgAhead; ++it) issue(it);
+        for (int64_t it = 0; it < nt; ++it) {
+            const int64_t later = nt - 1 - it;
+            tg_wait_copies<OPS>(static_cast<int>(later < kTgAhead - 1 ? later : kTgAhead - 1));
+            lds_barrier();
+            // the stage of tile it + kTgAhead last held tile it - 1, which
+            // every compute wave finished before this barrier
+            if (it + kTgAhead < nt) issue(it + kTgAhead);
+        }
+        if constexpr (!QUANT) lds_barrier();
+        return;
+    }
+
+    // ------------------------------------------------------ compute waves
+    const int l32 = lane & 31;
+    const int h = lane >> 5;
+    int64_t blk;                 // block of T this wave's rows belong to
+    int rb;                      // first row of the wave's 32 within the block
+    int xo;                      // first 16-byte unit of the block within the tile row
+    if constexpr (C::NCHUNK > 1) {
+        blk = gb;
+        rb = chunk * 256 + wave * 32;
+        xo = 0;
+    } else {
+        const int64_t c0 = cb + wave * 32;
+        blk = c0 / K;
+        rb = static_cast<int>(c0 % K);
+        xo = static_cast<int>((blk * K - cb) / 8);
+    }
+    const int64_t ch0 = blk * K + rb;    // first output channel of the wave
+    u32x4 tf[C::NS];
+    {
+        const u32x4* tg = reinterpret_cast<const u32x4*>(T + (blk * K + rb + fq_row(l32)) * K);
+#pragma unroll
+        for (int s = 0; s < C::NS; ++s) tf[s] = tg[2 * s + h];
+    }
+    if constexpr (!QUANT) {
+        for (int i = threadIdx.x; i < 2 * (ASYM ? 2 : 1) * C::TT; i += kTgCompute * kWave)
+            (&red[0][0][0])[i] = 0u;
+    }
+    // pass 1: fold the previous tile's LDS maxima into the global words
+    auto flush = [&](int64_t it) {
+        const int p = static_cast<int>(it & 1);
+        for (int j = lane; j < C::TT; j += kWave) {
+            const int64_t t = tile0(it) + j;
+            const uint32_t m = red[p][0][j];
+            red[p][0][j] = 0u;
+            if constexpr (ASYM) {
+                const uint32_t mn = red[p][1][j];
+                red[p][1][j] = 0u;
+                if (t < n) {
+                    atomicMax(ws + t, m);
+                    atomicMax(ws + n + t, mn);
+                }
+            } else {
+                if (t < n && m) atomicMax(ws + t, m);
+            }
+        }
+    };
+
+    for (int64_t it = 0; it < nt; ++it) {
+        lds_barrier();
+        if constexpr (!QUANT) {
+            if (wave == 0 && it > 0) flush(it - 1);
+        }
+        const int st = static_cast<int>(it % kTgStages);
+        f32x16 acc[C::NSB];
+#pragma unroll
+        for (int sb = 0; sb < C::NSB; ++sb) acc[sb] = f32x16{};
+#pragma unroll
+        for (int s = 0; s < C::NS; ++s) {
+#pragma unroll
+            for (int sb = 0; sb < C::NSB; ++sb) {
+                const int rr = sb * 32 + l32;
+                const u32x4 xf = ring[st][rr * C::U + ((xo + 2 * s + h) ^ (rr & 31))];
+                acc[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(tf[s]), as_bf16x8(xf),
+                                                                  acc[sb], 0, 0, 0);
+            }
+        }
+        // lane (token sb * 32 + l32, h) holds channels ch0 + 16 h .. + 15
+#pragma unroll
+        for (int sb = 0; sb < C::NSB; ++sb) {
+            const int j = sb * 32 + l32;
+            const int64_t t = tile0(it) + j;
+            const bool valid = t < n;
+            if constexpr (!QUANT && ASYM) {
+                uint32_t mx = 0, mn = 0;
+#pragma unroll
+                for (int q = 0; q < 16; ++q) {
+                    const uint32_t kq = fkey(acc[sb][q]);
+                    mx = max(mx, kq);
+                    mn = max(mn, ~kq);
+                }
+                mx = max(mx, static_cast<uint32_t>(__shfl_xor(static_cast<int>(mx), 32)));
+                mn = max(mn, static_cast<uint32_t>(__shfl_xor(static_cast<int>(mn), 32)));
+                if (h == 0) {
+                    atomicMax(&red[it & 1][0][j], mx);
+                    atomicMax(&red[it & 1][1][j], mn);
+                }
+            } else if constexpr (!QUANT) {
+                uint32_t m = fq_absmax16(acc[sb]);
+                m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), 32)));
+                if (h == 0) atomicMax(&red[it & 1][0][j], m);
+            } else if constexpr (QM == 0) {
+                if (valid) {
+                    float* zrow = reinterpret_cast<float*>(codes) + t * d + ch0 + 16 * h;
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        *reinterpret_cast<f32x4*>(zrow + 4 * q) =
+                            f32x4{acc[sb][4 * q], acc[sb][4 * q + 1], acc[sb][4 * q + 2],
+                                  acc[sb][4 * q + 3]};
+                }
+            } else if constexpr (ASYM) {
+                float zmin = 0.0f, s = 0.0f, inv = 0.0f;
+                asym_scale(words[st][j], words[st][64 + j], zmin, s, inv);
+                if (valid && h == 0 && wave == 0 && gb == 0 && chunk == 0) {
+                    s_x[t] = s;
+                    zmin_x[t] = zmin;
+                }
+                const u32x2 c = fq_quant16_asym(acc[sb], zmin, inv);
+                if (valid) *reinterpret_cast<u32x2*>(codes + t * (d / 2) + (ch0 + 16 * h) / 2) = c;
+            } else {
+                constexpr float qmax = static_cast<float>(QM);
+                const uint32_t wj = C::TT == 64 ? (j >> 5) * 64 + (j & 31) : j;
+                const float amax = __uint_as_float(words[st][wj]);
+                if (valid && h == 0 && wave == 0 && gb == 0 && chunk == 0)
+                    s_x[t] = __fdiv_rn(amax, qmax);
+                const float inv = amax > 0.0f ? __fdiv_rn(qmax, amax) : 0.0f;
+                if constexpr (QM == 7) {
+                    const u32x2 c = fq_quant16(acc[sb], inv);
+                    if (valid)
+                        *reinterpret_cast<u32x2*>(codes + t * (d / 2) + (ch0 + 16 * h) / 2) = c;
+                } else {
+                    const u32x4 c = fq_quant16_i8<QM>(acc[sb], inv);
+                    if (valid) *reinterpret_cast<u32x4*>(codes + t * d + ch0 + 16 * h) = c;
+                }
+            }
+        }
+    }
+    if constexpr (!QUANT) {
+        lds_barrier();
+        if (wave == 0) flush(nt - 1);
+    }
+}
+
 template <int K, int QM, bool ASYM = false>
-hipError_t launch_tq_ring(const uint16_t* X, int64_t n, int64_t d, const uint16_t* T,
-                          uint8_t* codes, float* s_x, uint32_t* ws, hipStream_t stream,
-                          float* zmin_x = nullptr) {
-    using C = TqRing<K>;
+hipError_t launch_tq_group(const uint16_t* X, int64_t n, int64_t d, const uint16_t* T,
+                           uint8_t* codes, float* s_x, uint32_t* ws, hipStream_t stream,
+                           float* zmin_x = nullptr, bool z_only = false) {
+    using C = TqGroup<K>;
     int dev = 0, cus = 0;
     hipError_t err = hipGetDevice(&dev);
     if (err != hipSuccess) return err;
     err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (err != hipSuccess) return err;
     const int64_t ntiles = (n + C::TT - 1) / C::TT;
-    const int64_t nbj = (d / K) * C::NCHUNK;
-    // about two resident workgroups per CU
-    int64_t R = (2 * static_cast<int64_t>(cus) + nbj - 1) / nbj;
+    const int64_t ngroups = d / C::COLS;
+    // one workgroup per CU: R token-tile rows per column group, rounded
+    // down so that every workgroup is resident at once
+    int64_t R = (static_cast<int64_t>(cus) / C::NCHUNK) / ngroups;
     if (R > ntiles) R = ntiles;
     if (R < 1) R = 1;
-    const int64_t grid = nbj * R;
+    const int64_t nunits = ngroups * R;
+    const int64_t grid = C::NCHUNK > 1 ? (nunits + 7) / 8 * 8 * C::NCHUNK : nunits;
+    if (z_only) {
+        hipLaunchKernelGGL((tq_group_kernel<K, true, 0, false>), dim3(static_cast<uint32_t>(grid)),
+                           dim3(kTgThreads), 0, stream, X, T, n, d, R, nunits, ws, codes, s_x,
+                           zmin_x);
+        return hipGetLastError();
+    }
+    hipLaunchKernelGGL((tq_group_kernel<K, false, 7, ASYM>), dim3(static_cast<uint32_t>(grid)),
+                       dim3(kTgThreads), 0, stream, X, T, n, d, R, nunits, ws, codes, s_x, zmin_x);
+    err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    hipLaunchKernelGGL((tq_group_kernel<K, true, QM, ASYM>), dim3(static_cast<uint32_t>(grid)),
+                       dim3(kTgThreads), 0, stream, X, T, n, d, R, nunits, ws, codes, s_x, zmin_x);
+    return hipGetLastError();
+}
+
+// The group kernels take bf16 k in {32, 64, 128, 256} when d is a multiple
+// of 256.
+static bool tq_group_fits(int64_t d, int64_t k) {
+    return (k == 32 || k == 64 || k == 128 || k == 256) && d % 256 == 0;
+}
+
+// Grid of the ring kernels: two resident workgroups per CU, R token-tile
+// rows per block rounded down so that every workgroup is resident at once
+// (a second round of workgroups would double the time); with NCHUNK > 1
+// the units are padded to a multiple of 8 (see the kernel's mapping).
+template <int K>
+static int64_t tq_ring_grid(int64_t n, int64_t d, int cus, int64_t& R) {
+    using C = TqRing<K>;
+    const int64_t ntiles = (n + C::TT - 1) / C::TT;
+    const int64_t nb = d / K;
+    R = (2 * static_cast<int64_t>(cus) / C::NCHUNK) / nb;
+    if (R > ntiles) R = ntiles;
+    if (R < 1) R = 1;
+    const int64_t units = nb * R;
+    return C::NCHUNK > 1 ? (units + 7) / 8 * 8 * C::NCHUNK : units;
+}
+
+template <int K, int QM, bool ASYM = false>
+hipError_t launch_tq_ring(const uint16_t* X, int64_t n, int64_t d, const uint16_t* T,
+                          uint8_t* codes, float* s_x, uint32_t* ws, hipStream_t stream,
+                          float* zmin_x = nullptr) {
+    int dev = 0, cus = 0;
+    hipError_t err = hipGetDevice(&dev);
+    if (err != hipSuccess) return err;
+    err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (err != hipSuccess) return err;
+    int64_t R = 0;
+    const int64_t grid = tq_ring_grid<K>(n, d, cus, R);
     hipLaunchKernelGGL((tq_ring_kernel<K, false, 7, ASYM>), dim3(static_cast<uint32_t>(grid)),
                        dim3(kTqThreads), 0, stream, X, T, n, d, R, ws, codes, s_x, zmin_x);
     err = hipGetLastError();
@@ -1144,6 +1486,17 @@ static hipError_t launch_tq_qm(const void* X, int x_bf16, int64_t n, int64_t d, 
                        dim3(256), 0, stream, amax_ws, n);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
+    if (x_bf16 && t_bf16 && tq_group_fits(d, k)) {
+        const uint16_t* Xb = static_cast<const uint16_t*>(X);
+        const uint16_t* Tb = static_cast<const uint16_t*>(T);
+        switch (k) {
+            case 32: return launch_tq_group<32, QM>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
+            case 64: return launch_tq_group<64, QM>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
+            case 128: return launch_tq_group<128, QM>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
+            case 256: return launch_tq_group<256, QM>(Xb, n, d, Tb, codes, s_x, amax_ws, stream);
+            default: break;
+        }
+    }
     if (x_bf16 && t_bf16 && k >= 32) {
         const uint16_t* Xb = static_cast<const uint16_t*>(X);
         const uint16_t* Tb = static_cast<const uint16_t*>(T);
@@ -1208,6 +1561,17 @@ hipError_t launch_transform_quant_asym(const void* X, int x_bf16, int64_t n, int
                        dim3(256), 0, stream, ws, 2 * n);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
+    if (x_bf16 && t_bf16 && tq_group_fits(d, k)) {
+        const uint16_t* Xb = static_cast<const uint16_t*>(X);
+        const uint16_t* Tb = static_cast<const uint16_t*>(T);
+        switch (k) {
+            case 32: return launch_tq_group<32, 7, true>(Xb, n, d, Tb, codes, s_x, ws, stream, zmin_x);
+            case 64: return launch_tq_group<64, 7, true>(Xb, n, d, Tb, codes, s_x, ws, stream, zmin_x);
+            case 128: return launch_tq_group<128, 7, true>(Xb, n, d, Tb, codes, s_x, ws, stream, zmin_x);
+            case 256: return launch_tq_group<256, 7, true>(Xb, n, d, Tb, codes, s_x, ws, stream, zmin_x);
+            default: break;
+        }
+    }
     if (x_bf16 && t_bf16) {
         const uint16_t* Xb = static_cast<const uint16_t*>(X);
         const uint16_t* Tb = static_cast<const uint16_t*>(T);
@@ -1351,19 +1715,19 @@ hipError_t launch_transform_quant_full(const void* X, int64_t n, int64_t d, cons
     if (err != hipSuccess) return err;
     auto zpass = [&](auto kc) -> hipError_t {
         constexpr int K = decltype(kc)::value;
-        using C = TqRing<K>;
-        const int64_t ntiles = (n + C::TT - 1) / C::TT;
-        const int64_t nbj = (d / K) * C::NCHUNK;
-        int64_t R = (2 * static_cast<int64_t>(cus) + nbj - 1) / nbj;
-        if (R > ntiles) R = ntiles;
-        if (R < 1) R = 1;
-        hipLaunchKernelGGL((tq_ring_kernel<K, true, 0, false>), dim3(static_cast<uint32_t>(nbj * R)),
+        int64_t R = 0;
+        const int64_t grid = tq_ring_grid<K>(n, d, cus, R);
+        hipLaunchKernelGGL((tq_ring_kernel<K, true, 0, false>), dim3(static_cast<uint32_t>(grid)),
                            dim3(kTqThreads), 0, stream, Xb, Tb, n, d, R, nullptr, zb, nullptr,
                            nullptr);
         return hipGetLastError();
     };
-    err = k == 128 ? zpass(std::integral_constant<int, 128>{})
-                   : zpass(std::integral_constant<int, 256>{});
+    if (tq_group_fits(d, k))
+        err = k == 128 ? launch_tq_group<128, 0>(Xb, n, d, Tb, zb, nullptr, nullptr, stream, nullptr, true)
+                       : launch_tq_group<256, 0>(Xb, n, d, Tb, zb, nullptr, nullptr, stream, nullptr, true);
+    else
+        err = k == 128 ? zpass(std::integral_constant<int, 128>{})
+                       : zpass(std::integral_constant<int, 256>{});
     if (err != hipSuccess) return err;
     const dim3 grid(static_cast<uint32_t>(n)), block(static_cast<uint32_t>(k));
     switch (d / k) {

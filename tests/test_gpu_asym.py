@@ -55,11 +55,12 @@ def _check_asym(q, s, m, X, T, label):
     say(f"  {label}: codes {q.size}, tie mismatches {nm}")
 
 
-# ring kernels (bf16, k = 128 at the single-pass width too, 256, 512) and
-# vector-ALU kernels (k = 64 bf16, fp32)
+# bf16 group kernels (k <= 256, d a multiple of 256), ring kernels (k = 512,
+# and k = 128 at d = 640) and vector-ALU kernels (fp32)
 @pytest.mark.parametrize("d,k,n,x_dtype,t_dtype", [
     (4096, 128, 300, "bf16", "bf16"), (1024, 256, 129, "bf16", "bf16"),
     (1024, 512, 65, "bf16", "bf16"), (512, 64, 70, "bf16", "bf16"), (256, 32, 33, "f32", "f32"),
+    (14336, 256, 130, "bf16", "bf16"), (768, 32, 65, "bf16", "bf16"), (640, 128, 97, "bf16", "bf16"),
 ])
 def test_transform_quant_asym_matches_oracle(d, k, n, x_dtype, t_dtype):
     say(f"tq asym d={d} k={k} n={n} {x_dtype}/{t_dtype}")

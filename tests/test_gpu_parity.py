@@ -301,6 +301,28 @@ def test_transform_quant_k128_other_widths(d, n):
     assert s[n // 3] == 0 and not codes[n // 3].any()
 
 
+@pytest.mark.parametrize("d,k,n", [
+    (14336, 256, 300), (8192, 256, 97), (768, 32, 65), (256, 32, 1), (2048, 64, 130),
+    (640, 128, 300), (384, 64, 129), (2048, 512, 1000), (4096, 512, 33),
+])
+def test_transform_quant_two_pass_shapes(d, k, n):
+    # bf16 two-pass paths: 256-channel group kernels (k <= 256, d a multiple
+    # of 256; the mlp_down width with a ragged last tile), the ring and
+    # small-block kernels they leave to (d = 640, 384), and k = 512 ring
+    # workgroups paired on one XCD
+    say(f"tq two-pass d={d} k={k} n={n}")
+    rng = np.random.default_rng(3 * d + k + n)
+    X = o.round_storage(rng.standard_normal((n, d)) * np.exp(rng.standard_normal(d)), "bf16")
+    if n > 2:
+        X[n // 2] = 0.0
+    T = _rand_T(d, k, seed=d + k)
+    codes, s = _tq_gpu(X, T, k, "bf16", "bf16")
+    _, _, s_or = check_codes(codes, X, T, label=f"two-pass d={d} k={k} n={n}")
+    _check_scales(s, s_or, f"two-pass d={d} k={k} n={n}")
+    if n > 2:
+        assert s[n // 2] == 0 and not codes[n // 2].any()
+
+
 def test_transform_quant_single_pass_mlp_up_full_size():
     # 8192 tokens x 4096 channels, the shape and launch the benchmark times
     say("tq single pass mlp_up 8192 x 4096")

@@ -39,12 +39,13 @@ def _rand_T(d, k, seed, dtype):
 
 
 # (d, k, n, x_dtype, t_dtype): the single-pass kernel (d = 4096, k = 128,
-# bf16), the two-pass ring kernels (k = 128 at another width, 256, 512),
-# the small-block MFMA kernels (k = 32, 64) and the vector-ALU kernels
-# (fp32, k = 16)
+# bf16), the two-pass group kernels (k <= 256 with d a multiple of 256),
+# the ring kernels (k = 512; k = 128 at d = 640), the small-block MFMA
+# kernel (k = 64 at d = 384) and the vector-ALU kernels (fp32, k = 16)
 PATHS = [(4096, 128, 300, "bf16", "bf16"), (1024, 128, 257, "bf16", "bf16"),
          (1024, 256, 129, "bf16", "bf16"), (1024, 512, 65, "bf16", "bf16"),
          (512, 64, 200, "bf16", "bf16"), (512, 32, 131, "bf16", "bf16"),
+         (640, 128, 77, "bf16", "bf16"), (384, 64, 90, "bf16", "bf16"),
          (256, 32, 70, "f32", "f32"), (256, 16, 33, "bf16", "bf16")]
 
 

@@ -1002,42 +1002,33 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
 // ------------------------------------------------ group two-pass path
 // bf16, k in {32, 64, 128, 256} with d a multiple of 256.  One persistent
 // workgroup per CU owns a group of 256 channels (one or more whole blocks)
-// for the token tiles r, r + R, ...  (The structure also takes 256-row
-// halves of a 512-block, the two halves of a block 8 apart in launch order
-// so that they share an XCD's L2; at k = 512 the 32 rows x 512 columns of
-// T a wave holds do not fit the registers that three waves per SIMD leave,
-// so that case runs on the ring kernels.)  Ten waves with fixed roles:
-//   waves 0-7  compute: wave w holds 32 rows of T (channels 32 w .. + 31 of
-//              the group, in the fq_row order, so each lane ends up with 16
-//              consecutive output channels) in registers and multiplies
-//              them with every token of the tile, read from LDS;
-//   waves 8-9  copy: stream 32 KiB token tiles (64 tokens x 256 channels,
-//              or 32 x 512) into a 4-stage LDS ring, three tiles ahead,
-//              and in pass 2 the tile's finished row maxima beside them.
+// for the token tiles r, r + R, ...  Six waves with fixed roles:
+//   waves 0-3  compute: wave w holds rows 64 w .. + 63 of the group's T
+//              (two 32-row MFMA groups, each in the fq_row order so that a
+//              lane ends up with 16 consecutive output channels) in
+//              registers and multiplies them with all 64 tokens of the
+//              tile, read from LDS; with k >= 64 both row groups share each
+//              X fragment, so every fragment read feeds two MFMAs;
+//   waves 4-5  copy: stream 32 KiB token tiles (64 tokens x 256 channels)
+//              into a 4-stage LDS ring, three tiles ahead, and in pass 2
+//              the tile's finished row words beside them.
 // The copy waves issue nothing but copies, so their vmcnt waits are exact
 // while the compute waves' stores and atomics stay out of the count.
-// Pass 1 folds per-token maxima of all eight waves with LDS atomics; the
+// Pass 1 folds per-token maxima of the four waves with LDS atomics; the
 // tile's maxima go to the global per-token words one step later (after the
 // next barrier), which needs no barrier of its own.
-constexpr int kTgCompute = 8;
+// (At k = 512 the 64 rows x 512 columns of T a wave would hold do not fit
+// its registers; that case runs on the ring kernels.)
+constexpr int kTgCompute = 4;
 constexpr int kTgCopy = 2;
 constexpr int kTgThreads = (kTgCompute + kTgCopy) * kWave;
 constexpr int kTgStages = 4;
 constexpr int kTgAhead = kTgStages - 1;     // tiles in flight ahead of the one multiplied
-
-template <int K>
-struct TqGroup {
-    static constexpr int COLS = K > 256 ? K : 256;     // X channels per tile row
-    static constexpr int U = COLS / 8;                 // 16-byte units per token row
-    static constexpr int TT = K > 256 ? 32 : 64;       // tokens per tile
-    static constexpr int NSB = TT / 32;                // 32-token MFMA subtiles
-    static constexpr int STAGE = TT * U;               // 16-byte units per stage (32 KiB)
-    static constexpr int NS = K / 16;                  // 16-deep MFMA steps
-    static constexpr int NCHUNK = K > 256 ? K / 256 : 1;   // workgroups per column group
-    static constexpr int COPY_OPS = STAGE / (kTgCopy * kWave);
-    static_assert(STAGE % (kTgCopy * kWave) == 0, "copies split evenly");
-    static_assert(U >= 32, "swizzle spans 32 units");
-};
+constexpr int kTgTT = 64;                   // tokens per tile
+constexpr int kTgU = 32;                    // 16-byte units per token row (256 channels)
+constexpr int kTgStage = kTgTT * kTgU;      // 16-byte units per stage (32 KiB)
+constexpr int kTgCopyOps = kTgStage / (kTgCopy * kWave);   // copies per lane per tile
+static_assert(kTgStage % (kTgCopy * kWave) == 0, "copies split evenly");
 
 // tile it has landed once at most `later` tiles issued after it are in flight
 template <int OPS>
@@ -1079,35 +1070,28 @@ __device__ __forceinline__ u32x2 fq_quant16_asym(const f32x16& z, float zmin, fl
 template <int K, bool QUANT, int QM, bool ASYM>
 __global__ __launch_bounds__(kTgThreads, 1) void tq_group_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ T, int64_t n, int64_t d,
-    int64_t R, int64_t nunits, uint32_t* __restrict__ ws, uint8_t* __restrict__ codes,
-    float* __restrict__ s_x, float* __restrict__ zmin_x) {
-    using C = TqGroup<K>;
+    int64_t R, uint32_t* __restrict__ ws, uint8_t* __restrict__ codes, float* __restrict__ s_x,
+    float* __restrict__ zmin_x) {
+    static_assert(K == 32 || K == 64 || K == 128 || K == 256, "block size");
+    constexpr int NS = K / 16;                          // 16-deep MFMA steps
+    constexpr int NSB = kTgTT / 32;                     // 32-token subtiles
+    constexpr bool kShare = K >= 64;                    // both row groups in one block
     constexpr bool kWordsIn = QUANT && QM != 0;         // pass 2 reads the row words
-    constexpr int OPS = C::COPY_OPS + (kWordsIn ? 1 : 0);
-    __shared__ __attribute__((aligned(16))) u32x4 ring[kTgStages][C::STAGE];
+    constexpr int OPS = kTgCopyOps + (kWordsIn ? 1 : 0);
+    __shared__ __attribute__((aligned(16))) u32x4 ring[kTgStages][kTgStage];
     __shared__ uint32_t words[kWordsIn ? kTgStages : 1][128];
-    __shared__ uint32_t red[QUANT ? 1 : 2][ASYM ? 2 : 1][C::TT];
+    __shared__ uint32_t red[QUANT ? 1 : 2][ASYM ? 2 : 1][kTgTT];
 
-    // workgroup -> (unit, chunk); the NCHUNK workgroups of a unit are 8
-    // apart in launch order, so round-robin dispatch puts them on one XCD
-    int64_t unit = blockIdx.x;
-    int chunk = 0;
-    if constexpr (C::NCHUNK > 1) {
-        const int64_t s = blockIdx.x >> 3;
-        chunk = static_cast<int>(s % C::NCHUNK);
-        unit = (s / C::NCHUNK) * 8 + (blockIdx.x & 7);
-    }
-    if (unit >= nunits) return;
-    const int64_t ngroups = d / C::COLS;
-    const int64_t gb = unit % ngroups;                  // column group
-    const int64_t r0 = unit / ngroups;                  // first token tile
-    const int64_t ntiles = (n + C::TT - 1) / C::TT;
-    if (r0 >= ntiles) return;
+    const int64_t ngroups = d / 256;
+    const int64_t gb = blockIdx.x % ngroups;            // channel group
+    const int64_t r0 = blockIdx.x / ngroups;            // first token tile
+    const int64_t ntiles = (n + kTgTT - 1) / kTgTT;
+    if (r0 >= R || r0 >= ntiles) return;
     const int64_t nt = (ntiles - r0 + R - 1) / R;       // tiles of this workgroup
-    const int64_t cb = gb * C::COLS;                    // first channel of the group
+    const int64_t cb = gb * 256;                        // first channel of the group
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
-    auto tile0 = [&](int64_t it) { return (r0 + it * R) * C::TT; };
+    auto tile0 = [&](int64_t it) { return (r0 + it * R) * kTgTT; };
 
     if (wave >= kTgCompute) {
         // ---------------------------------------------------- copy waves
@@ -1118,19 +1102,18 @@ __global__ __launch_bounds__(kTgThreads, 1) void tq_group_kernel(
             const int64_t last = n - 1 - t0;            // rows past the end: never used
             const int st = static_cast<int>(it % kTgStages);
 #pragma unroll
-            for (int q = 0; q < C::COPY_OPS; ++q) {
+            for (int q = 0; q < kTgCopyOps; ++q) {
                 const int first = (q * kTgCopy + cw) * kWave;
                 const int sl = first + lane;
-                int rr = sl / C::U;
-                const int u = (sl % C::U) ^ (rr & 31);
+                int rr = sl / kTgU;
+                const int u = (sl % kTgU) ^ (rr & 31);
                 rr = rr <= last ? rr : static_cast<int>(last);
                 dma16(base, static_cast<uint32_t>((rr * d + u * 8) * 2), lds_addr(&ring[st][first]));
             }
             if constexpr (kWordsIn) {
-                // symmetric: wave cw brings tokens 32 cw + (lane % 32) (64-token
-                // tiles); asymmetric: wave 0 the max keys, wave 1 the min keys
+                // symmetric: wave cw brings tokens 32 cw + (lane % 32);
+                // asymmetric: wave 0 the max keys, wave 1 the min keys
                 int j = ASYM ? lane : cw * 32 + (lane & 31);
-                if (j >= C::TT) j &= 31;
                 j = j <= last ? j : static_cast<int>(last);
                 const uint32_t* src = ws + (ASYM && cw ? n : 0) + t0;
                 dma4(src, static_cast<uint32_t>(j * 4), lds_addr(&words[st][cw * 64]));
@@ -1152,49 +1135,41 @@ __global__ __launch_bounds__(kTgThreads, 1) void tq_group_kernel(
     // ------------------------------------------------------ compute waves
     const int l32 = lane & 31;
     const int h = lane >> 5;
-    int64_t blk;                 // block of T this wave's rows belong to
-    int rb;                      // first row of the wave's 32 within the block
-    int xo;                      // first 16-byte unit of the block within the tile row
-    if constexpr (C::NCHUNK > 1) {
-        blk = gb;
-        rb = chunk * 256 + wave * 32;
-        xo = 0;
-    } else {
-        const int64_t c0 = cb + wave * 32;
-        blk = c0 / K;
-        rb = static_cast<int>(c0 % K);
-        xo = static_cast<int>((blk * K - cb) / 8);
-    }
-    const int64_t ch0 = blk * K + rb;    // first output channel of the wave
-    u32x4 tf[C::NS];
-    {
-        const u32x4* tg = reinterpret_cast<const u32x4*>(T + (blk * K + rb + fq_row(l32)) * K);
+    int64_t ch[2];               // first output channel of each 32-row group
+    int xo[2];                   // first 16-byte unit of its block within the tile row
+    u32x4 tf[2][NS];
 #pragma unroll
-        for (int s = 0; s < C::NS; ++s) tf[s] = tg[2 * s + h];
+    for (int g = 0; g < 2; ++g) {
+        ch[g] = cb + wave * 64 + g * 32;
+        const int64_t blk = ch[g] / K;
+        xo[g] = static_cast<int>((blk * K - cb) / 8);
+        const u32x4* tg = reinterpret_cast<const u32x4*>(T + (ch[g] + fq_row(l32)) * K);
+#pragma unroll
+        for (int s = 0; s < NS; ++s) tf[g][s] = tg[2 * s + h];
     }
     if constexpr (!QUANT) {
-        for (int i = threadIdx.x; i < 2 * (ASYM ? 2 : 1) * C::TT; i += kTgCompute * kWave)
+        for (int i = threadIdx.x; i < 2 * (ASYM ? 2 : 1) * kTgTT; i += kTgCompute * kWave)
             (&red[0][0][0])[i] = 0u;
     }
-    // pass 1: fold the previous tile's LDS maxima into the global words
+    // pass 1: fold a finished tile's LDS maxima into the global words
     auto flush = [&](int64_t it) {
         const int p = static_cast<int>(it & 1);
-        for (int j = lane; j < C::TT; j += kWave) {
-            const int64_t t = tile0(it) + j;
-            const uint32_t m = red[p][0][j];
-            red[p][0][j] = 0u;
-            if constexpr (ASYM) {
-                const uint32_t mn = red[p][1][j];
-                red[p][1][j] = 0u;
-                if (t < n) {
-                    atomicMax(ws + t, m);
-                    atomicMax(ws + n + t, mn);
-                }
-            } else {
-                if (t < n && m) atomicMax(ws + t, m);
+        const int j = lane;
+        const int64_t t = tile0(it) + j;
+        const uint32_t m = red[p][0][j];
+        red[p][0][j] = 0u;
+        if constexpr (ASYM) {
+            const uint32_t mn = red[p][1][j];
+            red[p][1][j] = 0u;
+            if (t < n) {
+                atomicMax(ws + t, m);
+                atomicMax(ws + n + t, mn);
             }
+        } else {
+            if (t < n && m) atomicMax(ws + t, m);
         }
     };
+    static_assert(kTgTT == kWave, "one token per lane in flush");
 
     for (int64_t it = 0; it < nt; ++it) {
         lds_barrier();
@@ -1202,33 +1177,41 @@ __global__ __launch_bounds__(kTgThreads, 1) void tq_group_kernel(
             if (wave == 0 && it > 0) flush(it - 1);
         }
         const int st = static_cast<int>(it % kTgStages);
-        f32x16 acc[C::NSB];
+        f32x16 acc[2][NSB];
 #pragma unroll
-        for (int sb = 0; sb < C::NSB; ++sb) acc[sb] = f32x16{};
+        for (int g = 0; g < 2; ++g)
 #pragma unroll
-        for (int s = 0; s < C::NS; ++s) {
+            for (int sb = 0; sb < NSB; ++sb) acc[g][sb] = f32x16{};
 #pragma unroll
-            for (int sb = 0; sb < C::NSB; ++sb) {
+        for (int s = 0; s < NS; ++s) {
+#pragma unroll
+            for (int sb = 0; sb < NSB; ++sb) {
                 const int rr = sb * 32 + l32;
-                const u32x4 xf = ring[st][rr * C::U + ((xo + 2 * s + h) ^ (rr & 31))];
-                acc[sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(tf[s]), as_bf16x8(xf),
-                                                                  acc[sb], 0, 0, 0);
+                const u32x4 x0 = ring[st][rr * kTgU + ((xo[0] + 2 * s + h) ^ (rr & 31))];
+                const u32x4 x1 =
+                    kShare ? x0 : ring[st][rr * kTgU + ((xo[1] + 2 * s + h) ^ (rr & 31))];
+                acc[0][sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                    as_bf16x8(tf[0][s]), as_bf16x8(x0), acc[0][sb], 0, 0, 0);
+                acc[1][sb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                    as_bf16x8(tf[1][s]), as_bf16x8(x1), acc[1][sb], 0, 0, 0);
             }
         }
-        // lane (token sb * 32 + l32, h) holds channels ch0 + 16 h .. + 15
+        // lane (token sb * 32 + l32, h) holds channels ch[g] + 16 h .. + 15
 #pragma unroll
-        for (int sb = 0; sb < C::NSB; ++sb) {
+        for (int sb = 0; sb < NSB; ++sb) {
             const int j = sb * 32 + l32;
             const int64_t t = tile0(it) + j;
             const bool valid = t < n;
             if constexpr (!QUANT && ASYM) {
                 uint32_t mx = 0, mn = 0;
 #pragma unroll
-                for (int q = 0; q < 16; ++q) {
-                    const uint32_t kq = fkey(acc[sb][q]);
-                    mx = max(mx, kq);
-                    mn = max(mn, ~kq);
-                }
+                for (int g = 0; g < 2; ++g)
+#pragma unroll
+                    for (int q = 0; q < 16; ++q) {
+                        const uint32_t kq = fkey(acc[g][sb][q]);
+                        mx = max(mx, kq);
+                        mn = max(mn, ~kq);
+                    }
                 mx = max(mx, static_cast<uint32_t>(__shfl_xor(static_cast<int>(mx), 32)));
                 mn = max(mn, static_cast<uint32_t>(__shfl_xor(static_cast<int>(mn), 32)));
                 if (h == 0) {
@@ -1236,41 +1219,49 @@ __global__ __launch_bounds__(kTgThreads, 1) void tq_group_kernel(
                     atomicMax(&red[it & 1][1][j], mn);
                 }
             } else if constexpr (!QUANT) {
-                uint32_t m = fq_absmax16(acc[sb]);
+                uint32_t m = max(fq_absmax16(acc[0][sb]), fq_absmax16(acc[1][sb]));
                 m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), 32)));
                 if (h == 0) atomicMax(&red[it & 1][0][j], m);
             } else if constexpr (QM == 0) {
                 if (valid) {
-                    float* zrow = reinterpret_cast<float*>(codes) + t * d + ch0 + 16 * h;
 #pragma unroll
-                    for (int q = 0; q < 4; ++q)
-                        *reinterpret_cast<f32x4*>(zrow + 4 * q) =
-                            f32x4{acc[sb][4 * q], acc[sb][4 * q + 1], acc[sb][4 * q + 2],
-                                  acc[sb][4 * q + 3]};
+                    for (int g = 0; g < 2; ++g) {
+                        float* zrow = reinterpret_cast<float*>(codes) + t * d + ch[g] + 16 * h;
+#pragma unroll
+                        for (int q = 0; q < 4; ++q)
+                            *reinterpret_cast<f32x4*>(zrow + 4 * q) =
+                                f32x4{acc[g][sb][4 * q], acc[g][sb][4 * q + 1],
+                                      acc[g][sb][4 * q + 2], acc[g][sb][4 * q + 3]};
+                    }
                 }
             } else if constexpr (ASYM) {
                 float zmin = 0.0f, s = 0.0f, inv = 0.0f;
                 asym_scale(words[st][j], words[st][64 + j], zmin, s, inv);
-                if (valid && h == 0 && wave == 0 && gb == 0 && chunk == 0) {
+                if (valid && h == 0 && wave == 0 && gb == 0) {
                     s_x[t] = s;
                     zmin_x[t] = zmin;
                 }
-                const u32x2 c = fq_quant16_asym(acc[sb], zmin, inv);
-                if (valid) *reinterpret_cast<u32x2*>(codes + t * (d / 2) + (ch0 + 16 * h) / 2) = c;
+#pragma unroll
+                for (int g = 0; g < 2; ++g) {
+                    const u32x2 c = fq_quant16_asym(acc[g][sb], zmin, inv);
+                    if (valid)
+                        *reinterpret_cast<u32x2*>(codes + t * (d / 2) + (ch[g] + 16 * h) / 2) = c;
+                }
             } else {
                 constexpr float qmax = static_cast<float>(QM);
-                const uint32_t wj = C::TT == 64 ? (j >> 5) * 64 + (j & 31) : j;
-                const float amax = __uint_as_float(words[st][wj]);
-                if (valid && h == 0 && wave == 0 && gb == 0 && chunk == 0)
-                    s_x[t] = __fdiv_rn(amax, qmax);
+                const float amax = __uint_as_float(words[st][(j >> 5) * 64 + (j & 31)]);
+                if (valid && h == 0 && wave == 0 && gb == 0) s_x[t] = __fdiv_rn(amax, qmax);
                 const float inv = amax > 0.0f ? __fdiv_rn(qmax, amax) : 0.0f;
-                if constexpr (QM == 7) {
-                    const u32x2 c = fq_quant16(acc[sb], inv);
-                    if (valid)
-                        *reinterpret_cast<u32x2*>(codes + t * (d / 2) + (ch0 + 16 * h) / 2) = c;
-                } else {
-                    const u32x4 c = fq_quant16_i8<QM>(acc[sb], inv);
-                    if (valid) *reinterpret_cast<u32x4*>(codes + t * d + ch0 + 16 * h) = c;
+#pragma unroll
+                for (int g = 0; g < 2; ++g) {
+                    if constexpr (QM == 7) {
+                        const u32x2 c = fq_quant16(acc[g][sb], inv);
+                        if (valid)
+                            *reinterpret_cast<u32x2*>(codes + t * (d / 2) + (ch[g] + 16 * h) / 2) = c;
+                    } else {
+                        const u32x4 c = fq_quant16_i8<QM>(acc[g][sb], inv);
+                        if (valid) *reinterpret_cast<u32x4*>(codes + t * d + ch[g] + 16 * h) = c;
+                    }
                 }
             }
         }
@@ -1285,33 +1276,30 @@ template <int K, int QM, bool ASYM = false>
 hipError_t launch_tq_group(const uint16_t* X, int64_t n, int64_t d, const uint16_t* T,
                            uint8_t* codes, float* s_x, uint32_t* ws, hipStream_t stream,
                            float* zmin_x = nullptr, bool z_only = false) {
-    using C = TqGroup<K>;
     int dev = 0, cus = 0;
     hipError_t err = hipGetDevice(&dev);
     if (err != hipSuccess) return err;
     err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (err != hipSuccess) return err;
-    const int64_t ntiles = (n + C::TT - 1) / C::TT;
-    const int64_t ngroups = d / C::COLS;
-    // one workgroup per CU: R token-tile rows per column group, rounded
+    const int64_t ntiles = (n + kTgTT - 1) / kTgTT;
+    const int64_t ngroups = d / 256;
+    // one workgroup per CU: R token-tile rows per channel group, rounded
     // down so that every workgroup is resident at once
-    int64_t R = (static_cast<int64_t>(cus) / C::NCHUNK) / ngroups;
+    int64_t R = static_cast<int64_t>(cus) / ngroups;
     if (R > ntiles) R = ntiles;
     if (R < 1) R = 1;
-    const int64_t nunits = ngroups * R;
-    const int64_t grid = C::NCHUNK > 1 ? (nunits + 7) / 8 * 8 * C::NCHUNK : nunits;
+    const dim3 grid(static_cast<uint32_t>(ngroups * R)), block(kTgThreads);
     if (z_only) {
-        hipLaunchKernelGGL((tq_group_kernel<K, true, 0, false>), dim3(static_cast<uint32_t>(grid)),
-                           dim3(kTgThreads), 0, stream, X, T, n, d, R, nunits, ws, codes, s_x,
-                           zmin_x);
+        hipLaunchKernelGGL((tq_group_kernel<K, true, 0, false>), grid, block, 0, stream, X, T, n, d,
+                           R, ws, codes, s_x, zmin_x);
         return hipGetLastError();
     }
-    hipLaunchKernelGGL((tq_group_kernel<K, false, 7, ASYM>), dim3(static_cast<uint32_t>(grid)),
-                       dim3(kTgThreads), 0, stream, X, T, n, d, R, nunits, ws, codes, s_x, zmin_x);
+    hipLaunchKernelGGL((tq_group_kernel<K, false, 7, ASYM>), grid, block, 0, stream, X, T, n, d, R,
+                       ws, codes, s_x, zmin_x);
     err = hipGetLastError();
     if (err != hipSuccess) return err;
-    hipLaunchKernelGGL((tq_group_kernel<K, true, QM, ASYM>), dim3(static_cast<uint32_t>(grid)),
-                       dim3(kTgThreads), 0, stream, X, T, n, d, R, nunits, ws, codes, s_x, zmin_x);
+    hipLaunchKernelGGL((tq_group_kernel<K, true, QM, ASYM>), grid, block, 0, stream, X, T, n, d, R,
+                       ws, codes, s_x, zmin_x);
     return hipGetLastError();
 }
 

@@ -62,6 +62,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-report", action="store_true",
                    help="skip the widened paths and the other configurations after the steps")
+    p.add_argument("--no-configs", action="store_true",
+                   help="keep the widened paths of the metric layer, skip the other configurations")
     p.add_argument("--wide-steps", type=int, default=10,
                    help="timed iterations of each pair measured after the steps")
     p.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -555,6 +557,7 @@ def main():
     if not args.no_report:
         widened(rec, torch, cat, B, P, layer, run, Xs, Ys, lay, n, d_in, d_out, k, tdt,
                 tq_bytes, gemm_ops, args.wide_steps)
+    if not args.no_report and not args.no_configs:
         # free the metric layer before the other configurations
         del run, Xs, Ys, X0, sigma, ws_c
         torch.cuda.empty_cache()

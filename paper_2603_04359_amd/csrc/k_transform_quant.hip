@@ -1064,9 +1064,7 @@ __device__ __forceinline__ u32x2 fq_quant16_asym(const f32x16& z, float zmin, fl
 
 // QUANT false: pass 1 (row maxima into ws[t], or for ASYM the max key into
 // ws[t] and the complemented min key into ws[n + t]).  QUANT true: pass 2
-// (codes and s_x from the finished words; for ASYM also zmin_x), or with
-// QM = 0 the transformed rows z themselves, fp32, into `codes` read as an
-// [n x d] float array (no pass 1 then).
+// (codes and s_x from the finished words; for ASYM also zmin_x).
 template <int K, bool QUANT, int QM, bool ASYM>
 __global__ __launch_bounds__(kTgThreads, 1) void tq_group_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ T, int64_t n, int64_t d,
@@ -1076,7 +1074,8 @@ __global__ __launch_bounds__(kTgThreads, 1) void tq_group_kernel(
     constexpr int NS = K / 16;                          // 16-deep MFMA steps
     constexpr int NSB = kTgTT / 32;                     // 32-token subtiles
     constexpr bool kShare = K >= 64;                    // both row groups in one block
-    constexpr bool kWordsIn = QUANT && QM != 0;         // pass 2 reads the row words
+    static_assert(QM == 7 || QM == 31 || QM == 127, "qmax");
+    constexpr bool kWordsIn = QUANT;                    // pass 2 reads the row words
     constexpr int OPS = kTgCopyOps + (kWordsIn ? 1 : 0);
     __shared__ __attribute__((aligned(16))) u32x4 ring[kTgStages][kTgStage];
     __shared__ uint32_t words[kWordsIn ? kTgStages : 1][128];
@@ -1222,18 +1221,6 @@ __global__ __launch_bounds__(kTgThreads, 1) void tq_group_kernel(
                 uint32_t m = max(fq_absmax16(acc[0][sb]), fq_absmax16(acc[1][sb]));
                 m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), 32)));
                 if (h == 0) atomicMax(&red[it & 1][0][j], m);
-            } else if constexpr (QM == 0) {
-                if (valid) {
-#pragma unroll
-                    for (int g = 0; g < 2; ++g) {
-                        float* zrow = reinterpret_cast<float*>(codes) + t * d + ch[g] + 16 * h;
-#pragma unroll
-                        for (int q = 0; q < 4; ++q)
-                            *reinterpret_cast<f32x4*>(zrow + 4 * q) =
-                                f32x4{acc[g][sb][4 * q], acc[g][sb][4 * q + 1],
-                                      acc[g][sb][4 * q + 2], acc[g][sb][4 * q + 3]};
-                    }
-                }
             } else if constexpr (ASYM) {
                 float zmin = 0.0f, s = 0.0f, inv = 0.0f;
                 asym_scale(words[st][j], words[st][64 + j], zmin, s, inv);
@@ -1275,7 +1262,7 @@ __global__ __launch_bounds__(kTgThreads, 1) void tq_group_kernel(
 template <int K, int QM, bool ASYM = false>
 hipError_t launch_tq_group(const uint16_t* X, int64_t n, int64_t d, const uint16_t* T,
                            uint8_t* codes, float* s_x, uint32_t* ws, hipStream_t stream,
-                           float* zmin_x = nullptr, bool z_only = false) {
+                           float* zmin_x = nullptr) {
     int dev = 0, cus = 0;
     hipError_t err = hipGetDevice(&dev);
     if (err != hipSuccess) return err;
@@ -1289,11 +1276,6 @@ hipError_t launch_tq_group(const uint16_t* X, int64_t n, int64_t d, const uint16
     if (R > ntiles) R = ntiles;
     if (R < 1) R = 1;
     const dim3 grid(static_cast<uint32_t>(ngroups * R)), block(kTgThreads);
-    if (z_only) {
-        hipLaunchKernelGGL((tq_group_kernel<K, true, 0, false>), grid, block, 0, stream, X, T, n, d,
-                           R, ws, codes, s_x, zmin_x);
-        return hipGetLastError();
-    }
     hipLaunchKernelGGL((tq_group_kernel<K, false, 7, ASYM>), grid, block, 0, stream, X, T, n, d, R,
                        ws, codes, s_x, zmin_x);
     err = hipGetLastError();
@@ -1710,12 +1692,10 @@ hipError_t launch_transform_quant_full(const void* X, int64_t n, int64_t d, cons
                            nullptr);
         return hipGetLastError();
     };
-    if (tq_group_fits(d, k))
-        err = k == 128 ? launch_tq_group<128, 0>(Xb, n, d, Tb, zb, nullptr, nullptr, stream, nullptr, true)
-                       : launch_tq_group<256, 0>(Xb, n, d, Tb, zb, nullptr, nullptr, stream, nullptr, true);
-    else
-        err = k == 128 ? zpass(std::integral_constant<int, 128>{})
-                       : zpass(std::integral_constant<int, 256>{});
+    // the z pass stays on the ring kernels: writing fp32 z, two workgroups
+    // per CU (measured 43 us at 8192 x 4096) beat the group kernel (59 us)
+    err = k == 128 ? zpass(std::integral_constant<int, 128>{})
+                   : zpass(std::integral_constant<int, 256>{});
     if (err != hipSuccess) return err;
     const dim3 grid(static_cast<uint32_t>(n)), block(static_cast<uint32_t>(k));
     switch (d / k) {

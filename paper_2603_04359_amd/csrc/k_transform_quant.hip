@@ -615,9 +615,9 @@ __global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
 }
 
 // ------------------------------------------------- single-pass variant
-// bf16, k = 128, d = 4096 (32 blocks), one launch, X read once.  One
-// workgroup per CU owns block b for the token tiles r, r + R, ... (a tile is
-// 64 tokens) and splits its eight waves by role:
+// bf16, k = 128, d = 128 NB with NB = 16, 32 or 64 blocks, one launch, X
+// read once.  One workgroup per CU owns block b for the token tiles r,
+// r + R, ... (a tile is 64 tokens) and splits its eight waves by role:
 //   waves 0-3  compute: wave w multiplies rows 64 (w / 2) .. + 63 of T_b
 //              (held in registers) with tokens 32 (w % 2) .. + 31 of the
 //              tile, read from LDS;
@@ -630,12 +630,13 @@ __global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
 // count their own copies, and the compiler tracks the loads of the gather
 // wave (stores of the others are never waited for).
 //
-// The row maximum of a token needs all 32 blocks, exchanged in two levels
+// The row maximum of a token needs all NB blocks, exchanged in two levels
 // through the workspace: every workgroup publishes its block maxima P(b, t)
-// of a tile; workgroup b owns tokens 2b, 2b + 1 of the tile, reduces their
-// 32 P words and has the row maximum F(t) published; every workgroup then
-// reads F of the tile's 64 tokens (1 KiB of reads per workgroup and tile
-// per level instead of 16 KiB for all P words).  A word is
+// of a tile; workgroup b owns the 64 / NB tokens (64 / NB) b, ... of the
+// tile, reduces their NB P words each and has the row maxima F(t)
+// published; every workgroup then reads F of the tile's 64 tokens (64
+// words of reads per workgroup and tile per level instead of 64 NB for all
+// P words).  A word is
 // (call tag << 32) | maximum bits written with one store, so a reader sees
 // either an old word (another tag) or the whole new one and the workspace
 // needs no clearing between calls.  Tags have bit 31 set; the two-pass
@@ -643,8 +644,8 @@ __global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
 // nothing they leave behind is read here.  Eager calls take the tag from a host
 // counter; a call captured into a graph takes it from a word a one-thread
 // kernel advances before every replay (see launch_tq_fused).  P(j, t) lives at
-// ((t / 16) * 32 + j) * 16 + t % 16 (16 tokens of a block fill one 128-byte
-// line), F(t) at 32 n' + t.
+// ((t / 16) * NB + j) * 16 + t % 16 (16 tokens of a block fill one 128-byte
+// line), F(t) at NB n' + t (n' = n rounded up to 16).
 //
 // Step s has barriers A and F.  A to F: the compute waves multiply tile s
 // and leave per-wave maxima in LDS; the gather wave takes F of tile s-3
@@ -672,7 +673,6 @@ constexpr int kFqTT = 64;                       // tokens per tile
 constexpr int kFqU = 16;                        // 16-byte units per token row
 constexpr int kFqStage = kFqTT * kFqU;          // units per stage (16 KiB)
 constexpr int kFqCopyOps = kFqStage / (kFqCopy * kWave);   // copies per lane per tile
-constexpr int kFqBlocks = 32;                   // d / 128
 constexpr int kFqLag = 3;                       // tile s is quantized in step s + kFqLag
 // Copies in flight per CU (kFqAhead tiles of 16 KiB).  Every load of this
 // CU, the exchange polls included, queues behind them: under a 6 TB/s
@@ -683,7 +683,6 @@ constexpr int kFqLag = 3;                       // tile s is quantized in step s
 constexpr int kFqAhead = 3;
 static_assert(kFqCopyOps * kFqAhead < 64, "copies in flight must fit the vmcnt range");
 static_assert(kFqAhead < kFqStages, "a stage is refilled only after its tile is multiplied");
-static_assert(kFqTT == 2 * kFqBlocks, "each workgroup reduces two tokens of a tile");
 
 struct TqFusedWs {
     uint64_t* pmax;       // P words, then F words (see above)
@@ -787,7 +786,7 @@ __device__ __forceinline__ void fq_wait_copies(int later) {
     }
 }
 
-template <int QM>
+template <int QM, int NB>
 __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ T, int64_t n, int64_t d,
     int64_t R, TqFusedWs ws, uint32_t host_tag, uint8_t* __restrict__ codes,
@@ -801,10 +800,12 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
     __shared__ __attribute__((aligned(16))) u32x4 ring[kFqStages][kFqStage];
     __shared__ uint32_t red[2][kFqTT];            // per-row-half maxima of the step's tile
     __shared__ uint32_t gat[kFqTT];               // row maxima of the tile being quantized
-    __shared__ uint32_t fred[2][2];               // reduced row maxima of the owned tokens
+    static_assert(NB >= 16 && NB <= kWave && kFqTT % NB == 0, "blocks per token-tile row");
+    constexpr int TPO = kFqTT / NB;               // tokens each workgroup reduces per tile
+    __shared__ uint32_t fred[2][TPO];             // reduced row maxima of the owned tokens
 
-    const int64_t b = blockIdx.x % kFqBlocks;
-    const int64_t r0 = blockIdx.x / kFqBlocks;
+    const int64_t b = blockIdx.x % NB;
+    const int64_t r0 = blockIdx.x / NB;
     const int64_t ntiles = (n + kFqTT - 1) / kFqTT;
     if (r0 >= ntiles) return;           // never taken: the launcher sizes R <= ntiles
     const int64_t nt = (ntiles - r0 + R - 1) / R;
@@ -819,10 +820,10 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
         // a wait for a load never includes a store's acknowledgement.
         const uint64_t hi = static_cast<uint64_t>(tag) << 32;
         const int64_t n16 = (n + 15) / 16 * 16;
-        uint64_t* const fw = ws.pmax + n16 * kFqBlocks;
+        uint64_t* const fw = ws.pmax + n16 * NB;
         auto clampt = [&](int64_t t) { return t < n ? t : n - 1; };
         auto p_word = [&](int64_t t, int64_t j) {
-            return ws.pmax + (t >> 4) * (kFqBlocks * 16) + j * 16 + (t & 15);
+            return ws.pmax + (t >> 4) * (NB * 16) + j * 16 + (t & 15);
         };
         auto store = [&](uint64_t* a, uint32_t m) {
             __hip_atomic_store(a, hi | m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -832,8 +833,8 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
             for (int64_t it = 0; it < nsteps; ++it) {
                 lds_barrier();                                        // A
                 if (it >= 2 && it - 2 < nt) {
-                    const int64_t t = tile0(it - 2) + 2 * b + (lane >> 5);
-                    if ((lane & 31) == 0 && t < n) store(fw + t, fred[it & 1][lane >> 5]);
+                    const int64_t t = tile0(it - 2) + TPO * b + lane;
+                    if (lane < TPO && t < n) store(fw + t, fred[it & 1][lane < TPO ? lane : 0]);
                 }
                 lds_barrier();                                        // F
                 if (it < nt) {
@@ -866,10 +867,10 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
             }
             return static_cast<uint32_t>(v);
         };
-        // F(token lane of tile j); P(block lane % 32, token 2b + lane / 32 of tile j)
+        // F(token lane of tile j); P(block lane % NB, token TPO b + lane / NB of tile j)
         auto f_addr = [&](int64_t j) { return fw + clampt(tile0(j) + lane); };
         auto p_addr = [&](int64_t j) {
-            return p_word(clampt(tile0(j) + 2 * b + (lane >> 5)), lane & 31);
+            return p_word(clampt(tile0(j) + TPO * b + lane / NB), lane % NB);
         };
         uint64_t fv = 0, pv = 0;
         for (int64_t it = 0; it < nsteps; ++it) {
@@ -885,9 +886,9 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
             if (it >= 1 && it <= nt) {
                 uint32_t m = await(pv, p_addr(it - 1));
 #pragma unroll
-                for (int x = 1; x < 32; x <<= 1)
+                for (int x = 1; x < NB; x <<= 1)
                     m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), x)));
-                if ((lane & 31) == 0) fred[(it + 1) & 1][lane >> 5] = m;
+                if (lane % NB == 0) fred[(it + 1) & 1][lane / NB] = m;
             }
             if (it + 1 >= kFqLag && it + 1 < nsteps) fv = load(f_addr(it + 1 - kFqLag));
         }
@@ -1355,10 +1356,10 @@ static uint32_t next_tq_tag() {
 
 // Resident workgroups of tq_fused_kernel on a device (CUs x blocks per CU
 // by its register and LDS use), queried once per device.
-template <int QM>
+template <int QM, int NB>
 static hipError_t tq_fused_resident(int dev, int64_t& resident) {
     constexpr int kMaxDev = 64;
-    static std::atomic<int64_t> cache[kMaxDev];   // 0 = not yet known
+    static std::atomic<int64_t> cache[kMaxDev];   // 0 = not yet known (one table per kernel)
     if (dev >= 0 && dev < kMaxDev) {
         resident = cache[dev].load(std::memory_order_relaxed);
         if (resident > 0) return hipSuccess;
@@ -1366,35 +1367,34 @@ static hipError_t tq_fused_resident(int dev, int64_t& resident) {
     int cus = 0, per_cu = 0;
     hipError_t err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (err != hipSuccess) return err;
-    err = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, tq_fused_kernel<QM>, kFqThreads, 0);
+    err = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, tq_fused_kernel<QM, NB>, kFqThreads, 0);
     if (err != hipSuccess) return err;
     resident = static_cast<int64_t>(per_cu) * cus;
     if (dev >= 0 && dev < kMaxDev && resident > 0) cache[dev].store(resident, std::memory_order_relaxed);
     return hipSuccess;
 }
 
-// Single-pass launch (k = 128, d = 4096) when the grid (d/128
+// Single-pass launch (k = 128, d = 2048, 4096 or 8192) when the grid (d/128
 // workgroups per token-tile row, as many rows as fit) can be resident all
 // at once; otherwise nothing is launched and the caller takes the two-pass
 // path.
 // The grid never exceeds the resident capacity, so every workgroup is on
 // the device together once other work has drained, and a peer a workgroup
 // waits for is always running or about to run.
-template <int QM>
-hipError_t launch_tq_fused(const uint16_t* X, int64_t n, int64_t d, const uint16_t* T,
-                           uint8_t* codes, float* s_x, uint8_t* ws, hipStream_t stream,
-                           bool& launched) {
+template <int QM, int NB>
+static hipError_t launch_tq_fused_nb(const uint16_t* X, int64_t n, int64_t d, const uint16_t* T,
+                                     uint8_t* codes, float* s_x, uint8_t* ws, hipStream_t stream,
+                                     bool& launched) {
     launched = false;
     int dev = 0;
     hipError_t err = hipGetDevice(&dev);
     if (err != hipSuccess) return err;
     int64_t resident = 0;
-    err = tq_fused_resident<QM>(dev, resident);
+    err = tq_fused_resident<QM, NB>(dev, resident);
     if (err != hipSuccess) return err;
-    const int64_t nbj = d / 128;
     const int64_t ntiles = (n + kFqTT - 1) / kFqTT;
-    if (nbj != kFqBlocks || nbj > resident) return hipSuccess;
-    int64_t R = resident / nbj;
+    if (NB > resident) return hipSuccess;
+    int64_t R = resident / NB;
     if (R > ntiles) R = ntiles;
     if (R < 1) R = 1;
     TqFusedWs w;
@@ -1416,12 +1416,25 @@ hipError_t launch_tq_fused(const uint16_t* X, int64_t n, int64_t d, const uint16
     } else {
         tag = next_tq_tag();
     }
-    hipLaunchKernelGGL(tq_fused_kernel<QM>, dim3(static_cast<uint32_t>(nbj * R)), dim3(kFqThreads),
-                       0, stream, X, T, n, d, R, w, tag, codes, s_x);
+    hipLaunchKernelGGL((tq_fused_kernel<QM, NB>), dim3(static_cast<uint32_t>(NB * R)),
+                       dim3(kFqThreads), 0, stream, X, T, n, d, R, w, tag, codes, s_x);
     err = hipGetLastError();
     if (err != hipSuccess) return err;
     launched = true;
     return hipSuccess;
+}
+
+template <int QM>
+hipError_t launch_tq_fused(const uint16_t* X, int64_t n, int64_t d, const uint16_t* T,
+                           uint8_t* codes, float* s_x, uint8_t* ws, hipStream_t stream,
+                           bool& launched) {
+    launched = false;
+    switch (d) {
+        case 2048: return launch_tq_fused_nb<QM, 16>(X, n, d, T, codes, s_x, ws, stream, launched);
+        case 4096: return launch_tq_fused_nb<QM, 32>(X, n, d, T, codes, s_x, ws, stream, launched);
+        case 8192: return launch_tq_fused_nb<QM, 64>(X, n, d, T, codes, s_x, ws, stream, launched);
+        default: return hipSuccess;
+    }
 }
 
 template <int QM, typename XT, typename TT>

@@ -267,6 +267,12 @@ def _rand_T(d, k, seed):
     return o.round_storage(rng.standard_normal((d // k, k, k)) / np.sqrt(k), "bf16")
 
 
+def _wide_X(n, d, seed):
+    # mlp_up-structured activations, tiled or cut to width d
+    X = _mlp_up_X(n, seed)
+    return np.tile(X, (1, (d + 4095) // 4096))[:, :d].copy() if d != 4096 else X
+
+
 def _mlp_up_X(n, seed):
     cfg = wl.get_config("mlp_up", n=n, n_cal=16)
     return wl.make_layer(cfg, seed=seed, with_cal=False, with_weights=False)["X"].astype(np.float64)
@@ -323,6 +329,34 @@ def test_transform_quant_two_pass_shapes(d, k, n):
         assert s[n // 2] == 0 and not codes[n // 2].any()
 
 
+@pytest.mark.parametrize("d,n", [(8192, 1), (8192, 65), (8192, 2049), (2048, 1), (2048, 300),
+                                 (2048, 4097)])
+def test_transform_quant_single_pass_other_widths(d, n):
+    # the single-pass kernel with 64 and 16 blocks per token-tile row (one
+    # and four owned tokens per workgroup and tile)
+    say(f"tq single pass d={d} k=128 n={n}")
+    X = _wide_X(n, d, seed=n + d)
+    if n > 2:
+        X[n // 2] = 0.0
+    T = _rand_T(d, 128, seed=d)
+    codes, s = _tq_gpu(X, T, 128, "bf16", "bf16")
+    _, _, s_or = check_codes(codes, X, T, label=f"single pass d={d} n={n}")
+    _check_scales(s, s_or, f"single pass d={d} n={n}")
+    if n > 2:
+        assert s[n // 2] == 0 and not codes[n // 2].any()
+
+
+def test_transform_quant_single_pass_stress_full_size():
+    # 16384 tokens x 8192 channels, the stress layer's k = 128 shape
+    say("tq single pass stress 16384 x 8192")
+    cfg = wl.get_config("stress", n=16384, n_cal=16, k=128)
+    X = wl.make_layer(cfg, seed=0, with_cal=False, with_weights=False)["X"].astype(np.float64)
+    T = _rand_T(8192, 128, seed=7)
+    codes, s = _tq_gpu(X, T, 128, "bf16", "bf16")
+    _, _, s_or = check_codes(codes, X, T, label="stress full")
+    _check_scales(s, s_or, "stress full")
+
+
 def test_transform_quant_single_pass_mlp_up_full_size():
     # 8192 tokens x 4096 channels, the shape and launch the benchmark times
     say("tq single pass mlp_up 8192 x 4096")
@@ -337,7 +371,7 @@ def test_transform_quant_workspace_reuse_across_paths():
     # One workspace through single-pass, two-pass and single-pass calls on
     # different data: words left by earlier calls must never pass for the
     # current call's.
-    say("tq workspace reuse: single pass / two pass / single pass")
+    say("tq workspace reuse: single pass / two pass / single pass at two widths")
     torch = torch_mod()
     n = 300
     wsb = max(cat.cat_transform_quant_workspace_bytes(n, 4096, 128),
@@ -345,37 +379,45 @@ def test_transform_quant_workspace_reuse_across_paths():
     ws = torch.zeros(wsb, dtype=torch.uint8, device="cuda")
     T4 = _rand_T(4096, 128, seed=3)
     T1 = _rand_T(1024, 128, seed=4)
+    T8 = _rand_T(8192, 128, seed=5)
+    wsb = max(wsb, cat.cat_transform_quant_workspace_bytes(n, 8192, 128))
+    ws = torch.zeros(wsb, dtype=torch.uint8, device="cuda")
     cases = [(_mlp_up_X(n, seed=10), T4), (_mlp_up_X(n, seed=11)[:, :1024].copy(), T1),
-             (_mlp_up_X(n, seed=12) * 2.0 ** -6, T4), (_mlp_up_X(n, seed=10), T4)]
+             (_wide_X(n, 8192, seed=13), T8), (_mlp_up_X(n, seed=12) * 2.0 ** -6, T4),
+             (_mlp_up_X(n, seed=10), T4)]
     first = None
     for i, (X, T) in enumerate(cases):
         d = X.shape[1]
         codes = torch.empty((n, d // 2), dtype=torch.uint8, device="cuda")
         s_x = torch.empty(n, dtype=torch.float32, device="cuda")
+        # the single-pass kernel's bounded waits record a timeout in the word
+        # at cat_transform_quant_flag_offset of the call's shape (wider calls
+        # put exchange words where a narrower call's flag sits, so each call
+        # clears and checks its own)
+        fo = cat.cat_transform_quant_flag_offset(n, d, 128)
+        ws[fo:fo + 4].zero_()
         cat.cat_transform_quant(dev(X, "bf16"), dev(T, "bf16"), 128, codes, s_x, ws)
         c, s = host(codes), host(s_x)
+        assert int(host(ws[fo:fo + 4].view(torch.int32))[0]) == 0, f"timeout flag, call {i}"
         _, _, s_or = check_codes(c, X, T, label=f"reuse call {i}")
         _check_scales(s, s_or, f"reuse call {i}")
         if i == 0:
             first = (c, s)
     assert np.array_equal(first[0], c) and np.array_equal(first[1], s)
-    # the single-pass kernel's bounded waits record a timeout in the word at
-    # cat_transform_quant_flag_offset; none may have happened
-    fo = cat.cat_transform_quant_flag_offset(n, 4096, 128)
-    assert int(host(ws[fo:fo + 4].view(torch.int32))[0]) == 0
 
 
-def test_transform_quant_graph_replays_see_fresh_inputs():
+@pytest.mark.parametrize("d", [4096, 8192, 2048])
+def test_transform_quant_graph_replays_see_fresh_inputs(d):
     # A captured single-pass call replayed with new activations each time:
     # every replay must publish under a tag of its own (made on the device),
     # and eager calls on the same workspace in between (host tags) must not
     # mix with it.  The workspace starts with whatever memory holds.
-    say("tq graph capture: 4 replays with new X, eager calls between")
+    say(f"tq graph capture d={d}: 4 replays with new X, eager calls between")
     torch = torch_mod()
-    n, d, k = 300, 4096, 128
+    n, k = 300, 128
     T = _rand_T(d, k, seed=21)
     dT = dev(T, "bf16")
-    Xs = [_mlp_up_X(n, seed=30 + i) for i in range(4)]
+    Xs = [_wide_X(n, d, seed=30 + i) for i in range(4)]
     Xs[2] = Xs[2] * 2.0 ** -6
     dX = dev(Xs[0], "bf16")
     wsb = cat.cat_transform_quant_workspace_bytes(n, d, k)

@@ -38,11 +38,12 @@ def _rand_T(d, k, seed, dtype):
     return o.round_storage(rng.standard_normal((d // k, k, k)) / np.sqrt(k), dtype)
 
 
-# (d, k, n, x_dtype, t_dtype): the single-pass kernel (d = 4096, k = 128,
-# bf16), the two-pass group kernels (k <= 256 with d a multiple of 256),
+# (d, k, n, x_dtype, t_dtype): the single-pass kernel (d = 2048, 4096,
+# 8192, k = 128, bf16), the two-pass group kernels (k <= 256 with d a multiple of 256),
 # the ring kernels (k = 512; k = 128 at d = 640), the small-block MFMA
 # kernel (k = 64 at d = 384) and the vector-ALU kernels (fp32, k = 16)
-PATHS = [(4096, 128, 300, "bf16", "bf16"), (1024, 128, 257, "bf16", "bf16"),
+PATHS = [(4096, 128, 300, "bf16", "bf16"), (8192, 128, 130, "bf16", "bf16"),
+         (2048, 128, 97, "bf16", "bf16"), (1024, 128, 257, "bf16", "bf16"),
          (1024, 256, 129, "bf16", "bf16"), (1024, 512, 65, "bf16", "bf16"),
          (512, 64, 200, "bf16", "bf16"), (512, 32, 131, "bf16", "bf16"),
          (640, 128, 77, "bf16", "bf16"), (384, 64, 90, "bf16", "bf16"),

@@ -230,7 +230,12 @@ int cat_int8_linear(const int8_t* codes_x, const float* s_x,
  *   q = clamp(rint(fl(fl(z - zmin) * inv)), 0, 15)     (ties to even)
  * so that z ~ s_x q + zmin.  codes hold q - 8 as packed INT4 (the layout
  * above, values in [-8, 7]); zmin_x device fp32 [n] (written).  Other
- * arguments, the workspace and errors as cat_transform_quant (bits is 4).
+ * arguments and errors as cat_transform_quant (bits is 4).  The workspace
+ * is at least cat_transform_quant_asym_workspace_bytes(n, d, k) bytes
+ * (larger than the symmetric one: the single-pass path, bf16 with k = 128
+ * and d = 2048, 4096 or 8192, exchanges a row minimum and maximum per
+ * token); the exchange timeout word is at cat_transform_quant_flag_offset
+ * as for the symmetric path, and a timed-out wait yields s_x = zmin_x = NaN.
  *
  * cat_w4a4_linear_asym: the product of those activations with symmetric
  * INT4 weights,
@@ -243,6 +248,7 @@ int cat_int8_linear(const int8_t* codes_x, const float* s_x,
  * cat_weight_code_sums: host; rsum_out[o] = sum of row o's codes of the
  * packed INT4 [d_out x d_in/2] codes_w; d_in even.
  */
+size_t cat_transform_quant_asym_workspace_bytes(int64_t n, int64_t d, int64_t k);
 int cat_transform_quant_asym(const void* X, int x_dtype, int64_t n, int64_t d,
                              const void* T, int t_dtype, int64_t k,
                              uint8_t* codes, float* s_x, float* zmin_x,

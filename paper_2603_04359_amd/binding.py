@@ -43,7 +43,8 @@ EXPORTED = (
     "cat_cov_workspace_bytes", "cat_cov_accumulate", "cat_transform_quant_workspace_bytes",
     "cat_transform_quant_flag_offset", "cat_transform_quant", "cat_transform_quant_noalloc_max_bytes",
     "cat_transform_quant_noalloc",
-    "cat_w4a4_linear", "cat_int8_linear", "cat_transform_quant_asym", "cat_w4a4_linear_asym",
+    "cat_w4a4_linear", "cat_int8_linear", "cat_transform_quant_asym_workspace_bytes",
+    "cat_transform_quant_asym", "cat_w4a4_linear_asym",
     "cat_weight_code_sums", "cat_sqnr_terms", "cat_transform_quant_full_workspace_bytes",
     "cat_transform_quant_full", "cat_full_hadamard_weights", "cat_sqnr_workspace_bytes", "cat_sqnr", "cat_build_transform",
     "cat_quantize_weights", "cat_last_error", "cat_version",
@@ -94,6 +95,8 @@ def lib() -> ctypes.CDLL:
     L.cat_w4a4_linear.restype = _int
     L.cat_int8_linear.argtypes = [_vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp]
     L.cat_int8_linear.restype = _int
+    L.cat_transform_quant_asym_workspace_bytes.argtypes = [_i64, _i64, _i64]
+    L.cat_transform_quant_asym_workspace_bytes.restype = _sz
     L.cat_transform_quant_asym.argtypes = [_vp, _int, _i64, _i64, _vp, _int, _i64, _vp, _vp, _vp,
                                            _vp, _sz, _vp]
     L.cat_transform_quant_asym.restype = _int
@@ -335,6 +338,10 @@ def cat_int8_linear(codes_x, s_x, codes_w, s_w, y_tilde, acc_out=None, stream=No
     _check("cat_int8_linear",
            lib().cat_int8_linear(pcx, psx, pcw, psw, n, d_in, d_out, py, pacc,
                                  _stream_ptr(stream)))
+
+
+def cat_transform_quant_asym_workspace_bytes(n: int, d: int, k: int) -> int:
+    return int(lib().cat_transform_quant_asym_workspace_bytes(n, d, k))
 
 
 def cat_transform_quant_asym(X, T, k: int, codes, s_x, zmin_x, workspace, stream=None):

@@ -87,6 +87,11 @@ extern "C" size_t cat_transform_quant_workspace_bytes(int64_t n, int64_t d, int6
     return catk::tq_workspace_bytes(n, d, k);
 }
 
+extern "C" size_t cat_transform_quant_asym_workspace_bytes(int64_t n, int64_t d, int64_t k) {
+    if (n < 1 || d < 1 || k < 1) return 0;
+    return catk::tq_asym_workspace_bytes(n, d, k);
+}
+
 extern "C" size_t cat_transform_quant_flag_offset(int64_t n, int64_t d, int64_t k) {
     (void)k;
     if (n < 1 || d < 1) return 0;
@@ -208,7 +213,7 @@ extern "C" int cat_transform_quant_asym(const void* X, int x_dtype, int64_t n, i
         if (!cat::aligned16(X) || !cat::aligned16(T) || !cat::aligned16(codes) ||
             !cat::aligned16(s_x) || !cat::aligned16(zmin_x))
             return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": pointers must be 16-byte aligned");
-        if (!workspace || workspace_bytes < cat_transform_quant_workspace_bytes(n, d, k))
+        if (!workspace || workspace_bytes < cat_transform_quant_asym_workspace_bytes(n, d, k))
             return fail(CAT_ERR_WORKSPACE, std::string(fn) + ": workspace missing or too small");
         if (!cat::aligned16(workspace))
             return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": workspace must be 16-byte aligned");

@@ -686,6 +686,7 @@ static_assert(kFqAhead < kFqStages, "a stage is refilled only after its tile is 
 
 struct TqFusedWs {
     uint64_t* pmax;       // P words, then F words (see above)
+    uint64_t* pmin;       // asymmetric codes: the same for the complemented minimum keys
     uint32_t* flag;       // timeout flag (0 = fine)
     // The call's tag: the host's when tag_word is NULL, else the word a
     // preceding tq_device_tag_kernel wrote (calls captured into a graph,
@@ -744,6 +745,42 @@ __device__ __forceinline__ u32x2 fq_quant16(const f32x16& z, float inv) {
     return out;
 }
 
+// Asymmetric INT4 codes of 16 consecutive channels: q = rint(clamp(fl(fl(z -
+// zmin) * inv), 0, 15)) (clamping first gives the same integer, as both
+// bounds are integers), stored as q - 8 = q ^ 8, channel 2m in the low
+// nibble of byte m.
+__device__ __forceinline__ u32x2 fq_quant16_asym(const f32x16& z, float zmin, float inv) {
+    uint32_t w[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+        float u = (z[r] - zmin) * inv;
+        u = __builtin_amdgcn_fmed3f(u, 0.0f, 15.0f);
+        w[r] = __float_as_uint(u + 12582912.0f) ^ 8u;
+    }
+    u32x2 out;
+#pragma unroll
+    for (int hw = 0; hw < 2; ++hw) {
+        const uint32_t* v = w + 8 * hw;
+        const uint32_t ev = fq_bytes(v[0], v[2], v[4], v[6]);
+        const uint32_t od = fq_bytes(v[1], v[3], v[5], v[7]);
+        out[hw] = (ev & 0x0F0F0F0Fu) | ((od << 4) & 0xF0F0F0F0u);
+    }
+    return out;
+}
+
+// Asymmetric scale from a row's exchanged keys, as asym_scale, except that
+// a range that is NaN (keys of a timed-out exchange are all ones, which
+// decode to NaN) keeps s = NaN instead of becoming a zero scale.
+__device__ __forceinline__ void fq_asym_scale(uint32_t kmax, uint32_t kmin_c, float& zmin, float& s,
+                                              float& inv) {
+    const float zmax = fkey_value(kmax);
+    zmin = fkey_value(~kmin_c);
+    const float r = zmax - zmin;
+    const bool nz = !(r <= 0.0f);
+    s = nz ? __fdiv_rn(r, 15.0f) : 0.0f;
+    inv = nz ? __fdiv_rn(15.0f, r) : 0.0f;
+}
+
 // 6- and 8-bit widths: one int8 per channel, channel m in byte m.
 template <int QM>
 __device__ __forceinline__ u32x4 fq_quant16_i8(const f32x16& z, float inv) {
@@ -786,11 +823,12 @@ __device__ __forceinline__ void fq_wait_copies(int later) {
     }
 }
 
-template <int QM, int NB>
+template <int QM, int NB, bool ASYM>
 __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ T, int64_t n, int64_t d,
     int64_t R, TqFusedWs ws, uint32_t host_tag, uint8_t* __restrict__ codes,
-    float* __restrict__ s_x) {
+    float* __restrict__ s_x, float* __restrict__ zmin_x) {
+    static_assert(!ASYM || QM == 7, "asymmetric codes are INT4");
     const uint32_t tag = ws.tag_word ? __hip_atomic_load(ws.tag_word, __ATOMIC_RELAXED,
                                                          __HIP_MEMORY_SCOPE_AGENT)
                                      : host_tag;
@@ -803,6 +841,11 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
     static_assert(NB >= 16 && NB <= kWave && kFqTT % NB == 0, "blocks per token-tile row");
     constexpr int TPO = kFqTT / NB;               // tokens each workgroup reduces per tile
     __shared__ uint32_t fred[2][TPO];             // reduced row maxima of the owned tokens
+    // asymmetric codes: red, gat and fred hold maximum keys, and these the
+    // complemented minimum keys
+    __shared__ uint32_t redn[ASYM ? 2 : 1][ASYM ? kFqTT : 1];
+    __shared__ uint32_t gatn[ASYM ? kFqTT : 1];
+    __shared__ uint32_t fredn[ASYM ? 2 : 1][ASYM ? TPO : 1];
 
     const int64_t b = blockIdx.x % NB;
     const int64_t r0 = blockIdx.x / NB;
@@ -821,9 +864,13 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
         const uint64_t hi = static_cast<uint64_t>(tag) << 32;
         const int64_t n16 = (n + 15) / 16 * 16;
         uint64_t* const fw = ws.pmax + n16 * NB;
+        uint64_t* const fwn = ASYM ? ws.pmin + n16 * NB : nullptr;
         auto clampt = [&](int64_t t) { return t < n ? t : n - 1; };
         auto p_word = [&](int64_t t, int64_t j) {
             return ws.pmax + (t >> 4) * (NB * 16) + j * 16 + (t & 15);
+        };
+        auto pn_word = [&](int64_t t, int64_t j) {
+            return ws.pmin + (t >> 4) * (NB * 16) + j * 16 + (t & 15);
         };
         auto store = [&](uint64_t* a, uint32_t m) {
             __hip_atomic_store(a, hi | m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -834,20 +881,29 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
                 lds_barrier();                                        // A
                 if (it >= 2 && it - 2 < nt) {
                     const int64_t t = tile0(it - 2) + TPO * b + lane;
-                    if (lane < TPO && t < n) store(fw + t, fred[it & 1][lane < TPO ? lane : 0]);
+                    const int o = lane < TPO ? lane : 0;
+                    if (lane < TPO && t < n) {
+                        store(fw + t, fred[it & 1][o]);
+                        if constexpr (ASYM) store(fwn + t, fredn[it & 1][o]);
+                    }
                 }
                 lds_barrier();                                        // F
                 if (it < nt) {
                     const int64_t t = tile0(it) + lane;
                     const uint32_t mm = max(red[0][lane], red[1][lane]);
                     if (t < n) store(p_word(t, b), mm);
+                    if constexpr (ASYM) {
+                        const uint32_t mn = max(redn[0][lane], redn[1][lane]);
+                        if (t < n) store(pn_word(t, b), mn);
+                    }
                 }
             }
             return;
         }
         // gather: takes F of tile it-3 after A, then requests P of tile
         // it-1; takes P after F and reduces it, then requests F of tile
-        // it-2.  Every read has a phase in flight, and only one read is
+        // it-2.  Every read has a phase in flight, and only one read (two
+        // for asymmetric codes, the maximum and the minimum key) is
         // outstanding when it is waited for.  A word that is not there yet
         // is re-read (bounded).
         auto load = [&](const uint64_t* a) {
@@ -856,11 +912,13 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
         // A wait that runs out yields a quiet NaN: as bits it exceeds every
         // finite maximum, so it survives both reduction levels, and the
         // tokens concerned get s_x = NaN instead of a silently wrong scale.
+        // Asymmetric keys take all ones instead: the largest key, which
+        // decodes to NaN both as a maximum and, complemented, as a minimum.
         auto await = [&](uint64_t v, const uint64_t* a) {
             for (uint32_t polls = 0; (v >> 32) != tag;) {
                 if (++polls >= kTqSpinLimit) {
                     __hip_atomic_store(ws.flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                    return 0x7FC00000u;
+                    return ASYM ? 0xFFFFFFFFu : 0x7FC00000u;
                 }
                 __builtin_amdgcn_s_sleep(1);
                 v = load(a);
@@ -872,25 +930,54 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
         auto p_addr = [&](int64_t j) {
             return p_word(clampt(tile0(j) + TPO * b + lane / NB), lane % NB);
         };
-        uint64_t fv = 0, pv = 0;
+        auto fn_addr = [&](int64_t j) { return fwn + clampt(tile0(j) + lane); };
+        auto pn_addr = [&](int64_t j) {
+            return pn_word(clampt(tile0(j) + TPO * b + lane / NB), lane % NB);
+        };
+        auto fold = [&](uint32_t m) {
+#pragma unroll
+            for (int x = 1; x < NB; x <<= 1)
+                m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), x)));
+            return m;
+        };
+        uint64_t fv = 0, pv = 0, fvn = 0, pvn = 0;
         for (int64_t it = 0; it < nsteps; ++it) {
             lds_barrier();                                            // A
             if (it >= kFqLag) {
                 const int64_t t = tile0(it - kFqLag) + lane;
                 const uint32_t m = await(fv, f_addr(it - kFqLag));
                 gat[lane] = m;
-                if (b == 0 && t < n) s_x[t] = __fdiv_rn(__uint_as_float(m), static_cast<float>(QM));
+                if constexpr (ASYM) {
+                    const uint32_t mn = await(fvn, fn_addr(it - kFqLag));
+                    gatn[lane] = mn;
+                    if (b == 0 && t < n) {
+                        float zmin, sc, inv;
+                        fq_asym_scale(m, mn, zmin, sc, inv);
+                        s_x[t] = sc;
+                        zmin_x[t] = zmin;
+                    }
+                } else {
+                    if (b == 0 && t < n)
+                        s_x[t] = __fdiv_rn(__uint_as_float(m), static_cast<float>(QM));
+                }
             }
-            if (it >= 1 && it <= nt) pv = load(p_addr(it - 1));
+            if (it >= 1 && it <= nt) {
+                pv = load(p_addr(it - 1));
+                if constexpr (ASYM) pvn = load(pn_addr(it - 1));
+            }
             lds_barrier();                                            // F
             if (it >= 1 && it <= nt) {
-                uint32_t m = await(pv, p_addr(it - 1));
-#pragma unroll
-                for (int x = 1; x < NB; x <<= 1)
-                    m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), x)));
+                const uint32_t m = fold(await(pv, p_addr(it - 1)));
                 if (lane % NB == 0) fred[(it + 1) & 1][lane / NB] = m;
+                if constexpr (ASYM) {
+                    const uint32_t mn = fold(await(pvn, pn_addr(it - 1)));
+                    if (lane % NB == 0) fredn[(it + 1) & 1][lane / NB] = mn;
+                }
             }
-            if (it + 1 >= kFqLag && it + 1 < nsteps) fv = load(f_addr(it + 1 - kFqLag));
+            if (it + 1 >= kFqLag && it + 1 < nsteps) {
+                fv = load(f_addr(it + 1 - kFqLag));
+                if constexpr (ASYM) fvn = load(fn_addr(it + 1 - kFqLag));
+            }
         }
         return;
     }
@@ -957,18 +1044,48 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
                 acc[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(tf[g][s]), as_bf16x8(xf),
                                                                  acc[g], 0, 0, 0);
         }
-        uint32_t m = max(fq_absmax16(acc[0]), fq_absmax16(acc[1]));
-        m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), 32)));
-        if (h == 0) red[rh][tok] = m;
+        if constexpr (ASYM) {
+            // order-preserving keys: the maximum, and the complemented minimum
+            uint32_t mx = 0, mn = 0;
+#pragma unroll
+            for (int g = 0; g < 2; ++g)
+#pragma unroll
+                for (int q = 0; q < 16; ++q) {
+                    const uint32_t kq = fkey(acc[g][q]);
+                    mx = max(mx, kq);
+                    mn = max(mn, ~kq);
+                }
+            mx = max(mx, static_cast<uint32_t>(__shfl_xor(static_cast<int>(mx), 32)));
+            mn = max(mn, static_cast<uint32_t>(__shfl_xor(static_cast<int>(mn), 32)));
+            if (h == 0) {
+                red[rh][tok] = mx;
+                redn[rh][tok] = mn;
+            }
+        } else {
+            uint32_t m = max(fq_absmax16(acc[0]), fq_absmax16(acc[1]));
+            m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), 32)));
+            if (h == 0) red[rh][tok] = m;
+        }
     };
     auto quant = [&](int64_t it, const f32x16 (&acc)[2]) {
         const int64_t t = tile0(it) + tok;
-        const float amax = __uint_as_float(gat[tok]);
-        const float inv = amax > 0.0f ? __fdiv_rn(static_cast<float>(QM), amax) : 0.0f;
+        float inv, zmin = 0.0f;
+        if constexpr (ASYM) {
+            float sc;
+            fq_asym_scale(gat[tok], gatn[tok], zmin, sc, inv);
+        } else {
+            const float amax = __uint_as_float(gat[tok]);
+            inv = amax > 0.0f ? __fdiv_rn(static_cast<float>(QM), amax) : 0.0f;
+        }
 #pragma unroll
         for (int g = 0; g < 2; ++g) {
             // lane (token, h) holds channels (2 rh + g) 32 + 16 h .. + 15
-            if constexpr (QM == 7) {
+            if constexpr (ASYM) {
+                const u32x2 c = fq_quant16_asym(acc[g], zmin, inv);
+                if (t < n)
+                    *reinterpret_cast<u32x2*>(codes + t * (d / 2) + b * (K / 2) +
+                                              (2 * rh + g) * 16 + 8 * h) = c;
+            } else if constexpr (QM == 7) {
                 const u32x2 c = fq_quant16(acc[g], inv);
                 if (t < n)
                     *reinterpret_cast<u32x2*>(codes + t * (d / 2) + b * (K / 2) +
@@ -1040,28 +1157,6 @@ __device__ __forceinline__ void tg_wait_copies(int later) {
     else wait_vmcnt<0>();
 }
 
-// Asymmetric INT4 codes of 16 consecutive channels: q = rint(clamp(fl(fl(z -
-// zmin) * inv), 0, 15)) (clamping first gives the same integer, as both
-// bounds are integers), stored as q - 8 = q ^ 8, channel 2m in the low
-// nibble of byte m.
-__device__ __forceinline__ u32x2 fq_quant16_asym(const f32x16& z, float zmin, float inv) {
-    uint32_t w[16];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-        float u = (z[r] - zmin) * inv;
-        u = __builtin_amdgcn_fmed3f(u, 0.0f, 15.0f);
-        w[r] = __float_as_uint(u + 12582912.0f) ^ 8u;
-    }
-    u32x2 out;
-#pragma unroll
-    for (int hw = 0; hw < 2; ++hw) {
-        const uint32_t* v = w + 8 * hw;
-        const uint32_t ev = fq_bytes(v[0], v[2], v[4], v[6]);
-        const uint32_t od = fq_bytes(v[1], v[3], v[5], v[7]);
-        out[hw] = (ev & 0x0F0F0F0Fu) | ((od << 4) & 0xF0F0F0F0u);
-    }
-    return out;
-}
 
 // QUANT false: pass 1 (row maxima into ws[t], or for ASYM the max key into
 // ws[t] and the complemented min key into ws[n + t]).  QUANT true: pass 2
@@ -1336,12 +1431,23 @@ hipError_t launch_tq_ring(const uint16_t* X, int64_t n, int64_t d, const uint16_
 // maximum per token, or the asymmetric path's two 32-bit keys per token).
 // The two regions never overlap, so words one path leaves behind are never
 // read by the other: the asymmetric keys can have bit 31 set and could
-// otherwise pass for a tagged word.
+// otherwise pass for a tagged word.  The asymmetric entry point's workspace
+// adds a third region (see tq_asym_min_offset).
 static int64_t tq_nbj_max(int64_t d) { return d / 128 > 1 ? d / 128 : 1; }
 static size_t tq_flag_offset(int64_t n, int64_t d) {
     return static_cast<size_t>((n + 15) / 16 * 16 * 8 * (tq_nbj_max(d) + 1));
 }
 static size_t tq_twopass_offset(int64_t n, int64_t d) { return tq_flag_offset(n, d) + 256; }
+// asymmetric single pass: the minimum keys' P and F words, laid out like the
+// maximum keys', after the two-pass region
+static size_t tq_asym_min_offset(int64_t n, int64_t d) {
+    return tq_twopass_offset(n, d) + static_cast<size_t>(n) * 8;
+}
+size_t tq_asym_workspace_bytes(int64_t n, int64_t d, int64_t k) {
+    (void)k;
+    if (n < 1) return 0;
+    return tq_asym_min_offset(n, d) + tq_flag_offset(n, d);
+}
 size_t tq_flag_offset_bytes(int64_t n, int64_t d) { return tq_flag_offset(n, d); }
 size_t tq_workspace_bytes(int64_t n, int64_t d, int64_t k) {
     (void)k;
@@ -1356,7 +1462,7 @@ static uint32_t next_tq_tag() {
 
 // Resident workgroups of tq_fused_kernel on a device (CUs x blocks per CU
 // by its register and LDS use), queried once per device.
-template <int QM, int NB>
+template <int QM, int NB, bool ASYM>
 static hipError_t tq_fused_resident(int dev, int64_t& resident) {
     constexpr int kMaxDev = 64;
     static std::atomic<int64_t> cache[kMaxDev];   // 0 = not yet known (one table per kernel)
@@ -1367,7 +1473,8 @@ static hipError_t tq_fused_resident(int dev, int64_t& resident) {
     int cus = 0, per_cu = 0;
     hipError_t err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (err != hipSuccess) return err;
-    err = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, tq_fused_kernel<QM, NB>, kFqThreads, 0);
+    err = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, tq_fused_kernel<QM, NB, ASYM>,
+                                                       kFqThreads, 0);
     if (err != hipSuccess) return err;
     resident = static_cast<int64_t>(per_cu) * cus;
     if (dev >= 0 && dev < kMaxDev && resident > 0) cache[dev].store(resident, std::memory_order_relaxed);
@@ -1381,16 +1488,16 @@ static hipError_t tq_fused_resident(int dev, int64_t& resident) {
 // The grid never exceeds the resident capacity, so every workgroup is on
 // the device together once other work has drained, and a peer a workgroup
 // waits for is always running or about to run.
-template <int QM, int NB>
+template <int QM, int NB, bool ASYM>
 static hipError_t launch_tq_fused_nb(const uint16_t* X, int64_t n, int64_t d, const uint16_t* T,
                                      uint8_t* codes, float* s_x, uint8_t* ws, hipStream_t stream,
-                                     bool& launched) {
+                                     bool& launched, float* zmin_x) {
     launched = false;
     int dev = 0;
     hipError_t err = hipGetDevice(&dev);
     if (err != hipSuccess) return err;
     int64_t resident = 0;
-    err = tq_fused_resident<QM, NB>(dev, resident);
+    err = tq_fused_resident<QM, NB, ASYM>(dev, resident);
     if (err != hipSuccess) return err;
     const int64_t ntiles = (n + kFqTT - 1) / kFqTT;
     if (NB > resident) return hipSuccess;
@@ -1399,6 +1506,7 @@ static hipError_t launch_tq_fused_nb(const uint16_t* X, int64_t n, int64_t d, co
     if (R < 1) R = 1;
     TqFusedWs w;
     w.pmax = reinterpret_cast<uint64_t*>(ws);
+    w.pmin = ASYM ? reinterpret_cast<uint64_t*>(ws + tq_asym_min_offset(n, d)) : nullptr;
     w.flag = reinterpret_cast<uint32_t*>(ws + tq_flag_offset(n, d));
     w.tag_word = nullptr;
     uint32_t tag = 0;
@@ -1416,23 +1524,26 @@ static hipError_t launch_tq_fused_nb(const uint16_t* X, int64_t n, int64_t d, co
     } else {
         tag = next_tq_tag();
     }
-    hipLaunchKernelGGL((tq_fused_kernel<QM, NB>), dim3(static_cast<uint32_t>(NB * R)),
-                       dim3(kFqThreads), 0, stream, X, T, n, d, R, w, tag, codes, s_x);
+    hipLaunchKernelGGL((tq_fused_kernel<QM, NB, ASYM>), dim3(static_cast<uint32_t>(NB * R)),
+                       dim3(kFqThreads), 0, stream, X, T, n, d, R, w, tag, codes, s_x, zmin_x);
     err = hipGetLastError();
     if (err != hipSuccess) return err;
     launched = true;
     return hipSuccess;
 }
 
-template <int QM>
+template <int QM, bool ASYM = false>
 hipError_t launch_tq_fused(const uint16_t* X, int64_t n, int64_t d, const uint16_t* T,
                            uint8_t* codes, float* s_x, uint8_t* ws, hipStream_t stream,
-                           bool& launched) {
+                           bool& launched, float* zmin_x = nullptr) {
     launched = false;
     switch (d) {
-        case 2048: return launch_tq_fused_nb<QM, 16>(X, n, d, T, codes, s_x, ws, stream, launched);
-        case 4096: return launch_tq_fused_nb<QM, 32>(X, n, d, T, codes, s_x, ws, stream, launched);
-        case 8192: return launch_tq_fused_nb<QM, 64>(X, n, d, T, codes, s_x, ws, stream, launched);
+        case 2048:
+            return launch_tq_fused_nb<QM, 16, ASYM>(X, n, d, T, codes, s_x, ws, stream, launched, zmin_x);
+        case 4096:
+            return launch_tq_fused_nb<QM, 32, ASYM>(X, n, d, T, codes, s_x, ws, stream, launched, zmin_x);
+        case 8192:
+            return launch_tq_fused_nb<QM, 64, ASYM>(X, n, d, T, codes, s_x, ws, stream, launched, zmin_x);
         default: return hipSuccess;
     }
 }
@@ -1533,12 +1644,22 @@ static hipError_t launch_tq_generic_asym(const XT* X, int64_t n, int64_t d, cons
     return hipGetLastError();
 }
 
-// Asymmetric INT4: two passes (row max and min keys, then codes), on the
-// ring kernels for bf16 with k in {128, 256, 512}, else the vector ALU.
+// Asymmetric INT4: the single-pass kernel for bf16 with k = 128 and d =
+// 2048, 4096 or 8192 (row max and min keys exchanged as two words); else two
+// passes (row max and min keys, then codes): the group kernels for bf16
+// with k <= 256 and d a multiple of 256, the ring kernels for bf16 with k in
+// {128, 256, 512} otherwise, else the vector ALU.
 hipError_t launch_transform_quant_asym(const void* X, int x_bf16, int64_t n, int64_t d,
                                        const void* T, int t_bf16, int64_t k, uint8_t* codes,
                                        float* s_x, float* zmin_x, uint32_t* ws,
                                        hipStream_t stream) {
+    if (x_bf16 && t_bf16 && k == 128) {
+        bool launched = false;
+        const hipError_t e = launch_tq_fused<7, true>(
+            static_cast<const uint16_t*>(X), n, d, static_cast<const uint16_t*>(T), codes, s_x,
+            reinterpret_cast<uint8_t*>(ws), stream, launched, zmin_x);
+        if (e != hipSuccess || launched) return e;
+    }
     ws = reinterpret_cast<uint32_t*>(reinterpret_cast<uint8_t*>(ws) + tq_twopass_offset(n, d));
     hipLaunchKernelGGL(fill_zero_u32_kernel, dim3(static_cast<uint32_t>((2 * n + 255) / 256)),
                        dim3(256), 0, stream, ws, 2 * n);

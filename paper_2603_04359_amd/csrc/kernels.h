@@ -25,6 +25,9 @@ hipError_t launch_sqnr(const float* y, const float* yt, int64_t count, double* p
 size_t tq_workspace_bytes(int64_t n, int64_t d, int64_t k);
 // byte offset of the 32-bit timeout flag inside that workspace
 size_t tq_flag_offset_bytes(int64_t n, int64_t d);
+// the asymmetric entry point's workspace: tq_workspace_bytes plus the
+// single pass's minimum-key words
+size_t tq_asym_workspace_bytes(int64_t n, int64_t d, int64_t k);
 hipError_t launch_transform_quant(const void* X, int x_bf16, int64_t n, int64_t d,
                                   const void* T, int t_bf16, int64_t k, int bits,
                                   uint8_t* codes, float* s_x, uint32_t* amax_ws,

@@ -92,7 +92,7 @@ class LayerRunner:
         k = layer["k"]
         self.codes4 = torch.empty((n, d_in // 2), dtype=torch.uint8, device=device)
         self.s_x = torch.empty(n, dtype=torch.float32, device=device)
-        self.ws_q = torch.empty(max(16, B.cat_transform_quant_workspace_bytes(n, d_in, k)),
+        self.ws_q = torch.empty(max(16, B.cat_transform_quant_asym_workspace_bytes(n, d_in, k)),
                                 dtype=torch.uint8, device=device)
         self.y_t = torch.empty((n, d_out), dtype=torch.float32, device=device)
         self.ws_s = torch.empty(B.cat_sqnr_workspace_bytes(n * d_out), dtype=torch.uint8,

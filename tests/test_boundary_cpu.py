@@ -131,7 +131,7 @@ def test_binding_rejects_cpu_tensors():
 
 def test_asymmetric_entry_points_invalid_args():
     L = cat.lib()
-    ws = L.cat_transform_quant_workspace_bytes(8, 64, 16)
+    ws = L.cat_transform_quant_asym_workspace_bytes(8, 64, 16)
     f = L.cat_transform_quant_asym
     assert f(P, 1, 8, 64, P, 1, 16, P, P, None, P, ws, None) == B.CAT_ERR_INVALID_ARG
     assert f(P, 1, 8, 64, P, 1, 12, P, P, P, P, ws, None) == B.CAT_ERR_INVALID_ARG

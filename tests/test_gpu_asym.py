@@ -21,7 +21,7 @@ def _tq_asym(X, T, k, x_dtype, t_dtype):
     codes = torch.empty((n, d // 2), dtype=torch.uint8, device="cuda")
     s_x = torch.empty(n, dtype=torch.float32, device="cuda")
     zmin = torch.empty(n, dtype=torch.float32, device="cuda")
-    ws = torch.empty(cat.cat_transform_quant_workspace_bytes(n, d, k), dtype=torch.uint8,
+    ws = torch.empty(cat.cat_transform_quant_asym_workspace_bytes(n, d, k), dtype=torch.uint8,
                      device="cuda")
     cat.cat_transform_quant_asym(dev(X, x_dtype), dev(T, t_dtype), k, codes, s_x, zmin, ws)
     return o.unpack_int4(host(codes)).astype(np.int16) + 8, host(s_x), host(zmin)
@@ -61,6 +61,7 @@ def _check_asym(q, s, m, X, T, label):
     (4096, 128, 300, "bf16", "bf16"), (1024, 256, 129, "bf16", "bf16"),
     (1024, 512, 65, "bf16", "bf16"), (512, 64, 70, "bf16", "bf16"), (256, 32, 33, "f32", "f32"),
     (14336, 256, 130, "bf16", "bf16"), (768, 32, 65, "bf16", "bf16"), (640, 128, 97, "bf16", "bf16"),
+    (8192, 128, 130, "bf16", "bf16"), (2048, 128, 257, "bf16", "bf16"), (4096, 128, 3, "bf16", "bf16"),
 ])
 def test_transform_quant_asym_matches_oracle(d, k, n, x_dtype, t_dtype):
     say(f"tq asym d={d} k={k} n={n} {x_dtype}/{t_dtype}")
@@ -76,13 +77,15 @@ def test_transform_quant_asym_matches_oracle(d, k, n, x_dtype, t_dtype):
     assert s[1] == 0 and m[1] == 0 and not q[1].any()
 
 
-def test_transform_quant_asym_identity_constant_rows_exact():
+@pytest.mark.parametrize("d", [512, 4096])
+def test_transform_quant_asym_identity_constant_rows_exact(d):
     # T = I: z = x exactly on both sides, so codes, scales and minima are
     # identical; a constant row is reconstructed exactly by its minimum
-    say("tq asym identity bf16 k=128")
-    X = wl.random_bf16_matrix(200, 512, seed=7, scale=2.0).astype(np.float64)
+    # (d = 4096: the single-pass kernel, d = 512: two passes)
+    say(f"tq asym identity bf16 k=128 d={d}")
+    X = wl.random_bf16_matrix(200, d, seed=7, scale=2.0).astype(np.float64)
     X[3] = 1.5
-    T = np.stack([np.eye(128)] * 4)
+    T = np.stack([np.eye(128)] * (d // 128))
     q, s, m = _tq_asym(X, T, 128, "bf16", "bf16")
     q_or, s_or, m_or = o.transform_quant_asym(X, T, 4)
     assert np.array_equal(q, q_or)
@@ -143,7 +146,7 @@ def test_end_to_end_asym_vs_sym_sqnr():
     codes = torch.empty((n, d // 2), dtype=torch.uint8, device="cuda")
     s_x = torch.empty(n, dtype=torch.float32, device="cuda")
     zmin = torch.empty(n, dtype=torch.float32, device="cuda")
-    ws = torch.empty(cat.cat_transform_quant_workspace_bytes(n, d, k), dtype=torch.uint8,
+    ws = torch.empty(cat.cat_transform_quant_asym_workspace_bytes(n, d, k), dtype=torch.uint8,
                      device="cuda")
     y = o.reference_output(X, W).astype(np.float32)
     dy = dev(y, "f32")
@@ -169,12 +172,14 @@ def test_end_to_end_asym_vs_sym_sqnr():
     assert asym_db > sym_db
 
 
-def test_asym_pair_graph_replays_match_eager():
-    # the asymmetric pair (key clear, two transform+quant passes, GEMM)
-    # captured once and replayed with new activations, against eager calls
+@pytest.mark.parametrize("d", [1024, 4096])
+def test_asym_pair_graph_replays_match_eager(d):
+    # the asymmetric pair captured once and replayed with new activations,
+    # against eager calls: d = 1024 runs the key clear and two passes,
+    # d = 4096 the single pass (a device tag per replay)
     torch = torch_mod()
-    n, d, d_out, k = 300, 1024, 384, 128
-    say("asymmetric pair under graph capture: 3 replays vs eager")
+    n, d_out, k = 300, 384, 128
+    say(f"asymmetric pair under graph capture d={d}: 3 replays vs eager")
     rng = np.random.default_rng(71)
     T = o.round_storage(rng.standard_normal((d // k, k, k)) / np.sqrt(k), "bf16")
     dT = dev(T, "bf16")
@@ -190,7 +195,7 @@ def test_asym_pair_graph_replays_match_eager():
                     s_x=torch.empty(n, dtype=torch.float32, device="cuda"),
                     zmin=torch.empty(n, dtype=torch.float32, device="cuda"),
                     yt=torch.empty((n, d_out), dtype=torch.float32, device="cuda"),
-                    ws=torch.empty(cat.cat_transform_quant_workspace_bytes(n, d, k),
+                    ws=torch.empty(cat.cat_transform_quant_asym_workspace_bytes(n, d, k),
                                    dtype=torch.uint8, device="cuda"))
 
     def pair(dX, b):

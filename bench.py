@@ -196,6 +196,57 @@ def copy_calibration(mib):
     print(json.dumps({"copy_calibration_bytes": mib << 20, "launches": 5}), flush=True)
 
 
+# --------------------------------------------- measured reference rates
+def reference_rates(torch, n, d_in, d_out, iters=10):
+    """Measured ceilings beside the published peaks, none of them part of
+    the path: a 1 GiB device copy (HBM), hipBLASLt's int8 GEMM at the
+    metric layer's shape through torch._int_mm (int8 operands, int32
+    output, no dequantization) and a bf16 X^T X matmul at the batch's Sigma_x
+    shape through torch.mm."""
+    dev = torch.device("cuda:0")
+    out = {}
+
+    def timed(fn):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(iters + 1)]
+        for i in range(iters):
+            ev[i].record()
+            fn()
+        ev[iters].record()
+        torch.cuda.synchronize()
+        return stats([ev[i].elapsed_time(ev[i + 1]) for i in range(iters)])
+
+    src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    st = timed(lambda: dst.copy_(src))
+    out["hbm_copy"] = {"ms": st, "GBps": 2.0 * (1 << 30) / (st["median"] * 1e-3) / 1e9,
+                       "bytes": "1 GiB read + 1 GiB written per call"}
+    del src, dst
+    g = torch.Generator(device=dev)
+    g.manual_seed(1)
+    a = torch.randint(-7, 8, (n, d_in), dtype=torch.int8, device=dev, generator=g)
+    b = torch.randint(-7, 8, (d_in, d_out), dtype=torch.int8, device=dev, generator=g)
+    try:
+        st = timed(lambda: torch._int_mm(a, b))
+        out["int8_gemm_hipblaslt"] = {"ms": st, "TOPS": gemm_ops_of(n, d_in, d_out) /
+                                      (st["median"] * 1e-3) / 1e12,
+                                      "shape": f"{n}x{d_in} @ {d_in}x{d_out}, int8 -> int32"}
+    except RuntimeError as e:            # a torch build without the int8 path
+        out["int8_gemm_hipblaslt"] = {"error": str(e)[:200]}
+    del a, b
+    x = torch.randn((n, d_in), dtype=torch.float32, device=dev, generator=g).to(torch.bfloat16)
+    xt = x.t().contiguous()
+    st = timed(lambda: torch.mm(xt, x))
+    out["bf16_xtx_hipblaslt"] = {"ms": st, "TFLOPS": 2.0 * n * d_in * d_in /
+                                 (st["median"] * 1e-3) / 1e12,
+                                 "shape": f"{d_in}x{n} @ {n}x{d_in}, bf16 (full square)"}
+    del x, xt
+    torch.cuda.empty_cache()
+    return out
+
+
 # ------------------------------------------------------------ GPU clocks
 class ClockSampler:
     """Samples the graphics and memory clocks of this process's GPU through
@@ -557,6 +608,8 @@ def main():
     if not args.no_report:
         widened(rec, torch, cat, B, P, layer, run, Xs, Ys, lay, n, d_in, d_out, k, tdt,
                 tq_bytes, gemm_ops, args.wide_steps)
+        log("[bench] measured reference rates (device copy, hipBLASLt int8 GEMM, bf16 X^T X)")
+        rec["references"] = reference_rates(torch, n, d_in, d_out)
     if not args.no_report and not args.no_configs:
         # free the metric layer before the other configurations
         del run, Xs, Ys, X0, sigma, ws_c

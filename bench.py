@@ -78,7 +78,7 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-GEMM_SOURCES = ("k_w4a4.hip", "device_common.h", "kernels.h")
+GEMM_SOURCES = ("k_w4a4.hip", "device_common.h")   # the GEMM kernel and its device helpers
 
 
 def kernel_sources_sha():

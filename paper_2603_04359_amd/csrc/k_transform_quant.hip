@@ -11,22 +11,31 @@
 // Every kernel below takes qmax as the template parameter QM.
 //
 // The row maximum couples all d/k blocks of a token, while reuse of T_b
-// wants many tokens per workgroup.  The kernels therefore split the work
-// by (block, token tile) and run two passes over the same tiles:
-//   pass 1 (amax)   computes z and folds max|z| into a per-token word with
-//                   an atomic max on the float's bit pattern (all values
-//                   are non-negative, so unsigned order = float order);
-//   pass 2 (quant)  recomputes z with the identical instruction sequence,
+// wants many tokens per workgroup.  The work is split by (block, token
+// tile), and the kernels differ in how a token's blocks meet:
+//   single pass     (bf16, k = 128, d = 2048, 4096, 8192; tq_fused_kernel)
+//                   one launch reads X once; workgroups exchange per-token
+//                   block maxima through the workspace in two levels;
+//   two passes      (every other case) run over the same tiles:
+//     pass 1 (amax) computes z and folds max|z| into a per-token word
+//                   (LDS atomics, then one atomic max per token on the
+//                   float's bit pattern: all values are non-negative, so
+//                   unsigned order = float order);
+//     pass 2 (quant) recomputes z with the identical instruction sequence,
 //                   reads the finished row maximum and writes packed codes.
-// A fill kernel clears the per-token words first (no hipMemset, so the
-// sequence can be captured in a graph).
+//   A fill kernel clears the per-token words first (no hipMemset, so the
+//   sequence can be captured in a graph).
+// Two-pass kernels, by case: tq_group_kernel (bf16, k <= 256, d a multiple
+// of 256), tq_ring_kernel (bf16 k = 512, and k = 128 or 256 otherwise),
+// tq_mfma_kernel (bf16 k = 32, 64 otherwise) and the vector-ALU kernels
+// (fp32 operands or other block sizes).  The asymmetric INT4 variant takes
+// the same routes with a row maximum and minimum, except that bf16 k = 32
+// and 64 off the group kernel's widths go to the vector ALU.
 //
-// bf16 path: v_mfma_f32_32x32x16_bf16 with A = rows of T_b (staged in LDS,
-// XOR-swizzled 16-byte units) and B = token rows of X (16-byte loads
-// straight from HBM), so Z^T tiles come out with one token per lane column;
-// the per-token maximum is a register max plus one lane swap, and codes are
-// packed 4 per lane, joined to 8 per dword with one lane swap.
-// fp32 (or small-k) path: plain fp32 FMA chains on the vector ALU.
+// bf16 kernels run v_mfma_f32_32x32x16_bf16 with A = rows of T_b and B =
+// token rows of X, so Z^T tiles come out with one token per lane column;
+// the per-token maximum is a register max plus one lane swap.  Where each
+// kernel keeps its operands (registers, LDS, DMA rings) is stated at it.
 #include <atomic>
 #include <type_traits>
 

@@ -142,8 +142,9 @@ int cat_cov_accumulate(const void* X, int x_dtype, int64_t n, int64_t d,
  * Capture: the call may be captured into a HIP graph and replayed (it
  *          enqueues kernels only; a captured call also enqueues a one-thread
  *          kernel that renews the exchange tag for every replay).
- * The d = 4096, k = 128 bf16 path runs one persistent launch whose
- * workgroups exchange row maxima through the workspace with bounded waits.
+ * The bf16 path with k = 128 and d = 2048, 4096 or 8192 runs one
+ * persistent launch whose workgroups exchange row maxima through the
+ * workspace with bounded waits.
  * Its grid never exceeds the device's resident capacity, so every wait ends
  * once the launch has the device; work from other streams that holds CUs
  * for seconds can still make a wait run out.  Then the tokens concerned get

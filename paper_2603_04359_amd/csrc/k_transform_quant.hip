@@ -626,18 +626,22 @@ __global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
 // ------------------------------------------------- single-pass variant
 // bf16, k = 128, d = 128 NB with NB = 16, 32 or 64 blocks, one launch, X
 // read once.  One workgroup per CU owns block b for the token tiles r,
-// r + R, ... (a tile is 64 tokens) and splits its eight waves by role:
-//   waves 0-3  compute: wave w multiplies rows 64 (w / 2) .. + 63 of T_b
-//              (held in registers) with tokens 32 (w % 2) .. + 31 of the
-//              tile, read from LDS;
-//   waves 4-5  copy: stream token tiles into an 8-stage LDS ring with
+// r + R, ... (a tile is 64 tokens) and splits its twelve waves by role:
+//   waves 0-7  compute: wave w multiplies the 32 rows 32 (w / 2) .. + 31 of
+//              T_b (staged in LDS once) with tokens 32 (w % 2) .. + 31 of
+//              the tile, read from LDS; two compute waves per SIMD, so one
+//              wave's rounding runs beside the other's MFMAs;
+//   waves 8-9  copy: stream token tiles into an LDS ring with
 //              global_load_lds_dwordx4, kFqAhead tiles ahead;
-//   wave 6     gather: reads the per-token maxima other workgroups published;
-//   wave 7     publish: writes this workgroup's per-token maxima.
+//   wave 10    gather: reads the per-token maxima other workgroups published;
+//   wave 11    publish: writes this workgroup's per-token maxima, and the
+//              codes and scales the compute waves leave in LDS (16-byte
+//              pieces, 64 contiguous bytes per token).
 // Each wave issues one kind of vector-memory traffic only, so every wait is
 // exact and no load waits for a store's acknowledgement: the copy waves
 // count their own copies, and the compiler tracks the loads of the gather
-// wave (stores of the others are never waited for).
+// wave (the compute waves issue no global memory operation after loading
+// T_b, and the stores of the publish wave are never waited for).
 //
 // The row maximum of a token needs all NB blocks, exchanged in two levels
 // through the workspace: every workgroup publishes its block maxima P(b, t)
@@ -656,16 +660,21 @@ __global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
 // ((t / 16) * NB + j) * 16 + t % 16 (16 tokens of a block fill one 128-byte
 // line), F(t) at NB n' + t (n' = n rounded up to 16).
 //
-// Step s has barriers A and F.  A to F: the compute waves multiply tile s
-// and leave per-wave maxima in LDS; the gather wave takes F of tile s-3
-// (requested one phase earlier) and requests P of tile s-1; the publish
-// wave writes F of tile s-2.  F to the next A: the compute waves quantize
-// tile s-3 from the accumulators they kept (four sets rotate); the publish
-// wave writes P of tile s; the gather wave reduces P of tile s-1 and
-// requests F of tile s-2.  Every device crossing thus has about a step.
-// Rows of T_b are permuted inside each 32-row MFMA group so that lane
-// (token, h) accumulates 16 consecutive output channels: its codes are 8
-// contiguous bytes, no cross-lane exchange.
+// Steps are separated by one workgroup barrier.  In step s the compute
+// waves multiply tile s and leave its per-token maxima in LDS while they
+// round tile s - L (L = kFqLag) from the accumulators they kept (seven
+// sets rotate); the publish wave writes P of tile s - 1, the codes of tile
+// s - L - 1 and, once the gather wave has reduced them, F of tile s - 3;
+// the gather wave takes the F words of tile s - L + 1 and the P words of
+// tile s - 3 it requested in the last step, reduces P, and requests P of
+// tile s - 2 and F of tile s - L + 2.  Every word is thus published a step
+// before it is first read and then has a whole step in flight: under a
+// full-rate stream a device-scope store takes about a microsecond to
+// become visible to a reader on another CU, and workgroups drift apart by
+// about as much, so a shorter lag makes reads find stale words and wait a
+// further round trip.  Rows of T_b are permuted inside each 32-row MFMA
+// group so that lane (token, h) accumulates 16 consecutive output
+// channels: its codes are 8 contiguous bytes, no cross-lane exchange.
 //
 // Progress: the grid never exceeds the device's resident capacity (see
 // launch_tq_fused) and every workgroup of a token-tile row visits its tiles
@@ -674,24 +683,21 @@ __global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
 // gather wave records a timeout flag and goes on with a NaN maximum, which
 // makes the affected scales NaN.
 constexpr uint32_t kTqSpinLimit = 1u << 22;
-constexpr int kFqCompute = 4;                   // compute waves
+constexpr int kFqCompute = 8;                   // compute waves
 constexpr int kFqCopy = 2;                      // copy waves
 constexpr int kFqThreads = (kFqCompute + kFqCopy + 2) * kWave;
-constexpr int kFqStages = 8;
 constexpr int kFqTT = 64;                       // tokens per tile
 constexpr int kFqU = 16;                        // 16-byte units per token row
 constexpr int kFqStage = kFqTT * kFqU;          // units per stage (16 KiB)
 constexpr int kFqCopyOps = kFqStage / (kFqCopy * kWave);   // copies per lane per tile
-constexpr int kFqLag = 3;                       // tile s is quantized in step s + kFqLag
-// Copies in flight per CU (kFqAhead tiles of 16 KiB).  Every load of this
-// CU, the exchange polls included, queues behind them: under a 6 TB/s
-// stream a store/poll round trip between two CUs of one XCD measures 3.1 us
-// with 16 KiB in flight per CU, 4.6 us with 32 KiB and 6 us with 64 KiB,
-// while the stream itself already reaches 5.9-6.1 TB/s at 16-32 KiB.  Three
-// tiles ahead (48 KiB) was 41.8 us per call against 43.6 us for seven.
-constexpr int kFqAhead = 3;
+constexpr int kFqLag = 6;                       // tile s is rounded in step s + kFqLag
+// Copies in flight per CU (kFqAhead tiles of 16 KiB): every load of the CU,
+// the exchange reads included, queues behind them, and 16-32 KiB per CU
+// already stream X at 5.9-6.1 TB/s.  Three tiles ahead measured the same.
+constexpr int kFqAhead = 2;
+constexpr int kFqStages = kFqAhead + 1;         // a stage is free once its tile is multiplied
 static_assert(kFqCopyOps * kFqAhead < 64, "copies in flight must fit the vmcnt range");
-static_assert(kFqAhead < kFqStages, "a stage is refilled only after its tile is multiplied");
+static_assert(kFqStages > kFqAhead, "a stage is refilled only after its tile is multiplied");
 
 struct TqFusedWs {
     uint64_t* pmax;       // P words, then F words (see above)
@@ -799,6 +805,22 @@ __device__ __forceinline__ u32x4 fq_quant16_i8(const f32x16& z, float inv) {
                  fq_bytes(w[8], w[9], w[10], w[11]), fq_bytes(w[12], w[13], w[14], w[15])};
 }
 
+// One code's rounding as in fq_round16 (symmetric) or fq_quant16_asym
+// (asymmetric, already offset by 8): the integer sits in the low bits.
+template <int QM, bool ASYM>
+__device__ __forceinline__ uint32_t fq_round1(float z, float inv, float zmin) {
+    if constexpr (ASYM) {
+        float u = (z - zmin) * inv;
+        u = __builtin_amdgcn_fmed3f(u, 0.0f, 15.0f);
+        return __float_as_uint(u + 12582912.0f) ^ 8u;
+    } else {
+        constexpr float q = static_cast<float>(QM);
+        float u = z * inv;
+        u = __builtin_amdgcn_fmed3f(u, -q, q);
+        return __float_as_uint(u + 12582912.0f);
+    }
+}
+
 // max |z| over 16 values, as float bits.  Read as signed ints, the largest
 // value is the largest positive (or, with none, the largest-magnitude
 // negative); read as unsigned, it is the largest-magnitude negative (or,
@@ -843,17 +865,25 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
                                      : host_tag;
     constexpr int K = 128;
     constexpr int NS = K / 16;          // 16-deep MFMA steps
-    static_assert(kFqTT == 64 && kFqCompute == 4, "compute waves: 2 token halves x 2 row halves");
+    constexpr int L = kFqLag;
+    static_assert(L == 6, "seven accumulator sets rotate");
+    static_assert(kFqTT == 64 && kFqCompute == 8, "compute waves: 2 token halves x 4 row groups");
+    constexpr int CB = QM == 7 ? K / 2 : K;       // code bytes per token and block
     __shared__ __attribute__((aligned(16))) u32x4 ring[kFqStages][kFqStage];
-    __shared__ uint32_t red[2][kFqTT];            // per-row-half maxima of the step's tile
-    __shared__ uint32_t gat[kFqTT];               // row maxima of the tile being quantized
+    // T_b in MFMA row order: LDS row p holds row (p & ~31) + fq_row(p & 31),
+    // 16-byte unit u at position u ^ tq_xswz(p)
+    __shared__ __attribute__((aligned(16))) u32x4 tl[K * kFqU];
+    __shared__ __attribute__((aligned(16))) uint8_t cbuf[2][kFqTT][CB];   // codes of a quantized tile
+    __shared__ float cscale[2][kFqTT];            // its s_x
+    __shared__ float czmin[ASYM ? 2 : 1][ASYM ? kFqTT : 1];
+    __shared__ uint32_t red[2][4][kFqTT];         // per-row-group maxima of a step's tile
+    __shared__ uint32_t gat[2][kFqTT];            // row maxima of a tile to quantize
     static_assert(NB >= 16 && NB <= kWave && kFqTT % NB == 0, "blocks per token-tile row");
     constexpr int TPO = kFqTT / NB;               // tokens each workgroup reduces per tile
     __shared__ uint32_t fred[2][TPO];             // reduced row maxima of the owned tokens
-    // asymmetric codes: red, gat and fred hold maximum keys, and these the
-    // complemented minimum keys
-    __shared__ uint32_t redn[ASYM ? 2 : 1][ASYM ? kFqTT : 1];
-    __shared__ uint32_t gatn[ASYM ? kFqTT : 1];
+    __shared__ uint32_t fready;                   // tiles whose fred is complete
+    __shared__ uint32_t redn[ASYM ? 2 : 1][4][ASYM ? kFqTT : 1];
+    __shared__ uint32_t gatn[ASYM ? 2 : 1][ASYM ? kFqTT : 1];
     __shared__ uint32_t fredn[ASYM ? 2 : 1][ASYM ? TPO : 1];
 
     const int64_t b = blockIdx.x % NB;
@@ -861,15 +891,25 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
     const int64_t ntiles = (n + kFqTT - 1) / kFqTT;
     if (r0 >= ntiles) return;           // never taken: the launcher sizes R <= ntiles
     const int64_t nt = (ntiles - r0 + R - 1) / R;
-    const int64_t nsteps = nt + kFqLag;
+    // step it: tile it multiplied (it < nt), tile it - L quantized into LDS,
+    // tile it - L - 1's codes stored
+    const int64_t nsteps = nt + L + 1;
     const int lane = threadIdx.x & (kWave - 1);
     const int wave = threadIdx.x / kWave;
     auto tile0 = [&](int64_t it) { return (r0 + it * R) * kFqTT; };   // first token
+    if (threadIdx.x == 0) fready = 0;
+    if (threadIdx.x < kFqCompute * kWave) {
+        const u32x4* tg = reinterpret_cast<const u32x4*>(T + b * K * K);
+#pragma unroll
+        for (int i = 0; i < K * kFqU / (kFqCompute * kWave); ++i) {
+            const int q = static_cast<int>(threadIdx.x) + i * kFqCompute * kWave;
+            const int p = q / kFqU, u = q % kFqU;
+            tl[p * kFqU + (u ^ tq_xswz<K>(p))] = tg[((p & ~31) + fq_row(p & 31)) * kFqU + u];
+        }
+    }
+    lds_barrier();
 
     if (wave >= kFqCompute + kFqCopy) {
-        // ------------------------------------------ gather / publish waves
-        // The gather wave only loads and the publish wave only stores, so
-        // a wait for a load never includes a store's acknowledgement.
         const uint64_t hi = static_cast<uint64_t>(tag) << 32;
         const int64_t n16 = (n + 15) / 16 * 16;
         uint64_t* const fw = ws.pmax + n16 * NB;
@@ -885,44 +925,76 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
             __hip_atomic_store(a, hi | m, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         };
         if (wave == kFqCompute + kFqCopy + 1) {
-            // publish: F of tile it-2 (reduced in the last step), P of tile it
+            // publish: P of tile it-1, the codes (and scales) of tile
+            // it-L-1, then F of tile it-3 once the gather wave has reduced it
             for (int64_t it = 0; it < nsteps; ++it) {
-                lds_barrier();                                        // A
-                if (it >= 2 && it - 2 < nt) {
-                    const int64_t t = tile0(it - 2) + TPO * b + lane;
-                    const int o = lane < TPO ? lane : 0;
-                    if (lane < TPO && t < n) {
-                        store(fw + t, fred[it & 1][o]);
-                        if constexpr (ASYM) store(fwn + t, fredn[it & 1][o]);
-                    }
-                }
-                lds_barrier();                                        // F
-                if (it < nt) {
-                    const int64_t t = tile0(it) + lane;
-                    const uint32_t mm = max(red[0][lane], red[1][lane]);
+                lds_barrier();
+                if (it >= 1 && it - 1 < nt) {
+                    const int64_t t = tile0(it - 1) + lane;
+                    const int sb = static_cast<int>((it - 1) & 1);
+                    const uint32_t mm = max(max(red[sb][0][lane], red[sb][1][lane]),
+                                            max(red[sb][2][lane], red[sb][3][lane]));
                     if (t < n) store(p_word(t, b), mm);
                     if constexpr (ASYM) {
-                        const uint32_t mn = max(redn[0][lane], redn[1][lane]);
+                        const uint32_t mn = max(max(redn[sb][0][lane], redn[sb][1][lane]),
+                                                max(redn[sb][2][lane], redn[sb][3][lane]));
                         if (t < n) store(pn_word(t, b), mn);
+                    }
+                }
+                const int64_t jc = it - L - 1;
+                if (jc >= 0 && jc < nt) {
+                    const int sb = static_cast<int>(jc & 1);
+                    constexpr int PER = CB / 16;          // 16-byte pieces per token
+                    constexpr int TPI = kWave / PER;      // tokens per instruction
+#pragma unroll
+                    for (int q = 0; q < kFqTT / TPI; ++q) {
+                        const int tk = q * TPI + lane / PER, pc = lane % PER;
+                        const int64_t t = tile0(jc) + tk;
+                        const u32x4 v = *reinterpret_cast<const u32x4*>(&cbuf[sb][tk][16 * pc]);
+                        if (t < n)
+                            *reinterpret_cast<u32x4*>(codes + t * (d * CB / K) + b * CB + 16 * pc) = v;
+                    }
+                    const int64_t t = tile0(jc) + lane;
+                    if (b == 0 && t < n) {
+                        s_x[t] = cscale[sb][lane];
+                        if constexpr (ASYM) zmin_x[t] = czmin[sb][lane];
+                    }
+                }
+                if (it >= 3 && it - 3 < nt) {
+                    // bounded like the gather wave's own waits (an LDS poll
+                    // is far shorter than a device read); a wait that runs
+                    // out publishes the NaN maximum instead of a stale one
+                    const uint32_t want = static_cast<uint32_t>(it - 2);
+                    bool ready = true;
+                    for (uint32_t polls = 0; __hip_atomic_load(&fready, __ATOMIC_ACQUIRE,
+                                                               __HIP_MEMORY_SCOPE_WORKGROUP) < want;) {
+                        if (++polls >= 16 * kTqSpinLimit) {
+                            __hip_atomic_store(ws.flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                            ready = false;
+                            break;
+                        }
+                        __builtin_amdgcn_s_sleep(1);
+                    }
+                    const int64_t t = tile0(it - 3) + TPO * b + lane;
+                    const int o = lane < TPO ? lane : 0;
+                    const int sb = static_cast<int>((it - 3) & 1);
+                    constexpr uint32_t kNaN = ASYM ? 0xFFFFFFFFu : 0x7FC00000u;
+                    if (lane < TPO && t < n) {
+                        store(fw + t, ready ? fred[sb][o] : kNaN);
+                        if constexpr (ASYM) store(fwn + t, ready ? fredn[sb][o] : kNaN);
                     }
                 }
             }
             return;
         }
-        // gather: takes F of tile it-3 after A, then requests P of tile
-        // it-1; takes P after F and reduces it, then requests F of tile
-        // it-2.  Every read has a phase in flight, and only one read (two
-        // for asymmetric codes, the maximum and the minimum key) is
-        // outstanding when it is waited for.  A word that is not there yet
-        // is re-read (bounded).
+        // gather, step it: take F of tile it-L+1 and P of tile it-3 (both
+        // requested in the last step), reduce P into the owned tokens' row
+        // maxima, then request P of tile it-2 and F of tile it-L+2 (both
+        // published in the last step).  Every read has a whole step in
+        // flight; a word that is not there yet is re-read (bounded).
         auto load = [&](const uint64_t* a) {
             return __hip_atomic_load(a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         };
-        // A wait that runs out yields a quiet NaN: as bits it exceeds every
-        // finite maximum, so it survives both reduction levels, and the
-        // tokens concerned get s_x = NaN instead of a silently wrong scale.
-        // Asymmetric keys take all ones instead: the largest key, which
-        // decodes to NaN both as a maximum and, complemented, as a minimum.
         auto await = [&](uint64_t v, const uint64_t* a) {
             for (uint32_t polls = 0; (v >> 32) != tag;) {
                 if (++polls >= kTqSpinLimit) {
@@ -934,7 +1006,6 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
             }
             return static_cast<uint32_t>(v);
         };
-        // F(token lane of tile j); P(block lane % NB, token TPO b + lane / NB of tile j)
         auto f_addr = [&](int64_t j) { return fw + clampt(tile0(j) + lane); };
         auto p_addr = [&](int64_t j) {
             return p_word(clampt(tile0(j) + TPO * b + lane / NB), lane % NB);
@@ -951,41 +1022,29 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
         };
         uint64_t fv = 0, pv = 0, fvn = 0, pvn = 0;
         for (int64_t it = 0; it < nsteps; ++it) {
-            lds_barrier();                                            // A
-            if (it >= kFqLag) {
-                const int64_t t = tile0(it - kFqLag) + lane;
-                const uint32_t m = await(fv, f_addr(it - kFqLag));
-                gat[lane] = m;
+            lds_barrier();
+            const int64_t jf = it - L + 1, jp = it - 3;
+            if (jf >= 0 && jf < nt) {
+                gat[jf & 1][lane] = await(fv, f_addr(jf));
+                if constexpr (ASYM) gatn[jf & 1][lane] = await(fvn, fn_addr(jf));
+            }
+            if (jp >= 0 && jp < nt) {
+                const uint32_t m = fold(await(pv, p_addr(jp)));
+                if (lane % NB == 0) fred[jp & 1][lane / NB] = m;
                 if constexpr (ASYM) {
-                    const uint32_t mn = await(fvn, fn_addr(it - kFqLag));
-                    gatn[lane] = mn;
-                    if (b == 0 && t < n) {
-                        float zmin, sc, inv;
-                        fq_asym_scale(m, mn, zmin, sc, inv);
-                        s_x[t] = sc;
-                        zmin_x[t] = zmin;
-                    }
-                } else {
-                    if (b == 0 && t < n)
-                        s_x[t] = __fdiv_rn(__uint_as_float(m), static_cast<float>(QM));
+                    const uint32_t mn = fold(await(pvn, pn_addr(jp)));
+                    if (lane % NB == 0) fredn[jp & 1][lane / NB] = mn;
                 }
+                __hip_atomic_store(&fready, static_cast<uint32_t>(jp + 1), __ATOMIC_RELEASE,
+                                   __HIP_MEMORY_SCOPE_WORKGROUP);
             }
-            if (it >= 1 && it <= nt) {
-                pv = load(p_addr(it - 1));
-                if constexpr (ASYM) pvn = load(pn_addr(it - 1));
+            if (it >= 2 && it - 2 < nt) {
+                pv = load(p_addr(it - 2));
+                if constexpr (ASYM) pvn = load(pn_addr(it - 2));
             }
-            lds_barrier();                                            // F
-            if (it >= 1 && it <= nt) {
-                const uint32_t m = fold(await(pv, p_addr(it - 1)));
-                if (lane % NB == 0) fred[(it + 1) & 1][lane / NB] = m;
-                if constexpr (ASYM) {
-                    const uint32_t mn = fold(await(pvn, pn_addr(it - 1)));
-                    if (lane % NB == 0) fredn[(it + 1) & 1][lane / NB] = mn;
-                }
-            }
-            if (it + 1 >= kFqLag && it + 1 < nsteps) {
-                fv = load(f_addr(it + 1 - kFqLag));
-                if constexpr (ASYM) fvn = load(fn_addr(it + 1 - kFqLag));
+            if (jf + 1 >= 0 && jf + 1 < nt) {
+                fv = load(f_addr(jf + 1));
+                if constexpr (ASYM) fvn = load(fn_addr(jf + 1));
             }
         }
         return;
@@ -1015,114 +1074,153 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
                 const int64_t hi_t = nt - 1 < it + kFqAhead - 1 ? nt - 1 : it + kFqAhead - 1;
                 fq_wait_copies(static_cast<int>(hi_t - it));
             }
-            lds_barrier();                                            // A
-            // the stage of tile it + kFqAhead last held a tile multiplied
-            // before A
+            lds_barrier();
+            // the stage of tile it + kFqAhead last held tile it + kFqAhead -
+            // kFqStages, whose last read (for its multiplication) was in
+            // step it + kFqAhead - kFqStages < it
             if (it + kFqAhead < nt) issue(it + kFqAhead);
-            lds_barrier();                                            // F
         }
         return;
     }
 
     // ------------------------------------------------------ compute waves
-    // Wave w takes the 32 tokens 32 (w % 2) .. + 31 of a tile against rows
-    // 64 (w / 2) .. + 63 of T_b (two 32-row MFMA groups held in registers),
-    // so each wave reads only its own tokens from LDS.
+    // Wave w multiplies the 32 rows 32 (w / 2) .. + 31 of T_b (read from
+    // LDS) with the 32 tokens 32 (w % 2) .. + 31 of a tile; a lane
+    // (token, h) accumulates 16 consecutive output channels.  Seven
+    // accumulator sets rotate: tile it is multiplied into set it % 7 while
+    // tile it - 6 (set (it + 1) % 7) is quantized, its rounding interleaved
+    // with the MFMAs.
     const int l32 = lane & 31;
     const int h = lane >> 5;
     const int th = wave & 1;            // token half of the tile
-    const int rh = wave >> 1;           // row half of T_b
+    const int rq = wave >> 1;           // 32-row group of T_b
     const int tok = th * 32 + l32;      // token (within the tile) of this lane
-    u32x4 tf[2][NS];
-#pragma unroll
-    for (int g = 0; g < 2; ++g) {
-        const int row = (2 * rh + g) * 32 + fq_row(l32);
-        const u32x4* tg = reinterpret_cast<const u32x4*>(T + (b * K + row) * K);
-#pragma unroll
-        for (int s = 0; s < NS; ++s) tf[g][s] = tg[2 * s + h];
-    }
-    auto mfma = [&](int64_t it, f32x16 (&acc)[2]) {
-        const int st = static_cast<int>(it % kFqStages);
-#pragma unroll
-        for (int g = 0; g < 2; ++g) acc[g] = f32x16{};
-#pragma unroll
-        for (int s = 0; s < NS; ++s) {
-            const u32x4 xf = ring[st][tok * kFqU + ((2 * s + h) ^ tq_xswz<K>(tok))];
-#pragma unroll
-            for (int g = 0; g < 2; ++g)
-                acc[g] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(tf[g][s]), as_bf16x8(xf),
-                                                                 acc[g], 0, 0, 0);
-        }
+    const int trow = rq * 32 + l32;     // LDS row of this lane's T_b row
+    auto tfrag = [&](int s) { return tl[trow * kFqU + ((2 * s + h) ^ tq_xswz<K>(trow))]; };
+    using CodeT = std::conditional_t<(QM == 7), u32x2, u32x4>;
+    auto keys_out = [&](int64_t it, const f32x16& acc) {
+        uint32_t mx, mn = 0;
         if constexpr (ASYM) {
-            // order-preserving keys: the maximum, and the complemented minimum
-            uint32_t mx = 0, mn = 0;
+            mx = 0;
 #pragma unroll
-            for (int g = 0; g < 2; ++g)
-#pragma unroll
-                for (int q = 0; q < 16; ++q) {
-                    const uint32_t kq = fkey(acc[g][q]);
-                    mx = max(mx, kq);
-                    mn = max(mn, ~kq);
-                }
-            mx = max(mx, static_cast<uint32_t>(__shfl_xor(static_cast<int>(mx), 32)));
+            for (int q = 0; q < 16; ++q) {
+                const uint32_t kq = fkey(acc[q]);
+                mx = max(mx, kq);
+                mn = max(mn, ~kq);
+            }
             mn = max(mn, static_cast<uint32_t>(__shfl_xor(static_cast<int>(mn), 32)));
-            if (h == 0) {
-                red[rh][tok] = mx;
-                redn[rh][tok] = mn;
-            }
         } else {
-            uint32_t m = max(fq_absmax16(acc[0]), fq_absmax16(acc[1]));
-            m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), 32)));
-            if (h == 0) red[rh][tok] = m;
+            mx = fq_absmax16(acc);
+        }
+        mx = max(mx, static_cast<uint32_t>(__shfl_xor(static_cast<int>(mx), 32)));
+        const int sb = static_cast<int>(it & 1);
+        if (h == 0) {
+            red[sb][rq][tok] = mx;
+            if constexpr (ASYM) redn[sb][rq][tok] = mn;
         }
     };
-    auto quant = [&](int64_t it, const f32x16 (&acc)[2]) {
-        const int64_t t = tile0(it) + tok;
-        float inv, zmin = 0.0f;
+    struct Sc {
+        float inv, zmin, s;
+    };
+    auto scale_of = [&](int64_t j) {
+        Sc p;
+        const int sb = static_cast<int>(j & 1);
         if constexpr (ASYM) {
-            float sc;
-            fq_asym_scale(gat[tok], gatn[tok], zmin, sc, inv);
+            fq_asym_scale(gat[sb][tok], gatn[sb][tok], p.zmin, p.s, p.inv);
         } else {
-            const float amax = __uint_as_float(gat[tok]);
-            inv = amax > 0.0f ? __fdiv_rn(static_cast<float>(QM), amax) : 0.0f;
+            const float amax = __uint_as_float(gat[sb][tok]);
+            p.inv = amax > 0.0f ? __fdiv_rn(static_cast<float>(QM), amax) : 0.0f;
+            p.s = __fdiv_rn(amax, static_cast<float>(QM));
+            p.zmin = 0.0f;
         }
-#pragma unroll
-        for (int g = 0; g < 2; ++g) {
-            // lane (token, h) holds channels (2 rh + g) 32 + 16 h .. + 15
-            if constexpr (ASYM) {
-                const u32x2 c = fq_quant16_asym(acc[g], zmin, inv);
-                if (t < n)
-                    *reinterpret_cast<u32x2*>(codes + t * (d / 2) + b * (K / 2) +
-                                              (2 * rh + g) * 16 + 8 * h) = c;
-            } else if constexpr (QM == 7) {
-                const u32x2 c = fq_quant16(acc[g], inv);
-                if (t < n)
-                    *reinterpret_cast<u32x2*>(codes + t * (d / 2) + b * (K / 2) +
-                                              (2 * rh + g) * 16 + 8 * h) = c;
-            } else {
-                const u32x4 c = fq_quant16_i8<QM>(acc[g], inv);
-                if (t < n)
-                    *reinterpret_cast<u32x4*>(codes + t * d + b * K + (2 * rh + g) * 32 + 16 * h) = c;
+        return p;
+    };
+    auto codes_out = [&](int64_t j, const CodeT& c, const Sc& p) {
+        const int sb = static_cast<int>(j & 1);
+        *reinterpret_cast<CodeT*>(&cbuf[sb][tok][(QM == 7 ? 16 : 32) * rq + (QM == 7 ? 8 : 16) * h]) = c;
+        if (rq == 0 && h == 0) {
+            cscale[sb][tok] = p.s;
+            if constexpr (ASYM) czmin[sb][tok] = p.zmin;
+        }
+    };
+    // rounding of values 2s, 2s + 1 of a set, packed as soon as a word is
+    // full; the empty asm keeps each word's packing at this point of the
+    // step (the compiler would otherwise sink it next to the LDS store,
+    // after every MFMA)
+    auto round_piece = [&](int s, const f32x16& z, const Sc& p, uint32_t (&w)[16], CodeT& c) {
+        w[2 * s] = fq_round1<QM, ASYM>(z[2 * s], p.inv, p.zmin);
+        w[2 * s + 1] = fq_round1<QM, ASYM>(z[2 * s + 1], p.inv, p.zmin);
+        if constexpr (QM == 7) {
+            if ((s & 3) == 3) {
+                const int hw = s >> 2;
+                const uint32_t* v = w + 8 * hw;
+                const uint32_t ev = fq_bytes(v[0], v[2], v[4], v[6]);
+                const uint32_t od = fq_bytes(v[1], v[3], v[5], v[7]);
+                uint32_t word = (ev & 0x0F0F0F0Fu) | ((od << 4) & 0xF0F0F0F0u);
+                asm volatile("" : "+v"(word));
+                c[hw] = word;
+            }
+        } else {
+            if (s & 1) {
+                const int q = s >> 1;
+                uint32_t word = fq_bytes(w[4 * q], w[4 * q + 1], w[4 * q + 2], w[4 * q + 3]);
+                asm volatile("" : "+v"(word));
+                c[q] = word;
             }
         }
     };
-    // step it: A, multiply tile it into cur, F, quantize tile it-3 from old
-    auto step = [&](int64_t it, f32x16 (&cur)[2], const f32x16 (&old)[2]) {
-        lds_barrier();                                                // A
-        if (it < nt) mfma(it, cur);
-        lds_barrier();                                                // F
-        if (it >= kFqLag) quant(it - kFqLag, old);
+    auto step = [&](int64_t it, f32x16& cur, const f32x16& old) {
+        lds_barrier();
+        const bool cd = it < nt, qd = it >= L && it - L < nt;
+        const int st = static_cast<int>(it % kFqStages);
+        if (cd && qd) {
+            // one MFMA and an eighth of the rounding per fenced group, so the
+            // vector ALU works while the MFMA runs
+            const Sc p = scale_of(it - L);
+            uint32_t w[16];
+            CodeT c;
+            cur = f32x16{};
+#pragma unroll
+            for (int s = 0; s < NS; ++s) {
+                const u32x4 xf = ring[st][tok * kFqU + ((2 * s + h) ^ tq_xswz<K>(tok))];
+                cur = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(tfrag(s)), as_bf16x8(xf), cur, 0, 0, 0);
+                round_piece(s, old, p, w, c);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+            codes_out(it - L, c, p);
+            keys_out(it, cur);
+        } else if (cd) {
+            cur = f32x16{};
+#pragma unroll
+            for (int s = 0; s < NS; ++s) {
+                const u32x4 xf = ring[st][tok * kFqU + ((2 * s + h) ^ tq_xswz<K>(tok))];
+                cur = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(tfrag(s)), as_bf16x8(xf), cur, 0, 0, 0);
+            }
+            keys_out(it, cur);
+        } else if (qd) {
+            const Sc p = scale_of(it - L);
+            uint32_t w[16];
+            CodeT c;
+#pragma unroll
+            for (int s = 0; s < NS; ++s) round_piece(s, old, p, w, c);
+            codes_out(it - L, c, p);
+        }
     };
-    static_assert(kFqLag == 3, "four accumulator sets rotate");
-    f32x16 s0[2], s1[2], s2[2], s3[2];
-    for (int64_t it = 0; it < nsteps; it += 4) {
-        step(it, s0, s1);
+    f32x16 a0, a1, a2, a3, a4, a5, a6;
+    for (int64_t it = 0; it < nsteps; it += 7) {
+        step(it, a0, a1);
         if (it + 1 >= nsteps) break;
-        step(it + 1, s1, s2);
+        step(it + 1, a1, a2);
         if (it + 2 >= nsteps) break;
-        step(it + 2, s2, s3);
+        step(it + 2, a2, a3);
         if (it + 3 >= nsteps) break;
-        step(it + 3, s3, s0);
+        step(it + 3, a3, a4);
+        if (it + 4 >= nsteps) break;
+        step(it + 4, a4, a5);
+        if (it + 5 >= nsteps) break;
+        step(it + 5, a5, a6);
+        if (it + 6 >= nsteps) break;
+        step(it + 6, a6, a0);
     }
 }
 

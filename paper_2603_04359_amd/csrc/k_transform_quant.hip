@@ -869,11 +869,15 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
     static_assert(L == 6, "seven accumulator sets rotate");
     static_assert(kFqTT == 64 && kFqCompute == 8, "compute waves: 2 token halves x 4 row groups");
     constexpr int CB = QM == 7 ? K / 2 : K;       // code bytes per token and block
+    // token stride of the code buffer: 16 bytes of padding put the 16 tokens
+    // of one LDS pass on distinct banks (8-byte writes at a 64-byte stride
+    // would share 4 banks), and keep every 16-byte piece aligned
+    constexpr int CBS = CB + 16;
     __shared__ __attribute__((aligned(16))) u32x4 ring[kFqStages][kFqStage];
     // T_b in MFMA row order: LDS row p holds row (p & ~31) + fq_row(p & 31),
     // 16-byte unit u at position u ^ tq_xswz(p)
     __shared__ __attribute__((aligned(16))) u32x4 tl[K * kFqU];
-    __shared__ __attribute__((aligned(16))) uint8_t cbuf[2][kFqTT][CB];   // codes of a quantized tile
+    __shared__ __attribute__((aligned(16))) uint8_t cbuf[2][kFqTT][CBS];  // codes of a quantized tile
     __shared__ float cscale[2][kFqTT];            // its s_x
     __shared__ float czmin[ASYM ? 2 : 1][ASYM ? kFqTT : 1];
     __shared__ uint32_t red[2][4][kFqTT];         // per-row-group maxima of a step's tile
@@ -898,6 +902,26 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
     const int wave = threadIdx.x / kWave;
     auto tile0 = [&](int64_t it) { return (r0 + it * R) * kFqTT; };   // first token
     if (threadIdx.x == 0) fready = 0;
+    // copy waves: tile it of this block into stage it % kFqStages; the first
+    // kFqAhead tiles are requested at once, beside the staging of T_b
+    const int cw = wave - kFqCompute;
+    auto issue = [&](int64_t it) {
+        const int64_t t0 = tile0(it);
+        const uint16_t* base = X + t0 * d + b * K;
+        const int64_t last = n - 1 - t0;
+        const int st = static_cast<int>(it % kFqStages);
+#pragma unroll
+        for (int q = 0; q < kFqCopyOps; ++q) {
+            const int first = (cw * kFqCopyOps + q) * kWave;   // first slot of this copy
+            const int sl = first + lane;
+            int rr = sl / kFqU;
+            const int u = (sl % kFqU) ^ tq_xswz<K>(rr);
+            rr = rr <= last ? rr : static_cast<int>(last);
+            dma16(base, static_cast<uint32_t>((rr * d + u * 8) * 2), lds_addr(&ring[st][first]));
+        }
+    };
+    if (wave >= kFqCompute && wave < kFqCompute + kFqCopy)
+        for (int64_t it = 0; it < nt && it < kFqAhead; ++it) issue(it);
     if (threadIdx.x < kFqCompute * kWave) {
         const u32x4* tg = reinterpret_cast<const u32x4*>(T + b * K * K);
 #pragma unroll
@@ -1052,23 +1076,6 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
 
     if (wave >= kFqCompute) {
         // ---------------------------------------------------- copy waves
-        const int cw = wave - kFqCompute;
-        auto issue = [&](int64_t it) {
-            const int64_t t0 = tile0(it);
-            const uint16_t* base = X + t0 * d + b * K;
-            const int64_t last = n - 1 - t0;
-            const int st = static_cast<int>(it % kFqStages);
-#pragma unroll
-            for (int q = 0; q < kFqCopyOps; ++q) {
-                const int first = (cw * kFqCopyOps + q) * kWave;   // first slot of this copy
-                const int sl = first + lane;
-                int rr = sl / kFqU;
-                const int u = (sl % kFqU) ^ tq_xswz<K>(rr);
-                rr = rr <= last ? rr : static_cast<int>(last);
-                dma16(base, static_cast<uint32_t>((rr * d + u * 8) * 2), lds_addr(&ring[st][first]));
-            }
-        };
-        for (int64_t it = 0; it < nt && it < kFqAhead; ++it) issue(it);
         for (int64_t it = 0; it < nsteps; ++it) {
             if (it < nt) {
                 const int64_t hi_t = nt - 1 < it + kFqAhead - 1 ? nt - 1 : it + kFqAhead - 1;

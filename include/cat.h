@@ -147,18 +147,29 @@ int cat_cov_accumulate(const void* X, int x_dtype, int64_t n, int64_t d,
  * workspace with bounded waits.
  * Its grid never exceeds the device's resident capacity, so every wait ends
  * once the launch has the device; work from other streams that holds CUs
- * for seconds can still make a wait run out.  Then the tokens concerned get
- * s_x = NaN and zero codes rather than a wrong scale, and the 32-bit word
- * at byte offset cat_transform_quant_flag_offset(n, d, k) of the workspace
- * is set to a non-zero value.  The library never clears that word: a
- * caller that wants to check it zeroes it before the call and reads it
- * after synchronising.
+ * for seconds can still make a wait run out.  Then the 32-bit word at byte
+ * offset cat_transform_quant_flag_offset(n, d, k) of the workspace is set
+ * to a non-zero value, and the call's results must be treated as invalid.
+ * No wrong scale is ever used even then: every workgroup reads a token's
+ * row maximum on its own and uses the exact value or NaN, so each
+ * 128-channel block of a token's codes is exact or (where that block's
+ * wait ran out) zero, and s_x is exact or NaN.  The library never clears
+ * that word: a caller that wants to check it zeroes it before the call and
+ * reads it after synchronising.
  */
 size_t cat_transform_quant_workspace_bytes(int64_t n, int64_t d, int64_t k);
 /* Byte offset, inside a workspace of cat_transform_quant_workspace_bytes
  * (n, d, k) bytes, of the exchange timeout word described above (0 when the
  * arguments are invalid). */
 size_t cat_transform_quant_flag_offset(int64_t n, int64_t d, int64_t k);
+/* Testing hook (no passage of the paper): bounds the polls of every wait in
+ * the single-pass exchange of later cat_transform_quant and
+ * cat_transform_quant_asym calls, process-wide.  0 restores the default
+ * (2^22, seconds of waiting); larger values are clamped to it.  A small
+ * bound makes waits run out as described above, so that tests can check
+ * that a timeout yields exact or NaN scales, exact or zero code blocks and
+ * the flag word, with every kernel still finishing normally. */
+void cat_set_exchange_spin_limit(uint32_t polls);
 int cat_transform_quant(const void* X, int x_dtype, int64_t n, int64_t d,
                         const void* T, int t_dtype, int64_t k, int bits,
                         uint8_t* codes, float* s_x, void* workspace,
@@ -177,7 +188,8 @@ int cat_transform_quant(const void* X, int x_dtype, int64_t n, int64_t d,
  * share that GPU's array, which keeps the last call's contents; calls that
  * overlap on one GPU (other streams, other threads) race and must not be
  * issued.  The exchange timeout word lives in that array and is not
- * reported (a timed-out wait still yields NaN scales). */
+ * reported: a timed-out wait shows only in the results (zero code blocks,
+ * NaN scales), never as a wrong scale. */
 size_t cat_transform_quant_noalloc_max_bytes(void);
 int cat_transform_quant_noalloc(const void* X, int x_dtype, int64_t n, int64_t d,
                                 const void* T, int t_dtype, int64_t k, int bits,
@@ -236,7 +248,9 @@ int cat_int8_linear(const int8_t* codes_x, const float* s_x,
  * (larger than the symmetric one: the single-pass path, bf16 with k = 128
  * and d = 2048, 4096 or 8192, exchanges a row minimum and maximum per
  * token); the exchange timeout word is at cat_transform_quant_flag_offset
- * as for the symmetric path, and a timed-out wait yields s_x = zmin_x = NaN.
+ * as for the symmetric path; a timed-out wait never yields a wrong scale
+ * (the blocks concerned are coded with a NaN range; where block 0's wait
+ * ran out s_x = NaN, and zmin_x is exact or NaN).
  *
  * cat_w4a4_linear_asym: the product of those activations with symmetric
  * INT4 weights,

@@ -41,7 +41,7 @@ CAT_MAX_BLOCK = 512
 # every symbol include/cat.h declares
 EXPORTED = (
     "cat_cov_workspace_bytes", "cat_cov_accumulate", "cat_transform_quant_workspace_bytes",
-    "cat_transform_quant_flag_offset", "cat_transform_quant", "cat_transform_quant_noalloc_max_bytes",
+    "cat_transform_quant_flag_offset", "cat_set_exchange_spin_limit", "cat_transform_quant", "cat_transform_quant_noalloc_max_bytes",
     "cat_transform_quant_noalloc",
     "cat_w4a4_linear", "cat_int8_linear", "cat_transform_quant_asym_workspace_bytes",
     "cat_transform_quant_asym", "cat_w4a4_linear_asym",
@@ -83,6 +83,8 @@ def lib() -> ctypes.CDLL:
     L.cat_transform_quant_workspace_bytes.restype = _sz
     L.cat_transform_quant_flag_offset.argtypes = [_i64, _i64, _i64]
     L.cat_transform_quant_flag_offset.restype = _sz
+    L.cat_set_exchange_spin_limit.argtypes = [ctypes.c_uint32]
+    L.cat_set_exchange_spin_limit.restype = None
     L.cat_transform_quant.argtypes = [_vp, _int, _i64, _i64, _vp, _int, _i64, _int, _vp, _vp,
                                       _vp, _sz, _vp]
     L.cat_transform_quant.restype = _int
@@ -244,6 +246,11 @@ def cat_transform_quant_workspace_bytes(n: int, d: int, k: int) -> int:
 def cat_transform_quant_flag_offset(n: int, d: int, k: int) -> int:
     """Byte offset of the exchange timeout word inside the workspace."""
     return int(lib().cat_transform_quant_flag_offset(n, d, k))
+
+
+def cat_set_exchange_spin_limit(polls: int) -> None:
+    """Testing hook: bound the single-pass exchange waits (0 = default)."""
+    lib().cat_set_exchange_spin_limit(int(polls))
 
 
 def cat_transform_quant(X, T, k: int, codes, s_x, workspace, bits: int = 4, stream=None):

@@ -98,6 +98,8 @@ extern "C" size_t cat_transform_quant_flag_offset(int64_t n, int64_t d, int64_t 
     return catk::tq_flag_offset_bytes(n, d);
 }
 
+extern "C" void cat_set_exchange_spin_limit(uint32_t polls) { catk::tq_set_spin_limit(polls); }
+
 extern "C" int cat_transform_quant(const void* X, int x_dtype, int64_t n, int64_t d, const void* T,
                                    int t_dtype, int64_t k, int bits, uint8_t* codes, float* s_x,
                                    void* workspace, size_t workspace_bytes, void* stream) {

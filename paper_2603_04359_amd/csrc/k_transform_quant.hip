@@ -679,10 +679,16 @@ __global__ __launch_bounds__(kTqThreads, 2) void tq_ring_kernel(
 // Progress: the grid never exceeds the device's resident capacity (see
 // launch_tq_fused) and every workgroup of a token-tile row visits its tiles
 // in the same order, so a workgroup only waits for peers that are running
-// or about to run.  Waits are still bounded: after kTqSpinLimit polls the
-// gather wave records a timeout flag and goes on with a NaN maximum, which
-// makes the affected scales NaN.
+// or about to run.  Waits are still bounded: after a limit of polls (by
+// default kTqSpinLimit; tq_set_spin_limit lowers it for tests that force a
+// timeout) the waiting wave records a timeout flag and goes on with a NaN
+// maximum, which makes the affected scales NaN.
 constexpr uint32_t kTqSpinLimit = 1u << 22;
+static std::atomic<uint32_t> g_tq_spin_limit{kTqSpinLimit};
+void tq_set_spin_limit(uint32_t polls) {
+    g_tq_spin_limit.store(polls == 0 ? kTqSpinLimit : (polls < kTqSpinLimit ? polls : kTqSpinLimit),
+                          std::memory_order_relaxed);
+}
 constexpr int kFqCompute = 8;                   // compute waves
 constexpr int kFqCopy = 2;                      // copy waves
 constexpr int kFqThreads = (kFqCompute + kFqCopy + 2) * kWave;
@@ -857,7 +863,7 @@ __device__ __forceinline__ void fq_wait_copies(int later) {
 template <int QM, int NB, bool ASYM>
 __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ T, int64_t n, int64_t d,
-    int64_t R, TqFusedWs ws, uint32_t host_tag, uint8_t* __restrict__ codes,
+    int64_t R, TqFusedWs ws, uint32_t host_tag, uint32_t spin, uint8_t* __restrict__ codes,
     float* __restrict__ s_x, float* __restrict__ zmin_x) {
     static_assert(!ASYM || QM == 7, "asymmetric codes are INT4");
     const uint32_t tag = ws.tag_word ? __hip_atomic_load(ws.tag_word, __ATOMIC_RELAXED,
@@ -992,7 +998,7 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
                     bool ready = true;
                     for (uint32_t polls = 0; __hip_atomic_load(&fready, __ATOMIC_ACQUIRE,
                                                                __HIP_MEMORY_SCOPE_WORKGROUP) < want;) {
-                        if (++polls >= 16 * kTqSpinLimit) {
+                        if (++polls >= 16 * spin) {
                             __hip_atomic_store(ws.flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                             ready = false;
                             break;
@@ -1021,7 +1027,7 @@ __global__ __launch_bounds__(kFqThreads, 1) void tq_fused_kernel(
         };
         auto await = [&](uint64_t v, const uint64_t* a) {
             for (uint32_t polls = 0; (v >> 32) != tag;) {
-                if (++polls >= kTqSpinLimit) {
+                if (++polls >= spin) {
                     __hip_atomic_store(ws.flag, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                     return ASYM ? 0xFFFFFFFFu : 0x7FC00000u;
                 }
@@ -1639,7 +1645,8 @@ static hipError_t launch_tq_fused_nb(const uint16_t* X, int64_t n, int64_t d, co
         tag = next_tq_tag();
     }
     hipLaunchKernelGGL((tq_fused_kernel<QM, NB, ASYM>), dim3(static_cast<uint32_t>(NB * R)),
-                       dim3(kFqThreads), 0, stream, X, T, n, d, R, w, tag, codes, s_x, zmin_x);
+                       dim3(kFqThreads), 0, stream, X, T, n, d, R, w, tag,
+                       g_tq_spin_limit.load(std::memory_order_relaxed), codes, s_x, zmin_x);
     err = hipGetLastError();
     if (err != hipSuccess) return err;
     launched = true;

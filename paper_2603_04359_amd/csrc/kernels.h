@@ -28,6 +28,9 @@ size_t tq_flag_offset_bytes(int64_t n, int64_t d);
 // the asymmetric entry point's workspace: tq_workspace_bytes plus the
 // single pass's minimum-key words
 size_t tq_asym_workspace_bytes(int64_t n, int64_t d, int64_t k);
+// polls after which a single-pass exchange wait gives up (0: the default);
+// applies to launches that follow
+void tq_set_spin_limit(uint32_t polls);
 hipError_t launch_transform_quant(const void* X, int x_bf16, int64_t n, int64_t d,
                                   const void* T, int t_bf16, int64_t k, int bits,
                                   uint8_t* codes, float* s_x, uint32_t* amax_ws,

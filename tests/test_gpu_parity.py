@@ -329,6 +329,22 @@ def test_transform_quant_two_pass_shapes(d, k, n):
         assert s[n // 2] == 0 and not codes[n // 2].any()
 
 
+@pytest.mark.parametrize("d,n", [(4096, 192), (4096, 512), (4096, 2561), (4096, 3135), (4096, 3584),
+                                 (8192, 1537), (2048, 6145)])
+def test_transform_quant_single_pass_tiles_per_workgroup(d, n):
+    # token counts that give each workgroup 1 to 7 tiles of 64 tokens, on
+    # both sides of the exchange lag of 6 steps: calls that are all ramp,
+    # and token-tile rows of unequal length (the first row one tile longer)
+    say(f"tq single pass d={d} k=128 n={n} (tiles per workgroup)")
+    X = _wide_X(n, d, seed=5 * n + d)
+    X[n - 1] = 0.0                                # a zero token row in the last tile
+    T = _rand_T(d, 128, seed=d + 7)
+    codes, s = _tq_gpu(X, T, 128, "bf16", "bf16")
+    _, _, s_or = check_codes(codes, X, T, label=f"single pass d={d} n={n}")
+    _check_scales(s, s_or, f"single pass d={d} n={n}")
+    assert s[n - 1] == 0 and not codes[n - 1].any()
+
+
 @pytest.mark.parametrize("d,n", [(8192, 1), (8192, 65), (8192, 2049), (2048, 1), (2048, 300),
                                  (2048, 4097)])
 def test_transform_quant_single_pass_other_widths(d, n):

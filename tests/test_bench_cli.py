@@ -1,5 +1,5 @@
 """bench.py's command-line contract on a host without a GPU: more than one
-GPU is refused with a message (this build runs on one GPU; collectives and
+GPU is refused with a message (the library runs on one GPU; collectives and
 sharding are design only)."""
 import os
 import subprocess

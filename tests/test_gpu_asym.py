@@ -77,6 +77,24 @@ def test_transform_quant_asym_matches_oracle(d, k, n, x_dtype, t_dtype):
     assert s[1] == 0 and m[1] == 0 and not q[1].any()
 
 
+@pytest.mark.parametrize("d,n", [(4096, 192), (4096, 3135), (4096, 3584), (8192, 1537),
+                                 (2048, 6145)])
+def test_transform_quant_asym_single_pass_tiles_per_workgroup(d, n):
+    # the asymmetric single pass at token counts that give each workgroup 1,
+    # 7 and 8 tiles of 64 tokens, on both sides of the exchange lag of 6
+    # steps, with unequal token-tile rows and a zero row in the last tile
+    say(f"tq asym single pass d={d} k=128 n={n} (tiles per workgroup)")
+    rng = np.random.default_rng(3 * n + d)
+    Xf = (rng.standard_normal((n, d)) * np.exp(0.5 * rng.standard_normal(d)) +
+          rng.standard_normal(d)).astype(np.float32)
+    Xf[n - 1] = 0.0
+    X = o.round_storage(Xf, "bf16")
+    T = o.round_storage(rng.standard_normal((d // 128, 128, 128)) / np.sqrt(128), "bf16")
+    q, s, m = _tq_asym(X, T, 128, "bf16", "bf16")
+    _check_asym(q, s, m, X, T, f"asym single pass d={d} n={n}")
+    assert s[n - 1] == 0 and m[n - 1] == 0 and not q[n - 1].any()
+
+
 @pytest.mark.parametrize("d", [512, 4096])
 def test_transform_quant_asym_identity_constant_rows_exact(d):
     # T = I: z = x exactly on both sides, so codes, scales and minima are

@@ -95,6 +95,11 @@ __device__ __forceinline__ void asym_scale(uint32_t kmax, uint32_t kmin_c, float
 }
 
 // ------------------------------------------------------------ generic path
+// Vector ALU, for fp32 operands and blocks the MFMA kernels do not take.
+// z is summed in fp64 and rounded to fp32 once, so it is fl32 of the exact
+// block product up to a rare double rounding: with fp32 sums a block whose
+// terms cancel heavily can move a code across a rounding boundary, and at
+// k = 256 or 512 with fp32 T the row maximum can drift by more than 1e-6.
 template <typename XT, typename TT>
 __device__ __forceinline__ float tq_dot(const XT* __restrict__ X, const TT* __restrict__ T,
                                         int64_t t, int64_t d, int64_t k, int64_t c) {
@@ -102,9 +107,11 @@ __device__ __forceinline__ float tq_dot(const XT* __restrict__ X, const TT* __re
     const int64_t j = c - b * k;
     const TT* trow = T + (b * k + j) * k;
     const XT* xrow = X + t * d + b * k;
-    float acc = 0.0f;
-    for (int64_t i = 0; i < k; ++i) acc = fmaf(load_as_f32(trow, i), load_as_f32(xrow, i), acc);
-    return acc;
+    double acc = 0.0;
+    for (int64_t i = 0; i < k; ++i)
+        acc = fma(static_cast<double>(load_as_f32(trow, i)), static_cast<double>(load_as_f32(xrow, i)),
+                  acc);
+    return static_cast<float>(acc);
 }
 
 template <typename XT, typename TT>

@@ -258,6 +258,41 @@ def test_transform_quant_other_paths(x_dtype, t_dtype, k, n):
     _check_scales(s, s_or, f"{x_dtype}/{t_dtype} k={k}")
 
 
+@pytest.mark.parametrize("x_dtype,t_dtype,k,bits", [
+    ("f32", "bf16", 64, 8), ("bf16", "f32", 256, 4), ("bf16", "f32", 512, 6),
+    ("f32", "f32", 512, 8), ("f32", "f32", 16, 4),
+])
+def test_transform_quant_fp32_operands_cancelling_sums(x_dtype, t_dtype, k, bits):
+    # the vector-ALU path (an fp32 operand): blocks with k up to 512 and
+    # rows whose block sums cancel heavily (each even row made nearly
+    # orthogonal to the first row of every T_b), where an fp32 running sum
+    # can move a code across a rounding boundary or the row maximum by more
+    # than 1e-6; the kernel's sums must keep codes to the tie rule and s_x
+    # within 1e-6, and exact on almost every token
+    say(f"tq {x_dtype}/{t_dtype} k={k} bits={bits} cancelling sums")
+    rng = np.random.default_rng(k + bits)
+    n, d = 160, 2 * k if k >= 256 else 8 * k
+    Xf = (rng.standard_normal((n, d)) * np.exp(0.7 * rng.standard_normal(d))).astype(np.float32)
+    T = o.round_storage(rng.standard_normal((d // k, k, k)) / np.sqrt(k), t_dtype)
+    for t in range(0, n, 2):
+        for b in range(d // k):
+            sl = slice(b * k, (b + 1) * k)
+            x, w = Xf[t, sl].astype(np.float64), T[b][0].astype(np.float64)
+            Xf[t, sl] = (x - (x @ w) / (w @ w) * w + 1e-4 * rng.standard_normal(k)).astype(np.float32)
+    X = o.round_storage(Xf, x_dtype)
+    torch = torch_mod()
+    codes = torch.empty((n, d // 2 if bits == 4 else d),
+                        dtype=torch.uint8 if bits == 4 else torch.int8, device="cuda")
+    s_x = torch.empty(n, dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(16, cat.cat_transform_quant_workspace_bytes(n, d, k)), dtype=torch.uint8,
+                     device="cuda")
+    cat.cat_transform_quant(dev(X, x_dtype), dev(T, t_dtype), k, codes, s_x, ws, bits=bits)
+    s = host(s_x)
+    _, _, s_or = check_codes(host(codes), X, T, bits=bits, label=f"cancelling k={k} bits={bits}")
+    _check_scales(s, s_or, f"cancelling k={k} bits={bits}")
+    assert np.mean(s == s_or) >= 0.99
+
+
 # ------------------------------------------ single-pass transform+quant
 # k = 128 with d a multiple of 4096 runs the single-pass kernel, which
 # exchanges per-block row maxima between workgroups through the workspace.

@@ -193,10 +193,15 @@ def geometric_mean(A, B) -> np.ndarray:
 
 def optimal_alignment(sigma_x, sigma_w) -> np.ndarray:
     """M_hat = (Sigma_w # Sigma_x^(-1))^(1/2), the maximiser of
-    A(M x, W M^-1) (Sec. 4, eq. 7).  Sigma_w = W^T W."""
+    A(M x, W M^-1) (Sec. 4, eq. 7).  Sigma_w = W^T W.
+    The mean is symmetric (A # B = B # A), and it is evaluated as
+    Sigma_x^(-1) # Sigma_w, whose congruence inverts only the positive
+    definite Sigma_x^(-1).  Sigma_w has rank below k when the layer has
+    fewer outputs than the block has channels, and the literal A # B would
+    then invert it."""
     sx_inv = spd_power(sigma_x, -1.0)
     sx_inv = 0.5 * (sx_inv + sx_inv.T)
-    return spd_power(geometric_mean(sigma_w, sx_inv), 0.5)
+    return spd_power(geometric_mean(sx_inv, sigma_w), 0.5)
 
 
 def hadamard(k: int) -> np.ndarray:

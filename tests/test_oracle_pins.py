@@ -128,6 +128,29 @@ def test_optimal_alignment_reaches_svd_maximum():
     assert got >= o.alignment(X, W)
 
 
+def test_optimal_alignment_with_rank_deficient_sigma_w():
+    # fewer outputs (5) than channels (8): Sigma_w has rank 5.  G = M_hat^2 =
+    # Sigma_w # Sigma_x^-1 still solves its Riccati equation G Sigma_x G =
+    # Sigma_w (X B^-1 X = A for X = A # B), and M_hat Sigma_x M_hat has the
+    # square roots of the spectrum of Sigma_x^(1/2) Sigma_w Sigma_x^(1/2)
+    # (eq. 8), computed with scipy's sqrtm, independently of the oracle.
+    # Three of those are zero; the eigenvalue floor of the inner square root
+    # (EIG_FLOOR times the largest eigenvalue) sets them to
+    # sqrt(EIG_FLOOR) times the largest.
+    rng = np.random.default_rng(17)
+    X = _act(rng, 3000, 8)
+    W = rng.standard_normal((5, 8))
+    Sx, Sw = o.second_moment(X), W.T @ W
+    M = o.optimal_alignment(Sx, Sw)
+    G = M @ M
+    np.testing.assert_allclose(G @ Sx @ G, Sw, atol=1e-9 * np.abs(Sw).max())
+    sxh = np.real(sla.sqrtm(Sx))
+    ev = np.sort(np.sqrt(np.clip(np.linalg.eigvalsh(sxh @ Sw @ sxh), 0.0, None)))
+    got = np.sort(np.linalg.eigvalsh(M @ Sx @ M))
+    np.testing.assert_allclose(got[3:], ev[3:], rtol=1e-8)
+    np.testing.assert_allclose(got[:3], np.sqrt(o.EIG_FLOOR) * ev[-1], rtol=1e-6)
+
+
 def test_optimal_alignment_balance_identity():
     # eq. 8, first equality: M Sx M = M^-1 Sw M^-1; its spectrum is sqrt of
     # the spectrum of Sx^(1/2) Sw Sx^(1/2).

@@ -32,7 +32,10 @@
  *  - 6- and 8-bit codes (the W6A6 / W8A8 comparison widths): one int8 per
  *    element, codes in [-31, 31] or [-127, 127].
  *  - Calls are stateless and may be issued from several threads.
- *  - NaN / Inf inputs give undefined (but memory-safe) results.
+ *  - NaN / Inf inputs give undefined (but memory-safe) results.  So do
+ *    rows the fp32 quantizer cannot represent: a token whose transformed
+ *    values z all lie below qmax * 2^-128 in magnitude (about 2e-38 at 4
+ *    bits; the reciprocal qmax / amax overflows) or whose z overflows fp32.
  */
 #ifndef CAT_H
 #define CAT_H

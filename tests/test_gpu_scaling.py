@@ -1,0 +1,134 @@
+"""Power-of-two scaling through the device path, with no oracle involved.
+
+Multiplying X by 2^m multiplies every product, every fp32 or fp64 partial
+sum, z and the row maximum by exactly 2^m (no value leaves the normal
+range here), so the quantizer's u = fl(z fl(qmax / amax)) is unchanged:
+the codes must be bit-identical and s_x must scale by exactly 2^m (the
+quantizer's scaling invariance, Lemma 2.2's symmetric range; Sec. 3,
+eq. 5).  The same holds for the asymmetric minimum, for the GEMM's
+dequantization (scaling s_x scales y~ exactly), for Sigma_x (2^2m) and for
+the SQNR sums (2^2m each, the ratio unchanged)."""
+import numpy as np
+import pytest
+
+import paper_2603_04359_amd as cat
+from oracle import cat_oracle as o
+from paper_2603_04359_amd import binding as B
+
+from gpu_common import dev, host, say, torch_mod
+
+pytestmark = pytest.mark.gpu
+
+
+def _inputs(n, d, k, x_dtype, t_dtype, seed):
+    rng = np.random.default_rng(seed)
+    Xf = (rng.standard_normal((n, d)) * np.exp(0.7 * rng.standard_normal(d)) +
+          0.3 * rng.standard_normal(d)).astype(np.float32)
+    Xf[n // 2] = 0.0
+    X = o.round_storage(Xf, x_dtype)
+    T = o.round_storage(rng.standard_normal((d // k, k, k)) / np.sqrt(k), t_dtype)
+    return X, T
+
+
+def _tq(X, T, k, x_dtype, t_dtype, bits, asym=False):
+    torch = torch_mod()
+    n, d = X.shape
+    shp = (n, d // 2 if bits == 4 else d)
+    codes = torch.empty(shp, dtype=torch.uint8 if bits == 4 else torch.int8, device="cuda")
+    s_x = torch.empty(n, dtype=torch.float32, device="cuda")
+    if asym:
+        zm = torch.empty(n, dtype=torch.float32, device="cuda")
+        ws = torch.empty(max(16, cat.cat_transform_quant_asym_workspace_bytes(n, d, k)),
+                         dtype=torch.uint8, device="cuda")
+        cat.cat_transform_quant_asym(dev(X, x_dtype), dev(T, t_dtype), k, codes, s_x, zm, ws)
+        return host(codes), host(s_x), host(zm)
+    ws = torch.empty(max(16, cat.cat_transform_quant_workspace_bytes(n, d, k)), dtype=torch.uint8,
+                     device="cuda")
+    cat.cat_transform_quant(dev(X, x_dtype), dev(T, t_dtype), k, codes, s_x, ws, bits=bits)
+    return host(codes), host(s_x), None
+
+
+# (d, k, n, x_dtype, t_dtype): the single pass, the group, ring and
+# small-block MFMA kernels, and the vector-ALU kernels
+PATHS = [(4096, 128, 300, "bf16", "bf16"), (2048, 256, 200, "bf16", "bf16"),
+         (1024, 512, 65, "bf16", "bf16"), (384, 64, 90, "bf16", "bf16"),
+         (640, 128, 77, "bf16", "bf16"), (256, 16, 70, "f32", "bf16"),
+         (512, 64, 40, "bf16", "f32")]
+
+
+@pytest.mark.parametrize("m", [-20, 17])
+@pytest.mark.parametrize("bits", [4, 8])
+@pytest.mark.parametrize("d,k,n,x_dtype,t_dtype", PATHS)
+def test_transform_quant_power_of_two_scaling(d, k, n, x_dtype, t_dtype, bits, m):
+    say(f"tq scaling 2^{m} d={d} k={k} n={n} {x_dtype}/{t_dtype} bits={bits}")
+    X, T = _inputs(n, d, k, x_dtype, t_dtype, seed=d + k + n)
+    c0, s0, _ = _tq(X, T, k, x_dtype, t_dtype, bits)
+    c1, s1, _ = _tq(np.ldexp(X, m), T, k, x_dtype, t_dtype, bits)
+    assert np.array_equal(c0, c1)
+    assert np.array_equal(s1, np.ldexp(s0, m))
+    assert s0[n // 2] == 0
+
+
+@pytest.mark.parametrize("m", [-20, 17])
+@pytest.mark.parametrize("d,k,n,x_dtype,t_dtype", [PATHS[0], PATHS[1], PATHS[2], PATHS[5]])
+def test_transform_quant_asym_power_of_two_scaling(d, k, n, x_dtype, t_dtype, m):
+    say(f"tq asym scaling 2^{m} d={d} k={k} n={n} {x_dtype}/{t_dtype}")
+    X, T = _inputs(n, d, k, x_dtype, t_dtype, seed=d + 3 * k + n)
+    c0, s0, z0 = _tq(X, T, k, x_dtype, t_dtype, 4, asym=True)
+    c1, s1, z1 = _tq(np.ldexp(X, m), T, k, x_dtype, t_dtype, 4, asym=True)
+    assert np.array_equal(c0, c1)
+    assert np.array_equal(s1, np.ldexp(s0, m))
+    assert np.array_equal(z1, np.ldexp(z0, m))
+
+
+@pytest.mark.parametrize("n,d_in,d_out", [(300, 4096, 1000), (8192, 4096, 512)])
+def test_w4a4_linear_scales_exactly_with_s_x(n, d_in, d_out):
+    say(f"w4a4 scaling n={n} d_in={d_in} d_out={d_out}")
+    torch = torch_mod()
+    rng = np.random.default_rng(n + d_out)
+    qx = rng.integers(-7, 8, size=(n, d_in)).astype(np.int8)
+    qw = rng.integers(-7, 8, size=(d_out, d_in)).astype(np.int8)
+    sx = rng.uniform(0.01, 1.0, n).astype(np.float32)
+    sw = rng.uniform(0.01, 1.0, d_out).astype(np.float32)
+    px, pw, dsw = dev(o.pack_int4(qx), "u8"), dev(o.pack_int4(qw), "u8"), dev(sw, "f32")
+    ys = []
+    for m in (0, -24, 30):
+        y = torch.empty((n, d_out), dtype=torch.float32, device="cuda")
+        cat.cat_w4a4_linear(px, dev(np.ldexp(sx, m), "f32"), pw, dsw, y)
+        ys.append(host(y))
+    assert np.array_equal(ys[1], np.ldexp(ys[0], -24))
+    assert np.array_equal(ys[2], np.ldexp(ys[0], 30))
+
+
+@pytest.mark.parametrize("mode,k,d,n", [(B.CAT_COV_FULL, 1, 1024, 3000),
+                                        (B.CAT_COV_BLOCK_DIAG, 128, 4096, 2000),
+                                        (B.CAT_COV_FULL, 1, 200, 500)])
+def test_cov_scales_by_the_square(mode, k, d, n):
+    say(f"cov scaling mode={mode} k={k} d={d} n={n}")
+    torch = torch_mod()
+    X, _ = _inputs(n, d, k if k > 1 else 8, "bf16", "bf16", seed=d + n)
+    shape = (d, d) if mode == B.CAT_COV_FULL else (d // k, k, k)
+    accs = []
+    for m in (0, 12):
+        acc = torch.zeros(shape, dtype=torch.float32, device="cuda")
+        cat.cat_cov_accumulate(dev(np.ldexp(X, m), "bf16"), acc, mode, k)
+        accs.append(host(acc))
+    assert np.array_equal(accs[1], np.ldexp(accs[0], 24))
+
+
+def test_sqnr_sums_scale_and_ratio_is_unchanged():
+    say("sqnr scaling")
+    torch = torch_mod()
+    rng = np.random.default_rng(11)
+    count = 1_000_003
+    y = rng.standard_normal(count).astype(np.float32)
+    yt = (y + 0.05 * rng.standard_normal(count)).astype(np.float32)
+    ws = torch.empty(cat.cat_sqnr_workspace_bytes(count), dtype=torch.uint8, device="cuda")
+    outs = []
+    for m in (0, 40):
+        out = torch.empty(3, dtype=torch.float64, device="cuda")
+        cat.cat_sqnr(dev(np.ldexp(y, m), "f32"), dev(np.ldexp(yt, m), "f32"), ws, out)
+        outs.append(host(out))
+    assert outs[1][0] == np.ldexp(outs[0][0], 80)
+    assert outs[1][1] == np.ldexp(outs[0][1], 80)
+    assert outs[1][2] == outs[0][2]

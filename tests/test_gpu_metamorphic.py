@@ -1,6 +1,12 @@
-"""Power-of-two scaling through the device path, with no oracle involved.
+"""Properties of the device path that need no oracle.
 
-Multiplying X by 2^m multiplies every product, every fp32 or fp64 partial
+Token permutation: every token is quantized on its own (Sec. 6: dynamic
+per-token ranges), with the same arithmetic whichever tile, lane or
+workgroup takes it, so permuting the rows of X must permute the codes and
+scales bit for bit; permuting the GEMM's rows and output channels must
+permute y~ bit for bit (Sec. 3, eq. 5).
+
+Power-of-two scaling: multiplying X by 2^m multiplies every product, every fp32 or fp64 partial
 sum, z and the row maximum by exactly 2^m (no value leaves the normal
 range here), so the quantizer's u = fl(z fl(qmax / amax)) is unchanged:
 the codes must be bit-identical and s_x must scale by exactly 2^m (the
@@ -132,3 +138,38 @@ def test_sqnr_sums_scale_and_ratio_is_unchanged():
     assert outs[1][0] == np.ldexp(outs[0][0], 80)
     assert outs[1][1] == np.ldexp(outs[0][1], 80)
     assert outs[1][2] == outs[0][2]
+
+
+@pytest.mark.parametrize("d,k,n,x_dtype,t_dtype", PATHS + [(4096, 128, 3000, "bf16", "bf16"),
+                                                          (8192, 128, 2500, "bf16", "bf16")])
+def test_transform_quant_token_permutation(d, k, n, x_dtype, t_dtype):
+    say(f"tq token permutation d={d} k={k} n={n} {x_dtype}/{t_dtype}")
+    X, T = _inputs(n, d, k, x_dtype, t_dtype, seed=d + k + n + 5)
+    perm = np.random.default_rng(n).permutation(n)
+    for bits in (4, 8):
+        c0, s0, _ = _tq(X, T, k, x_dtype, t_dtype, bits)
+        c1, s1, _ = _tq(X[perm], T, k, x_dtype, t_dtype, bits)
+        assert np.array_equal(c0[perm], c1) and np.array_equal(s0[perm], s1), f"bits={bits}"
+    c0, s0, z0 = _tq(X, T, k, x_dtype, t_dtype, 4, asym=True)
+    c1, s1, z1 = _tq(X[perm], T, k, x_dtype, t_dtype, 4, asym=True)
+    assert np.array_equal(c0[perm], c1) and np.array_equal(s0[perm], s1)
+    assert np.array_equal(z0[perm], z1)
+
+
+@pytest.mark.parametrize("n,d_in,d_out", [(300, 4096, 1000), (2048, 1024, 4096)])
+def test_w4a4_linear_row_and_column_permutation(n, d_in, d_out):
+    say(f"w4a4 permutation n={n} d_in={d_in} d_out={d_out}")
+    torch = torch_mod()
+    rng = np.random.default_rng(n + d_in)
+    qx = rng.integers(-7, 8, size=(n, d_in)).astype(np.int8)
+    qw = rng.integers(-7, 8, size=(d_out, d_in)).astype(np.int8)
+    sx = rng.uniform(0.01, 1.0, n).astype(np.float32)
+    sw = rng.uniform(0.01, 1.0, d_out).astype(np.float32)
+    pr, pc = rng.permutation(n), rng.permutation(d_out)
+    ys = []
+    for a, b, c, e in ((qx, sx, qw, sw), (qx[pr], sx[pr], qw[pc], sw[pc])):
+        y = torch.empty((n, d_out), dtype=torch.float32, device="cuda")
+        cat.cat_w4a4_linear(dev(o.pack_int4(a), "u8"), dev(b, "f32"), dev(o.pack_int4(c), "u8"),
+                            dev(e, "f32"), y)
+        ys.append(host(y))
+    assert np.array_equal(ys[0][np.ix_(pr, pc)], ys[1])

@@ -173,3 +173,49 @@ def test_w4a4_linear_row_and_column_permutation(n, d_in, d_out):
                             dev(e, "f32"), y)
         ys.append(host(y))
     assert np.array_equal(ys[0][np.ix_(pr, pc)], ys[1])
+
+
+@pytest.mark.parametrize("d,k,n,x_dtype,t_dtype", PATHS + [(8192, 128, 700, "bf16", "bf16")])
+def test_transform_quant_block_permutation(d, k, n, x_dtype, t_dtype):
+    # permuting the channel blocks of X with their T_b permutes the code
+    # blocks; the row maximum is a maximum over blocks, so s_x (and the
+    # asymmetric minimum) stay bit-identical (Sec. 4, eq. 10: T is
+    # block-diagonal, each block acting on its own channels)
+    say(f"tq block permutation d={d} k={k} n={n} {x_dtype}/{t_dtype}")
+    X, T = _inputs(n, d, k, x_dtype, t_dtype, seed=d + 7 * k + n)
+    nb = d // k
+    pb = np.random.default_rng(d + n).permutation(nb)
+    cols = (pb[:, None] * k + np.arange(k)[None, :]).reshape(-1)
+    Xp, Tp = np.ascontiguousarray(X[:, cols]), np.ascontiguousarray(T[pb])
+    for bits in (4, 8):
+        c0, s0, _ = _tq(X, T, k, x_dtype, t_dtype, bits)
+        c1, s1, _ = _tq(Xp, Tp, k, x_dtype, t_dtype, bits)
+        q0 = o.unpack_int4(c0) if bits == 4 else c0.view(np.int8)
+        q1 = o.unpack_int4(c1) if bits == 4 else c1.view(np.int8)
+        assert np.array_equal(q0[:, cols], q1) and np.array_equal(s0, s1), f"bits={bits}"
+    c0, s0, z0 = _tq(X, T, k, x_dtype, t_dtype, 4, asym=True)
+    c1, s1, z1 = _tq(Xp, Tp, k, x_dtype, t_dtype, 4, asym=True)
+    assert np.array_equal(o.unpack_int4(c0)[:, cols], o.unpack_int4(c1))
+    assert np.array_equal(s0, s1) and np.array_equal(z0, z1)
+
+
+@pytest.mark.parametrize("n,d_in,d_out", [(300, 4096, 1000), (1000, 160, 700)])
+def test_w4a4_linear_reduction_order(n, d_in, d_out):
+    # the same permutation of the reduction index on both operands leaves
+    # the exact integer sums, and so y~, bit-identical
+    say(f"w4a4 reduction permutation n={n} d_in={d_in} d_out={d_out}")
+    torch = torch_mod()
+    rng = np.random.default_rng(n + 3 * d_in)
+    qx = rng.integers(-7, 8, size=(n, d_in)).astype(np.int8)
+    qw = rng.integers(-7, 8, size=(d_out, d_in)).astype(np.int8)
+    sx = rng.uniform(0.01, 1.0, n).astype(np.float32)
+    sw = rng.uniform(0.01, 1.0, d_out).astype(np.float32)
+    pk = rng.permutation(d_in)
+    dsx, dsw = dev(sx, "f32"), dev(sw, "f32")
+    ys = []
+    for a, c in ((qx, qw), (qx[:, pk], qw[:, pk])):
+        y = torch.empty((n, d_out), dtype=torch.float32, device="cuda")
+        acc = torch.empty((n, d_out), dtype=torch.int32, device="cuda")
+        cat.cat_w4a4_linear(dev(o.pack_int4(a), "u8"), dsx, dev(o.pack_int4(c), "u8"), dsw, y, acc)
+        ys.append((host(y), host(acc)))
+    assert np.array_equal(ys[0][1], ys[1][1]) and np.array_equal(ys[0][0], ys[1][0])

@@ -212,7 +212,10 @@ __global__ __launch_bounds__(kCovThreads) void cov_mfma_kernel(const uint16_t* _
 
 // ------------------------------------------------------- vector-ALU path
 // 64 x 64 tile, 16 x 16 threads each owning 4 x 4 outputs; 16-token slabs
-// staged in LDS as fp32.
+// staged in LDS as fp32.  The partial sums are fp64 and reach acc rounded
+// once per flush: with fp32 running sums over thousands of tokens, a column
+// of heavy-tailed values (say Student-t with two degrees of freedom) left
+// its sum of squares about 1e-5 off.
 template <typename XT>
 __global__ __launch_bounds__(kCovThreads) void cov_valu_kernel(const XT* __restrict__ X, int64_t n,
                                                                int64_t d, int mode, int64_t k,
@@ -225,7 +228,7 @@ __global__ __launch_bounds__(kCovThreads) void cov_valu_kernel(const XT* __restr
     const int ti = threadIdx.x / 16, tj = threadIdx.x % 16;
     for (int64_t f0 = 0; f0 < n; f0 += kCovFlush) {
         const int64_t f1 = f0 + kCovFlush < n ? f0 + kCovFlush : n;
-        float part[4][4] = {};
+        double part[4][4] = {};
         for (int64_t t0 = f0; t0 < f1; t0 += TKV) {
             for (int e = threadIdx.x; e < TKV * TILE; e += kCovThreads) {
                 const int tt = e / TILE, c = e % TILE;
@@ -245,7 +248,9 @@ __global__ __launch_bounds__(kCovThreads) void cov_valu_kernel(const XT* __restr
 #pragma unroll
                 for (int p = 0; p < 4; ++p)
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) part[p][q] = fmaf(a[p], b[q], part[p][q]);
+                    for (int q = 0; q < 4; ++q)
+                        part[p][q] = fma(static_cast<double>(a[p]), static_cast<double>(b[q]),
+                                         part[p][q]);
             }
             __syncthreads();
         }
@@ -256,10 +261,10 @@ __global__ __launch_bounds__(kCovThreads) void cov_valu_kernel(const XT* __restr
                 const int64_t gi = ct.I0 + 4 * ti + p, gj = ct.J0 + 4 * tj + q;
                 if (gi >= ct.dim || gj >= ct.dim) continue;
                 float* ptr = acc + ct.base + gi * ct.dim + gj;
-                *ptr = *ptr + part[p][q];
+                *ptr = static_cast<float>(*ptr + part[p][q]);
                 if (!diag) {
                     float* m = acc + ct.base + gj * ct.dim + gi;
-                    *m = *m + part[p][q];
+                    *m = static_cast<float>(*m + part[p][q]);
                 }
             }
     }

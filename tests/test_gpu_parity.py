@@ -612,6 +612,29 @@ def test_cov_block_diag_full_size_batch(name, k):
     assert err <= 1e-5
 
 
+@pytest.mark.parametrize("mode,k,d,n,dtype,seed", [
+    (B.CAT_COV_BLOCK_DIAG, 1, 512, 3000, "bf16", 122),
+    (B.CAT_COV_BLOCK_DIAG, 16, 512, 5000, "bf16", 92),
+    (B.CAT_COV_FULL, 1, 200, 5000, "f32", 7),
+])
+def test_cov_heavy_tailed_columns(mode, k, d, n, dtype, seed):
+    # Student-t (two degrees of freedom) columns on the vector-ALU path
+    # (blocks under 64 channels, fp32 X): sums of squares whose terms span
+    # many orders of magnitude.  fp32 running sums left the k = 1 case of
+    # seed 122 at 1.14e-5; the kernel's fp64 partials keep it near 1e-7
+    say(f"cov heavy tails mode={mode} k={k} d={d} n={n} {dtype}")
+    rng = np.random.default_rng(seed)
+    X = o.round_storage((rng.standard_t(2, (n, d)) * np.exp(0.7 * rng.standard_normal(d))
+                         ).astype(np.float32), dtype)
+    acc = _cov_gpu(X, dtype, mode, k)
+    S = o.second_moment_sum(X)
+    ref = S if mode == B.CAT_COV_FULL else _blocks(S, k)
+    err = rel_fro(acc, ref)
+    say(f"  rel Frobenius {err:.2e}")
+    assert err <= 1e-5
+    assert err <= 1e-6
+
+
 def test_cov_split_batches_equal_one_shot():
     say("cov split batches")
     cfg = wl.get_config("attn4096", d_in=256, d_out=256, n_cal=3000, n=1)

@@ -150,7 +150,10 @@ int cat_cov_accumulate(const void* X, int x_dtype, int64_t n, int64_t d,
  * workspace with bounded waits.
  * Its grid never exceeds the device's resident capacity, so every wait ends
  * once the launch has the device; work from other streams that holds CUs
- * for seconds can still make a wait run out.  Then the 32-bit word at byte
+ * for seconds can still make a wait run out.  In particular, two such calls
+ * (cat_transform_quant, _asym or _noalloc) must not run at the same time on
+ * one device: each may hold CUs that the other's waiting workgroups need.
+ * Issue them on one stream, or order them with events.  Then the 32-bit word at byte
  * offset cat_transform_quant_flag_offset(n, d, k) of the workspace is set
  * to a non-zero value, and the call's results must be treated as invalid.
  * No wrong scale is ever used even then: every workgroup reads a token's

@@ -114,6 +114,39 @@ def test_w4a4_linear_many_short_tiles_per_workgroup(d_in):
     assert torch.equal(y2, y)
 
 
+@pytest.mark.parametrize("n,d_in,d_out,with_acc,int8", [
+    (512, 1024, 512, False, False), (300, 800, 510, True, False), (512, 1024, 512, False, True),
+])
+def test_linear_scales_across_the_fp32_range(n, d_in, d_out, with_acc, int8):
+    # scales log-uniform over 1e-30 .. 1e30 (and some zero): y~ =
+    # fl(fl(acc) s_x) s_w runs into subnormal and infinite values, which
+    # the epilogue must round as IEEE fp32 does (no flush to zero), bit for
+    # bit with the oracle; full tiles without acc_out take the straight-line
+    # epilogue, the others the checked one
+    say(f"linear extreme scales n={n} d_in={d_in} d_out={d_out} acc={with_acc} int8={int8}")
+    torch = torch_mod()
+    rng = np.random.default_rng(n + d_out + int8)
+    sx = np.exp(rng.uniform(np.log(1e-30), np.log(1e30), n)).astype(np.float32)
+    sw = np.exp(rng.uniform(np.log(1e-30), np.log(1e30), d_out)).astype(np.float32)
+    sx[rng.random(n) < 0.05] = 0.0
+    qmax = 127 if int8 else 7
+    qx = wl.random_codes(n, d_in, n + 1, qmax=qmax)
+    qw = wl.random_codes(d_out, d_in, n + 2, qmax=qmax)
+    with np.errstate(over="ignore"):
+        acc_or, y_or = o.w4a4_linear(qx, sx, qw, sw)
+    assert np.isinf(y_or).any() and ((y_or != 0) & (np.abs(y_or) < np.finfo(np.float32).tiny)).any()
+    y = torch.empty((n, d_out), dtype=torch.float32, device="cuda")
+    acc = torch.empty((n, d_out), dtype=torch.int32, device="cuda") if with_acc else None
+    if int8:
+        cat.cat_int8_linear(dev(qx, "i8"), dev(sx, "f32"), dev(qw, "i8"), dev(sw, "f32"), y, acc)
+    else:
+        cat.cat_w4a4_linear(dev(o.pack_int4(qx), "u8"), dev(sx, "f32"), dev(o.pack_int4(qw), "u8"),
+                            dev(sw, "f32"), y, acc)
+    assert np.array_equal(host(y), y_or)
+    if with_acc:
+        assert np.array_equal(host(acc), acc_or)
+
+
 def test_w4a4_linear_extreme_codes_at_max_d_in():
     torch = torch_mod()
     d_in = B.CAT_MAX_D_IN

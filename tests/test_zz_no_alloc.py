@@ -1,7 +1,8 @@
 """The allocation-free transform+quant entry point against the workspace
 one: identical codes and scales on two calls in a row (the second with a
 smaller input that leaves the first call's words in the shared scratch),
-through the C ABI, on the single-pass and two-pass shapes."""
+through the C ABI, on the single-pass and two-pass shapes, and captured
+in a graph and replayed with new inputs."""
 import numpy as np
 import pytest
 
@@ -60,6 +61,46 @@ def test_noalloc_equals_workspace_entry_point_twice(d, n_first, n_second, bits):
         assert np.array_equal(s_na, s_ref), f"scales differ on call {i + 1}"
         # and the workspace path itself is right, to the oracle's bar
         check_codes(c_na, X, T, bits, label=f"noalloc n={n}")
+
+
+@pytest.mark.parametrize("d", [4096, 1024])
+def test_noalloc_graph_replays_match_the_workspace_entry_point(d):
+    # the callers this entry point is for capture it: a captured call
+    # replayed with new activations, eager calls of both entry points in
+    # between (the eager allocation-free ones share the captured call's
+    # scratch), each replay bit for bit equal to the workspace entry point
+    # (d = 4096: the single pass with its device-made tags; d = 1024: two
+    # passes, whose words are cleared by a kernel, not a memset)
+    say(f"noalloc graph capture d={d}: 3 replays with new X, eager calls between")
+    torch = torch_mod()
+    n, k = 300, 128
+    T = _T(d, k, seed=d + 1)
+    dT = dev(T, "bf16")
+    Xs = [_X(n, d, seed=50 + i) for i in range(3)]
+    dX = dev(Xs[0], "bf16")
+    codes = torch.empty((n, d // 2), dtype=torch.uint8, device="cuda")
+    s_x = torch.empty(n, dtype=torch.float32, device="cuda")
+    B.cat_transform_quant_noalloc(dX, dT, k, codes, s_x)       # eager warm-up
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    with torch.cuda.graph(g, stream=side):
+        B.cat_transform_quant_noalloc(dX, dT, k, codes, s_x)
+    c_e, s_e = torch.empty_like(codes), torch.empty_like(s_x)
+    ws = torch.empty(cat.cat_transform_quant_workspace_bytes(n, d, k), dtype=torch.uint8,
+                     device="cuda")
+    for i, X in enumerate(Xs):
+        dX.copy_(dev(X, "bf16"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        c, sx = host(codes), host(s_x)
+        cat.cat_transform_quant(dX, dT, k, c_e, s_e, ws)
+        torch.cuda.synchronize()
+        assert np.array_equal(host(c_e), c) and np.array_equal(host(s_e), sx), f"replay {i}"
+        B.cat_transform_quant_noalloc(dX, dT, k, c_e, s_e)   # eager, shared scratch
+        torch.cuda.synchronize()
+        assert np.array_equal(host(c_e), c) and np.array_equal(host(s_e), sx), f"eager {i}"
 
 
 def test_noalloc_rejects_inputs_beyond_its_scratch():

@@ -153,9 +153,10 @@ int cat_cov_accumulate(const void* X, int x_dtype, int64_t n, int64_t d,
  * for seconds can still make a wait run out.  In particular, two such calls
  * (cat_transform_quant, _asym or _noalloc) must not run at the same time on
  * one device: each may hold CUs that the other's waiting workgroups need.
- * Issue them on one stream, or order them with events.  Then the 32-bit word at byte
- * offset cat_transform_quant_flag_offset(n, d, k) of the workspace is set
- * to a non-zero value, and the call's results must be treated as invalid.
+ * Issue them on one stream, or order them with events.  When a wait runs
+ * out, the 32-bit word at byte offset cat_transform_quant_flag_offset(n, d,
+ * k) of the workspace is set to a non-zero value, and the call's results
+ * must be treated as invalid.
  * No wrong scale is ever used even then: every workgroup reads a token's
  * row maximum on its own and uses the exact value or NaN, so each
  * 128-channel block of a token's codes is exact or (where that block's

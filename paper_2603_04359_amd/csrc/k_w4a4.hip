@@ -8,7 +8,11 @@
 // 2 x 4 grid, each wave 128 x 64 = 4 x 2 MFMA tiles with int32
 // accumulators; one workgroup per CU (two waves per SIMD, 144 KiB of LDS).
 // One K step covers 128 codes (64 packed bytes per row); a tile reads
-// 32 KiB of packed codes per step.
+// 32 KiB of packed codes per step.  When 256-token tiles would leave CUs
+// idle (fewer tiles than workgroup slots) and 128-token tiles take no more
+// rounds of the grid, the launch uses 128 x 256 tiles instead: each wave
+// 64 x 64 (2 x 2 MFMA tiles), the same ring and schedule, 24 KiB per step
+// spread as three direct loads per wave.
 //
 // Ping-pong schedule: waves 0-3 (rows 0-127 of the tile, one wave per
 // SIMD) and waves 4-7 (rows 128-255, the other wave of each SIMD) are
@@ -23,7 +27,8 @@
 // Operand path: packed INT4 tiles go straight from global memory into an
 // LDS ring of kStages (4) steps with global_load_lds_dwordx4 (no register
 // staging, no LDS store instructions), requested kStages-1 steps ahead;
-// waves 0-3 load operand A (codes_x), waves 4-7 operand B (codes_w).  The
+// waves 0-3 load operand A (codes_x), waves 4-7 operand B (codes_w) (with
+// 128-token tiles waves 0-3 also load B's first 64 rows).  The
 // barrier waits for LDS traffic only (a plain workgroup barrier would also
 // drain the loads in flight); each wave waits for its own loads of the next
 // step (vmcnt) before the barrier that publishes it.  Each lane reads 16
@@ -67,7 +72,7 @@ namespace catk {
 
 constexpr int kGemmWaves = 8;
 constexpr int kGemmThreads = kGemmWaves * 64;
-constexpr int kBM = 256;           // tokens per tile
+constexpr int kBM = 256;           // tokens per tile (the LDS layout's maximum)
 constexpr int kBN = 256;           // outputs per tile
 constexpr int kKBP = 64;           // packed bytes per row per K step (128 codes)
 constexpr int kUP = kKBP / 16;     // 16-byte units per row per step
@@ -85,8 +90,9 @@ struct GemmTile {
     int64_t m0, n0;
 };
 
+template <int BM>
 __device__ __forceinline__ bool gemm_tile(int64_t k, int64_t n, int64_t d_out, GemmTile& t) {
-    const int64_t tiles_m = (n + kBM - 1) / kBM;
+    const int64_t tiles_m = (n + BM - 1) / BM;
     const int64_t tiles_n = (d_out + kBN - 1) / kBN;
     const int64_t T = tiles_m * tiles_n;
     const int64_t per_xcd = (T + kXcd - 1) / kXcd;
@@ -100,7 +106,7 @@ __device__ __forceinline__ bool gemm_tile(int64_t k, int64_t n, int64_t d_out, G
     const int64_t first_m = group * kGroupM;
     const int64_t gm = (tiles_m - first_m) < kGroupM ? (tiles_m - first_m) : kGroupM;
     const int64_t in_group = tau % (kGroupM * tiles_n);
-    t.m0 = (first_m + in_group % gm) * kBM;
+    t.m0 = (first_m + in_group % gm) * BM;
     t.n0 = (in_group / gm) * kBN;
     return true;
 }
@@ -112,12 +118,16 @@ __device__ __forceinline__ i32x4 widen8(u32x4 v, int half) {
 }
 
 constexpr int kPpUnits = kBM * kUP;                        // units per operand stage
-constexpr int kPpLoads = kPpUnits / (kGemmThreads / 2);    // direct loads per thread per step
+// direct loads (64-slot instructions) per wave and step: 4 with 256-token
+// tiles (group 0 loads A, group 1 B); 3 with 128-token tiles (A's 8
+// chunks and B's first 4 from group 0, B's other 12 from group 1)
+template <int BM>
+constexpr int gemm_loads() { return BM == kBM ? 4 : 3; }
 // scale slots: a tile's slot is reused 8 tiles later, after both groups'
 // epilogues of the earlier tile even when every tile is one K step
 constexpr int kScaleSlots = 8;
 static_assert(kBM == kBN, "both operands share the stage layout");
-static_assert(kPpLoads == 4, "four 64-slot instructions per wave per step");
+static_assert(kPpUnits / (kGemmThreads / 2) == 4, "four 64-slot instructions per wave per step");
 
 // ring[o][stage]: operand o (0 = A, 1 = B), kStages steps deep.
 // sscale[slot]: s_x of a tile's rows and s_w of its outputs; slot = tile
@@ -133,7 +143,7 @@ typedef float GemmScales[kScaleSlots][kBM + kBN];
 // minimum zmin_x, weights with row code sums rsum_w: the epilogue adds
 // 8 R_o back (int32, exact) and forms
 // y = fl(fl(fl(acc) s_x) + fl(zmin fl(R_o))) s_w.
-template <bool I8, bool ASYM>
+template <bool I8, bool ASYM, int BM>
 __device__ __forceinline__ void gemm_body(
     const uint8_t* __restrict__ qx, const float* __restrict__ s_x,
     const uint8_t* __restrict__ qw, const float* __restrict__ s_w, int64_t n, int64_t d_in,
@@ -141,6 +151,9 @@ __device__ __forceinline__ void gemm_body(
     GemmScales& sscale, const float* __restrict__ zmin_x, const int32_t* __restrict__ rsum_w,
     GemmScales* sasym) {
     static_assert(!(I8 && ASYM), "asymmetric codes are INT4");
+    static_assert(BM == kBM || BM == kBM / 2, "256- or 128-token tiles");
+    constexpr int IM = BM / 64;            // 32-row accumulator groups per wave
+    constexpr int NL = gemm_loads<BM>();
     const int64_t row_bytes = I8 ? d_in : d_in / 2;
     const int nk = static_cast<int>((row_bytes + kKBP - 1) / kKBP);
 
@@ -157,48 +170,66 @@ __device__ __forceinline__ void gemm_body(
     int n_tiles = 0;
     {
         GemmTile t;
-        while (gemm_tile(n_tiles, n, d_out, t)) ++n_tiles;
+        while (gemm_tile<BM>(n_tiles, n, d_out, t)) ++n_tiles;
     }
     if (n_tiles == 0) return;
     const int G = n_tiles * nk;
 
-    // Direct loads of this wave's operand: instruction q fills slots
-    // [64 (4q + w4), +64) of the stage; slot s holds row s / 4, logical unit
-    // (s % 4) ^ swz(row).  swz(row) depends on lane bits 4-5 only.
-    const uint8_t* src = grp == 0 ? qx : qw;
-    const int64_t src_rows = grp == 0 ? n : d_out;
-    const uint8_t* src_base = src;
-    uint32_t src_off[kPpLoads];
+    // Direct loads: instruction q of this wave fills chunk ch(q) (64 slots,
+    // 16 rows) of operand op(q)'s stage; slot s of a chunk holds row s / 4
+    // of the chunk, logical unit (s % 4) ^ swz(row).  swz(row) depends on
+    // lane bits 4-5 only.  256-token tiles: group 0 loads A, group 1 B,
+    // chunk 4q + w4.  128-token tiles: group 0 loads A's chunks 2 w4, 2 w4
+    // + 1 and B's chunk w4, group 1 B's chunks 4 + 3 w4 + q.
+    auto ld_op = [&](int q) { return BM == kBM ? grp : (grp == 1 || q == 2 ? 1 : 0); };
+    auto ld_ch = [&](int q) {
+        if constexpr (BM == kBM) return 4 * q + w4;
+        return grp == 0 ? (q < 2 ? 2 * w4 + q : w4) : 4 + 3 * w4 + q;
+    };
+    const uint8_t* base_a = qx;
+    const uint8_t* base_b = qw;
+    uint32_t src_off[NL];
     const int u_off = ((lane % kUP) ^ gemm_swz(lane / kUP)) * 16;
     // row offsets inside a tile are below 256 * 65536 bytes: 32-bit
     const uint32_t rb32 = static_cast<uint32_t>(row_bytes);
     auto set_rows = [&](const GemmTile& tl) {
-        const int64_t r0 = grp == 0 ? tl.m0 : tl.n0;
-        src_base = src + r0 * row_bytes;
-        const int rows_left = static_cast<int>(src_rows - r0 < kBM ? src_rows - r0 : kBM);
+        base_a = qx + tl.m0 * row_bytes;
+        base_b = qw + tl.n0 * row_bytes;
+        const int left_a = static_cast<int>(n - tl.m0 < BM ? n - tl.m0 : BM);
+        const int left_b = static_cast<int>(d_out - tl.n0 < kBN ? d_out - tl.n0 : kBN);
         int el = lane;
         asm volatile("" : "+v"(el));
 #pragma unroll
-        for (int q = 0; q < kPpLoads; ++q) {
-            const int r = (q * 4 + w4) * (64 / kUP) + el / kUP;
-            const int rr = r < rows_left ? r : rows_left - 1;   // clamped rows: never stored
+        for (int q = 0; q < NL; ++q) {
+            const int r = ld_ch(q) * (64 / kUP) + el / kUP;
+            const int left = ld_op(q) == 0 ? left_a : left_b;
+            const int rr = r < left ? r : left - 1;   // clamped rows: never stored
             src_off[q] = static_cast<uint32_t>(rr) * rb32;
         }
     };
-    const uint32_t lds0 = static_cast<uint32_t>(
-        __builtin_amdgcn_readfirstlane(lds_addr(&ring[grp][0][w4 * 64])));
+    uint32_t lds_q[NL];
+#pragma unroll
+    for (int q = 0; q < NL; ++q)
+        lds_q[q] = static_cast<uint32_t>(
+            __builtin_amdgcn_readfirstlane(lds_addr(&ring[ld_op(q)][0][ld_ch(q) * 64])));
     auto issue_step = [&](int kt, int st) {
         const int64_t k0 = static_cast<int64_t>(kt) * kKBP;
         int64_t col = k0 + u_off;
         col = col < row_bytes ? col : 0;      // past the row end: any in-bounds unit
         const uint32_t cu = static_cast<uint32_t>(col);
-        const uint32_t l = lds0 + static_cast<uint32_t>(st) * (kPpUnits * 16);
+        const uint32_t so = static_cast<uint32_t>(st) * (kPpUnits * 16);
 #pragma unroll
-        for (int q = 0; q < kPpLoads; ++q) dma16(src_base, src_off[q] + cu, l + q * (4 * 1024u));
+        for (int q = 0; q < NL; ++q)
+            dma16(ld_op(q) == 0 ? base_a : base_b, src_off[q] + cu, lds_q[q] + so);
     };
-    // s_x (group 0) or s_w (group 1) of a tile into its scale slot: rows /
-    // outputs past the end load the last one (never stored)
+    // s_x (group 0) or s_w (group 1) of a tile into its scale slot (s_x at
+    // [0, BM), s_w at [kBM, kBM + kBN)): rows / outputs past the end load
+    // the last one (never stored).  With 128-token tiles waves 0 and 1 load
+    // s_x and waves 2 and 3 load none.
+    const int64_t src_rows = grp == 0 ? n : d_out;
+    const bool ld_scales = grp == 1 || 64 * w4 < BM;
     auto issue_scales = [&](const GemmTile& tl, int slot) {
+        if (!ld_scales) return;
         const int64_t r = (grp == 0 ? tl.m0 : tl.n0) + 64 * w4 + lane;
         dma4(grp == 0 ? s_x : s_w, static_cast<uint32_t>((r < src_rows ? r : src_rows - 1) * 4),
              lds_addr(&sscale[slot][grp * kBM + 64 * w4]));
@@ -216,19 +247,19 @@ __device__ __forceinline__ void gemm_body(
     auto clear_ragged = [&](int kt, int st) {
         if (grp == 0 && kt == nk - 1 && (row_bytes % kKBP) != 0) {
 #pragma unroll
-            for (int q = 0; q < kPpLoads; ++q)
-                if (static_cast<int64_t>(kt) * kKBP + u_off >= row_bytes)
-                    ring[0][st][(q * 4 + w4) * 64 + lane] = u32x4{0u, 0u, 0u, 0u};
+            for (int q = 0; q < NL; ++q)
+                if (ld_op(q) == 0 && static_cast<int64_t>(kt) * kKBP + u_off >= row_bytes)
+                    ring[0][st][ld_ch(q) * 64 + lane] = u32x4{0u, 0u, 0u, 0u};
         }
     };
 
-    i32x16 acc[4][2];
+    i32x16 acc[IM][2];
     // Fragments of one K step, read in the load phase: unit u = 2h + c of
     // each row (c = 0, 1), 32 codes each; sub-step s = 2c + half covers
     // codes [32 s, 32 s + 32) of the step (a permutation of the reduction
     // index shared by both operands).  A stays packed until the compute
     // phase; B is widened in the load phase.
-    u32x4 pa[2][4];
+    u32x4 pa[2][IM];
     i32x4 fb[4][2];
     // Row r = base + 32 i + l32 of a fragment has swz(r) = swz(l32) (bits 2
     // and 3 of r come from l32), so each unit's address is one per-lane
@@ -238,13 +269,13 @@ __device__ __forceinline__ void gemm_body(
     // (int8 codes: unit c of the lane is sub-step c as it is; fb[0..1] hold
     // B's two units)
     auto load_frags = [&](int st) {
-        const u32x4* ra = &ring[0][st][wm * 128 * kUP + frag_lane];
+        const u32x4* ra = &ring[0][st][wm * (BM / 2) * kUP + frag_lane];
         const u32x4* rb = &ring[1][st][wn * 64 * kUP + frag_lane];
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
             const int uo = frag_u0 ^ c;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) pa[c][i] = ra[i * 32 * kUP + uo];
+            for (int i = 0; i < IM; ++i) pa[c][i] = ra[i * 32 * kUP + uo];
 #pragma unroll
             for (int j = 0; j < 2; ++j) {
                 const u32x4 pbj = rb[j * 32 * kUP + uo];
@@ -263,13 +294,13 @@ __device__ __forceinline__ void gemm_body(
         __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int s = 0; s < (I8 ? 2 : 4); ++s) {
-            i32x4 wa[4];
+            i32x4 wa[IM];
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < IM; ++i)
                 wa[i] = I8 ? __builtin_bit_cast(i32x4, pa[s][i]) : widen8(pa[s >> 1][i], s & 1);
             const i32x4* wb = fb[s];
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < IM; ++i)
 #pragma unroll
                 for (int j = 0; j < 2; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_i32_32x32x32_i8(wa[i], wb[j], acc[i][j], 0,
@@ -293,9 +324,9 @@ __device__ __forceinline__ void gemm_body(
         const int64_t tile_off = tl.m0 * d_out + tl.n0;
         float* yt = y + tile_off;
         int32_t* at = acc_out ? acc_out + tile_off : nullptr;
-        const int rows_left = static_cast<int>(n - tl.m0 < kBM ? n - tl.m0 : kBM);
+        const int rows_left = static_cast<int>(n - tl.m0 < BM ? n - tl.m0 : BM);
         const int cols_left = static_cast<int>(d_out - tl.n0 < kBN ? d_out - tl.n0 : kBN);
-        if (rows_left == kBM && cols_left == kBN && !at && d_out < (int64_t{1} << 29)) {
+        if (rows_left == BM && cols_left == kBN && !at && d_out < (int64_t{1} << 29)) {
             // full tile: straight-line code, a wave-uniform row base per
             // accumulator row plus a 32-bit per-lane offset (row 4h, column
             // of fragment j; below 2^32 for d_out < 2^29), no bounds checks
@@ -312,23 +343,23 @@ __device__ __forceinline__ void gemm_body(
                     rs[j] = __float_as_int(za[kBM + wn * 64 + j * 32 + l32]);
             }
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
+            for (int i = 0; i < IM; ++i) {
                 float sx[16], zm[16];
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
-                    const f32x4 v = *reinterpret_cast<const f32x4*>(sc + wm * 128 + i * 32 + 8 * q + 4 * h);
+                    const f32x4 v = *reinterpret_cast<const f32x4*>(sc + wm * (BM / 2) + i * 32 + 8 * q + 4 * h);
 #pragma unroll
                     for (int e = 0; e < 4; ++e) sx[4 * q + e] = v[e];
                     if constexpr (ASYM) {
                         const f32x4 z = *reinterpret_cast<const f32x4*>(
-                            za + wm * 128 + i * 32 + 8 * q + 4 * h);
+                            za + wm * (BM / 2) + i * 32 + 8 * q + 4 * h);
 #pragma unroll
                         for (int e = 0; e < 4; ++e) zm[4 * q + e] = z[e];
                     }
                 }
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
-                    float* yr = yt + static_cast<int64_t>(wm * 128 + i * 32 + 8 * (r >> 2) + (r & 3)) * d_out;
+                    float* yr = yt + static_cast<int64_t>(wm * (BM / 2) + i * 32 + 8 * (r >> 2) + (r & 3)) * d_out;
 #pragma unroll
                     for (int j = 0; j < 2; ++j) {
                         const int v = acc[i][j][r] >> kShift;
@@ -345,12 +376,12 @@ __device__ __forceinline__ void gemm_body(
             return;
         }
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int rb = wm * 128 + i * 32 + 4 * h;
+        for (int i = 0; i < IM; ++i) {
+            const int rb = wm * (BM / 2) + i * 32 + 4 * h;
             float sx[16];
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                const f32x4 v = *reinterpret_cast<const f32x4*>(sc + wm * 128 + i * 32 + 8 * q + 4 * h);
+                const f32x4 v = *reinterpret_cast<const f32x4*>(sc + wm * (BM / 2) + i * 32 + 8 * q + 4 * h);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) sx[4 * q + e] = v[e];
             }
@@ -384,7 +415,7 @@ __device__ __forceinline__ void gemm_body(
     // issue cursor: the next step whose direct loads are requested
     int is_g = 0, is_kt = 0, is_ti = 0;
     GemmTile is_tile;
-    gemm_tile(0, n, d_out, is_tile);
+    gemm_tile<BM>(0, n, d_out, is_tile);
     set_rows(is_tile);
     auto issue_next = [&]() {
         if (is_g >= G) return;
@@ -394,7 +425,7 @@ __device__ __forceinline__ void gemm_body(
         if (++is_kt == nk && is_g < G) {
             is_kt = 0;
             ++is_ti;
-            gemm_tile(is_ti, n, d_out, is_tile);
+            gemm_tile<BM>(is_ti, n, d_out, is_tile);
             set_rows(is_tile);
         }
     };
@@ -403,8 +434,8 @@ __device__ __forceinline__ void gemm_body(
     auto wait_step = [&](int g) {
         if (g >= G) return;
         const int newer = is_g - 1 - g;
-        if (newer >= 2) wait_vmcnt<2 * kPpLoads>();
-        else if (newer == 1) wait_vmcnt<kPpLoads>();
+        if (newer >= 2) wait_vmcnt<2 * NL>();
+        else if (newer == 1) wait_vmcnt<NL>();
         else wait_vmcnt<0>();
     };
 
@@ -444,7 +475,7 @@ __device__ __forceinline__ void gemm_body(
         int g = 0;   // global index of the tile's first step
         for (int ti = 0; ti < n_tiles; ++ti) {
             GemmTile tl;
-            gemm_tile(ti, n, d_out, tl);
+            gemm_tile<BM>(ti, n, d_out, tl);
             zero_acc();
             for (int i = 0; i < nk; ++i) {
                 issue_next();                        // phase 2i
@@ -464,7 +495,7 @@ __device__ __forceinline__ void gemm_body(
         int g = 0;
         for (int ti = 0; ti < n_tiles; ++ti) {
             GemmTile tl;
-            gemm_tile(ti, n, d_out, tl);
+            gemm_tile<BM>(ti, n, d_out, tl);
             zero_acc();
             phase_end();                             // phase 0
             for (int i = 0; i < nk; ++i) {
@@ -482,26 +513,29 @@ __device__ __forceinline__ void gemm_body(
     }
 }
 
+template <int BM>
 __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_gemm_kernel(
     const uint8_t* __restrict__ qx, const float* __restrict__ s_x,
     const uint8_t* __restrict__ qw, const float* __restrict__ s_w, int64_t n, int64_t d_in,
     int64_t d_out, float* __restrict__ y, int32_t* __restrict__ acc_out) {
     __shared__ __attribute__((aligned(16))) GemmRing ring;
     __shared__ __attribute__((aligned(16))) GemmScales sscale;
-    gemm_body<false, false>(qx, s_x, qw, s_w, n, d_in, d_out, y, acc_out, ring, sscale, nullptr,
+    gemm_body<false, false, BM>(qx, s_x, qw, s_w, n, d_in, d_out, y, acc_out, ring, sscale, nullptr,
                             nullptr, nullptr);
 }
 
+template <int BM>
 __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void int8_gemm_kernel(
     const uint8_t* __restrict__ qx, const float* __restrict__ s_x,
     const uint8_t* __restrict__ qw, const float* __restrict__ s_w, int64_t n, int64_t d_in,
     int64_t d_out, float* __restrict__ y, int32_t* __restrict__ acc_out) {
     __shared__ __attribute__((aligned(16))) GemmRing ring;
     __shared__ __attribute__((aligned(16))) GemmScales sscale;
-    gemm_body<true, false>(qx, s_x, qw, s_w, n, d_in, d_out, y, acc_out, ring, sscale, nullptr,
+    gemm_body<true, false, BM>(qx, s_x, qw, s_w, n, d_in, d_out, y, acc_out, ring, sscale, nullptr,
                            nullptr, nullptr);
 }
 
+template <int BM>
 __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_asym_gemm_kernel(
     const uint8_t* __restrict__ qx, const float* __restrict__ s_x,
     const uint8_t* __restrict__ qw, const float* __restrict__ s_w, int64_t n, int64_t d_in,
@@ -511,7 +545,7 @@ __global__ __launch_bounds__(kGemmThreads, kWgPerCu) void w4a4_asym_gemm_kernel(
     __shared__ __attribute__((aligned(16))) GemmScales sscale;
     // zmin of a tile's rows and the code sums of its outputs, slots as sscale
     __shared__ __attribute__((aligned(16))) GemmScales sasym;
-    gemm_body<false, true>(qx, s_x, qw, s_w, n, d_in, d_out, y, acc_out, ring, sscale, zmin_x,
+    gemm_body<false, true, BM>(qx, s_x, qw, s_w, n, d_in, d_out, y, acc_out, ring, sscale, zmin_x,
                            rsum_w, &sasym);
 }
 
@@ -524,20 +558,42 @@ static hipError_t launch_gemm(bool i8, const uint8_t* codes_x, const float* s_x,
     if (err != hipSuccess) return err;
     err = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (err != hipSuccess) return err;
-    const int64_t T = ((n + kBM - 1) / kBM) * ((d_out + kBN - 1) / kBN);
+    // 256 x 256 tiles, or 128 x 256 when the 256-token tiles leave CUs idle
+    // and the 128-token ones still take no more rounds of the grid
+    const int64_t tiles_n = (d_out + kBN - 1) / kBN;
+    const int64_t T256 = ((n + kBM - 1) / kBM) * tiles_n;
+    const int64_t T128 = ((n + kBM / 2 - 1) / (kBM / 2)) * tiles_n;
     // kWgPerCu resident workgroups per CU, a multiple of the XCD count
-    int64_t grid = (static_cast<int64_t>(cus) * kWgPerCu / kXcd) * kXcd;
+    const int64_t slots = (static_cast<int64_t>(cus) * kWgPerCu / kXcd) * kXcd;
+    const bool small = T256 < slots && (T128 + slots - 1) / slots <= (T256 + slots - 1) / slots;
+    const int64_t T = small ? T128 : T256;
+    int64_t grid = slots;
     const int64_t t_pad = ((T + kXcd - 1) / kXcd) * kXcd;
     if (grid > t_pad) grid = t_pad;
     if (grid < kXcd) grid = kXcd;
-    if (zmin_x)
-        hipLaunchKernelGGL(w4a4_asym_gemm_kernel, dim3(static_cast<uint32_t>(grid)),
-                           dim3(kGemmThreads), 0, stream, codes_x, s_x, codes_w, s_w, n, d_in,
-                           d_out, y, acc_out, zmin_x, rsum_w);
-    else
-        hipLaunchKernelGGL(i8 ? int8_gemm_kernel : w4a4_gemm_kernel,
-                           dim3(static_cast<uint32_t>(grid)), dim3(kGemmThreads), 0, stream,
-                           codes_x, s_x, codes_w, s_w, n, d_in, d_out, y, acc_out);
+    const dim3 g(static_cast<uint32_t>(grid)), blk(kGemmThreads);
+    if (zmin_x) {
+        if (small)
+            hipLaunchKernelGGL(w4a4_asym_gemm_kernel<kBM / 2>, g, blk, 0, stream, codes_x, s_x,
+                               codes_w, s_w, n, d_in, d_out, y, acc_out, zmin_x, rsum_w);
+        else
+            hipLaunchKernelGGL(w4a4_asym_gemm_kernel<kBM>, g, blk, 0, stream, codes_x, s_x,
+                               codes_w, s_w, n, d_in, d_out, y, acc_out, zmin_x, rsum_w);
+    } else if (i8) {
+        if (small)
+            hipLaunchKernelGGL(int8_gemm_kernel<kBM / 2>, g, blk, 0, stream, codes_x, s_x,
+                               codes_w, s_w, n, d_in, d_out, y, acc_out);
+        else
+            hipLaunchKernelGGL(int8_gemm_kernel<kBM>, g, blk, 0, stream, codes_x, s_x, codes_w,
+                               s_w, n, d_in, d_out, y, acc_out);
+    } else {
+        if (small)
+            hipLaunchKernelGGL(w4a4_gemm_kernel<kBM / 2>, g, blk, 0, stream, codes_x, s_x,
+                               codes_w, s_w, n, d_in, d_out, y, acc_out);
+        else
+            hipLaunchKernelGGL(w4a4_gemm_kernel<kBM>, g, blk, 0, stream, codes_x, s_x, codes_w,
+                               s_w, n, d_in, d_out, y, acc_out);
+    }
     return hipGetLastError();
 }
 

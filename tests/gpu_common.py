@@ -43,6 +43,25 @@ def dev(a, dtype):
     raise ValueError(dtype)
 
 
+def gemm_tile_rows(n, d_out):
+    """Token rows per tile the integer GEMMs launch with on this device:
+    128 when 256-row tiles would leave CUs idle and 128-row ones take no
+    more rounds of the one-workgroup-per-CU grid, else 256."""
+    torch = torch_mod()
+    slots = torch.cuda.get_device_properties(0).multi_processor_count // 8 * 8
+    tn = -(-d_out // 256)
+    t256, t128 = -(-n // 256) * tn, -(-n // 128) * tn
+    return 128 if t256 < slots and -(-t128 // slots) <= -(-t256 // slots) else 256
+
+
+def check_tile_rows(n, d_out, rows):
+    """On a 256-CU MI355X, asserts that the case runs on the expected tile
+    height (elsewhere the rule may pick another, and the case still runs)."""
+    torch = torch_mod()
+    if torch.cuda.get_device_properties(0).multi_processor_count == 256:
+        assert gemm_tile_rows(n, d_out) == rows
+
+
 def host(t):
     torch = torch_mod()
     torch.cuda.synchronize()

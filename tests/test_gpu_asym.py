@@ -10,7 +10,7 @@ import workloads as wl
 from oracle import cat_oracle as o
 from paper_2603_04359_amd import binding as B
 
-from gpu_common import dev, host, say, torch_mod
+from gpu_common import check_tile_rows, dev, host, say, torch_mod
 
 pytestmark = pytest.mark.gpu
 
@@ -140,6 +140,18 @@ def test_w4a4_linear_asym_matches_oracle(n, d_in, d_out):
     assert np.array_equal(acc, acc_or)
     assert np.array_equal(y, y_or)
     _, y2, _, _ = _asym_gemm(n, d_in, d_out, seed=n + d_out, with_acc=False)
+    assert np.array_equal(y2, y_or)
+
+
+@pytest.mark.parametrize("n,d_in,d_out,rows", [(4097, 256, 4100, 256), (1900, 4160, 3000, 128),
+                                              (2048, 4096, 4096, 128)])
+def test_w4a4_linear_asym_both_tile_heights(n, d_in, d_out, rows):
+    say(f"w4a4 asym tile rows {rows}: n={n} d_in={d_in} d_out={d_out}")
+    check_tile_rows(n, d_out, rows)
+    acc, y, acc_or, y_or = _asym_gemm(n, d_in, d_out, seed=n + d_in)
+    assert np.array_equal(acc, acc_or)
+    assert np.array_equal(y, y_or)
+    _, y2, _, _ = _asym_gemm(n, d_in, d_out, seed=n + d_in, with_acc=False)
     assert np.array_equal(y2, y_or)
 
 

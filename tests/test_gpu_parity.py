@@ -9,7 +9,7 @@ import workloads as wl
 from oracle import cat_oracle as o
 from paper_2603_04359_amd import binding as B
 
-from gpu_common import check_codes, dev, host, rel_fro, say, torch_mod
+from gpu_common import check_codes, check_tile_rows, dev, host, rel_fro, say, torch_mod
 
 pytestmark = pytest.mark.gpu
 
@@ -87,6 +87,29 @@ def test_w4a4_linear_without_acc_out_matches_oracle(n, d_in, d_out):
     _, y, _, y_or = _gemm_case(n, d_in, d_out, seed=3 * n + d_out, zero_rows=(0,), with_acc=False)
     assert np.array_equal(y, y_or)
     assert not y[0].any()
+
+
+# (n, d_in, d_out, acc_out, token rows per tile on a 256-CU device)
+TILE_HEIGHT_CASES = [
+    (4097, 160, 4100, True, 256),     # 289 tiles of 256 rows: ragged rows, outputs and K
+    (4352, 1056, 3840, False, 256),   # 255 tiles of 256 rows: one CU idle, stays at 256
+    (1900, 4160, 3000, True, 128),    # 96 tiles of 256 rows become 180 of 128, ragged
+    (2048, 4096, 4096, False, 128),   # the attention-projection shape, full tiles
+    (129, 96, 8000, False, 128),      # a last 128-row panel holding one row
+]
+
+
+@pytest.mark.parametrize("n,d_in,d_out,with_acc,rows", TILE_HEIGHT_CASES)
+def test_w4a4_linear_both_tile_heights(n, d_in, d_out, with_acc, rows):
+    # the launcher takes 128-row tiles when 256-row ones leave CUs idle
+    say(f"w4a4 tile rows {rows}: n={n} d_in={d_in} d_out={d_out} acc={with_acc}")
+    check_tile_rows(n, d_out, rows)
+    acc, y, acc_or, y_or = _gemm_case(n, d_in, d_out, seed=n + d_in + d_out, zero_rows=(0, n - 1),
+                                      with_acc=with_acc)
+    if with_acc:
+        assert np.array_equal(acc, acc_or)
+    assert np.array_equal(y, y_or)
+    assert not y[0].any() and not y[n - 1].any()
 
 
 @pytest.mark.parametrize("d_in", [96, 224])

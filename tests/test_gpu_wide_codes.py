@@ -10,7 +10,7 @@ import workloads as wl
 from oracle import cat_oracle as o
 from paper_2603_04359_amd import binding as B
 
-from gpu_common import check_codes, dev, host, rel_fro, say, torch_mod
+from gpu_common import check_codes, check_tile_rows, dev, host, rel_fro, say, torch_mod
 
 pytestmark = pytest.mark.gpu
 
@@ -96,6 +96,18 @@ def test_int8_linear_matches_oracle(n, d_in, d_out, qmax):
     assert not y[0].any()
     _, y2, _, _ = _int8_case(n, d_in, d_out, qmax, seed=n + d_in + qmax, with_acc=False)
     assert np.array_equal(y2, y_or)                    # full tiles' store path
+
+
+@pytest.mark.parametrize("n,d_in,d_out,rows", [(4097, 160, 4100, 256), (2048, 1088, 4096, 128),
+                                              (1900, 1056, 3000, 128)])
+def test_int8_linear_both_tile_heights(n, d_in, d_out, rows):
+    say(f"int8 linear tile rows {rows}: n={n} d_in={d_in} d_out={d_out}")
+    check_tile_rows(n, d_out, rows)
+    acc, y, acc_or, y_or = _int8_case(n, d_in, d_out, 127, seed=n + d_out)
+    assert np.array_equal(acc, acc_or)
+    assert np.array_equal(y, y_or)
+    _, y2, _, _ = _int8_case(n, d_in, d_out, 127, seed=n + d_out, with_acc=False)
+    assert np.array_equal(y2, y_or)
 
 
 def test_int8_linear_extreme_codes_at_max_d_in():

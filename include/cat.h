@@ -53,7 +53,8 @@ typedef enum {
     CAT_ERR_UNSUPPORTED = -2,   /* valid but not implemented (e.g. bits) */
     CAT_ERR_WORKSPACE = -3,     /* workspace missing or too small */
     CAT_ERR_HIP = -4,           /* HIP runtime / launch failure */
-    CAT_ERR_INTERNAL = -5       /* anything else (e.g. host allocation) */
+    CAT_ERR_INTERNAL = -5,      /* anything else (e.g. host allocation) */
+    CAT_ERR_TIMEOUT = -6        /* an exchange wait ran out (status queries) */
 } cat_status;
 
 typedef enum {
@@ -169,6 +170,19 @@ size_t cat_transform_quant_workspace_bytes(int64_t n, int64_t d, int64_t k);
  * (n, d, k) bytes, of the exchange timeout word described above (0 when the
  * arguments are invalid). */
 size_t cat_transform_quant_flag_offset(int64_t n, int64_t d, int64_t k);
+/* Status query for the exchange timeout word (no passage of the paper: a
+ * property of this library's single-pass exchange).  Waits for every call
+ * issued to `stream` so far, reads the word at
+ * cat_transform_quant_flag_offset(n, d, k) of `workspace` and clears it.
+ * Returns CAT_OK when it was zero and CAT_ERR_TIMEOUT when a wait of a call
+ * of that shape on this workspace ran out since the word was last cleared
+ * (those calls' results are invalid, as described above).  workspace
+ * device, at least cat_transform_quant_workspace_bytes(n, d, k) bytes (or
+ * the asymmetric size, whose word lies at the same offset).  It
+ * synchronises, so it must not be captured into a graph.  Errors:
+ * CAT_ERR_INVALID_ARG (NULL workspace, n or d < 1), CAT_ERR_HIP. */
+int cat_transform_quant_status(const void* workspace, int64_t n, int64_t d, int64_t k,
+                               void* stream);
 /* Testing hook (no passage of the paper): bounds the polls of every wait in
  * the single-pass exchange of later cat_transform_quant and
  * cat_transform_quant_asym calls, process-wide.  0 restores the default
@@ -194,13 +208,19 @@ int cat_transform_quant(const void* X, int x_dtype, int64_t n, int64_t d,
  * (8192 x 14336 and 16384 x 8192 bf16 inputs fit).  All calls on one GPU
  * share that GPU's array, which keeps the last call's contents; calls that
  * overlap on one GPU (other streams, other threads) race and must not be
- * issued.  The exchange timeout word lives in that array and is not
- * reported: a timed-out wait shows only in the results (zero code blocks,
- * NaN scales), never as a wrong scale. */
+ * issued.  The exchange timeout word lives in that array, at the offset
+ * a workspace of the call's shape would hold it; a timed-out wait never
+ * yields a wrong scale (zero code blocks, NaN scales), and
+ * cat_transform_quant_noalloc_status reports it. */
 size_t cat_transform_quant_noalloc_max_bytes(void);
 int cat_transform_quant_noalloc(const void* X, int x_dtype, int64_t n, int64_t d,
                                 const void* T, int t_dtype, int64_t k, int bits,
                                 uint8_t* codes, float* s_x, void* stream);
+/* cat_transform_quant_status for the current device's array of
+ * cat_transform_quant_noalloc: the timeout word of calls of shape (n, d, k)
+ * (each shape has its own word in the array; the array starts zeroed).
+ * Same returns; CAT_ERR_UNSUPPORTED for a shape the array cannot hold. */
+int cat_transform_quant_noalloc_status(int64_t n, int64_t d, int64_t k, void* stream);
 
 /* ------------------------------------------------------------------ (3)
  * W4A4 integer GEMM with dequantization (Sec. 3, eq. 5:

@@ -24,6 +24,7 @@ CAT_ERR_UNSUPPORTED = -2
 CAT_ERR_WORKSPACE = -3
 CAT_ERR_HIP = -4
 CAT_ERR_INTERNAL = -5
+CAT_ERR_TIMEOUT = -6
 
 CAT_F32 = 0
 CAT_BF16 = 1
@@ -42,7 +43,7 @@ CAT_MAX_BLOCK = 512
 EXPORTED = (
     "cat_cov_workspace_bytes", "cat_cov_accumulate", "cat_transform_quant_workspace_bytes",
     "cat_transform_quant_flag_offset", "cat_set_exchange_spin_limit", "cat_transform_quant", "cat_transform_quant_noalloc_max_bytes",
-    "cat_transform_quant_noalloc",
+    "cat_transform_quant_noalloc", "cat_transform_quant_status", "cat_transform_quant_noalloc_status",
     "cat_w4a4_linear", "cat_int8_linear", "cat_transform_quant_asym_workspace_bytes",
     "cat_transform_quant_asym", "cat_w4a4_linear_asym",
     "cat_weight_code_sums", "cat_sqnr_terms", "cat_transform_quant_full_workspace_bytes",
@@ -93,6 +94,10 @@ def lib() -> ctypes.CDLL:
     L.cat_transform_quant_noalloc.argtypes = [_vp, _int, _i64, _i64, _vp, _int, _i64, _int, _vp,
                                               _vp, _vp]
     L.cat_transform_quant_noalloc.restype = _int
+    L.cat_transform_quant_status.argtypes = [_vp, _i64, _i64, _i64, _vp]
+    L.cat_transform_quant_status.restype = _int
+    L.cat_transform_quant_noalloc_status.argtypes = [_i64, _i64, _i64, _vp]
+    L.cat_transform_quant_noalloc_status.restype = _int
     L.cat_w4a4_linear.argtypes = [_vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp]
     L.cat_w4a4_linear.restype = _int
     L.cat_int8_linear.argtypes = [_vp, _vp, _vp, _vp, _i64, _i64, _i64, _vp, _vp, _vp]
@@ -314,6 +319,25 @@ def cat_transform_quant_noalloc(X, T, k: int, codes, s_x, bits: int = 4, stream=
     _check("cat_transform_quant_noalloc",
            lib().cat_transform_quant_noalloc(px, _dtype_code(X), n, d, pt, _dtype_code(T), k, bits,
                                              pc, ps, _stream_ptr(stream)))
+
+
+def cat_transform_quant_status(workspace, n: int, d: int, k: int, stream=None):
+    """Waits for the stream, then reads and clears the exchange timeout word
+    of a workspace used by calls of shape (n, d, k); raises CatError
+    (code CAT_ERR_TIMEOUT) when a wait ran out."""
+    torch = _torch()
+    pw = _dev_ptr(workspace, "workspace", (torch.uint8,))
+    if workspace.numel() < cat_transform_quant_flag_offset(n, d, k) + 4:
+        raise ValueError("workspace is smaller than a workspace of this shape")
+    _check("cat_transform_quant_status",
+           lib().cat_transform_quant_status(pw, n, d, k, _stream_ptr(stream)))
+
+
+def cat_transform_quant_noalloc_status(n: int, d: int, k: int, stream=None):
+    """cat_transform_quant_status for the library's per-device scratch of
+    cat_transform_quant_noalloc."""
+    _check("cat_transform_quant_noalloc_status",
+           lib().cat_transform_quant_noalloc_status(n, d, k, _stream_ptr(stream)))
 
 
 def cat_w4a4_linear(codes_x, s_x, codes_w, s_w, y_tilde, acc_out=None, stream=None):

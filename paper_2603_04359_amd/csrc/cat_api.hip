@@ -100,6 +100,43 @@ extern "C" size_t cat_transform_quant_flag_offset(int64_t n, int64_t d, int64_t 
 
 extern "C" void cat_set_exchange_spin_limit(uint32_t polls) { catk::tq_set_spin_limit(polls); }
 
+// Reads and clears the 32-bit timeout word at ws + flag offset after the
+// stream's work so far (the copies are ordered on the stream itself).
+static int tq_read_clear_flag(const char* fn, const void* workspace, int64_t n, int64_t d,
+                              void* stream) {
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    uint32_t* word = reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(const_cast<void*>(workspace)) +
+                                                 catk::tq_flag_offset_bytes(n, d));
+    uint32_t v = 0;
+    hipError_t err = hipMemcpyAsync(&v, word, sizeof(v), hipMemcpyDeviceToHost, st);
+    if (err == hipSuccess) err = hipStreamSynchronize(st);
+    if (err != hipSuccess) return hip_fail(fn, err);
+    if (v == 0) return CAT_OK;
+    const uint32_t zero = 0;
+    err = hipMemcpyAsync(word, &zero, sizeof(zero), hipMemcpyHostToDevice, st);
+    if (err == hipSuccess) err = hipStreamSynchronize(st);
+    if (err != hipSuccess) return hip_fail(fn, err);
+    return fail(CAT_ERR_TIMEOUT, std::string(fn) +
+                                     ": an exchange wait ran out; the results of the calls "
+                                     "concerned are invalid");
+}
+
+extern "C" int cat_transform_quant_status(const void* workspace, int64_t n, int64_t d, int64_t k,
+                                          void* stream) {
+    const char* fn = "cat_transform_quant_status";
+    (void)k;
+    try {
+        if (!workspace) return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": NULL workspace");
+        if (n < 1 || d < 1) return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": n, d >= 1");
+        if (int rc = require_device(fn)) return rc;
+        return tq_read_clear_flag(fn, workspace, n, d, stream);
+    } catch (const std::exception& e) {
+        return fail(CAT_ERR_INTERNAL, std::string(fn) + ": " + e.what());
+    } catch (...) {
+        return fail(CAT_ERR_INTERNAL, std::string(fn) + ": unknown error");
+    }
+}
+
 extern "C" int cat_transform_quant(const void* X, int x_dtype, int64_t n, int64_t d, const void* T,
                                    int t_dtype, int64_t k, int bits, uint8_t* codes, float* s_x,
                                    void* workspace, size_t workspace_bytes, void* stream) {
@@ -190,6 +227,23 @@ extern "C" int cat_transform_quant_noalloc(const void* X, int x_dtype, int64_t n
         if (int rc = scratch_on_current_device(fn, &ws)) return rc;
         return cat_transform_quant(X, x_dtype, n, d, T, t_dtype, k, bits, codes, s_x, ws,
                                    kScratchBytes, stream);
+    } catch (const std::exception& e) {
+        return fail(CAT_ERR_INTERNAL, std::string(fn) + ": " + e.what());
+    } catch (...) {
+        return fail(CAT_ERR_INTERNAL, std::string(fn) + ": unknown error");
+    }
+}
+
+extern "C" int cat_transform_quant_noalloc_status(int64_t n, int64_t d, int64_t k, void* stream) {
+    const char* fn = "cat_transform_quant_noalloc_status";
+    try {
+        if (n < 1 || d < 1) return fail(CAT_ERR_INVALID_ARG, std::string(fn) + ": n, d >= 1");
+        if (cat_transform_quant_workspace_bytes(n, d, k) > kScratchBytes)
+            return fail(CAT_ERR_UNSUPPORTED, std::string(fn) + ": shape beyond the scratch array");
+        if (int rc = require_device(fn)) return rc;
+        void* ws = nullptr;
+        if (int rc = scratch_on_current_device(fn, &ws)) return rc;
+        return tq_read_clear_flag(fn, ws, n, d, stream);
     } catch (const std::exception& e) {
         return fail(CAT_ERR_INTERNAL, std::string(fn) + ": " + e.what());
     } catch (...) {

@@ -77,6 +77,19 @@ def test_transform_quant_invalid_args():
     assert call(codes=P + 8) == B.CAT_ERR_INVALID_ARG
 
 
+def test_transform_quant_status_invalid_args():
+    # argument errors come back before the device is touched
+    L = cat.lib()
+    assert L.cat_transform_quant_status(None, 8, 64, 16, None) == B.CAT_ERR_INVALID_ARG
+    assert L.cat_transform_quant_status(P, 0, 64, 16, None) == B.CAT_ERR_INVALID_ARG
+    assert L.cat_transform_quant_status(P, 8, 0, 16, None) == B.CAT_ERR_INVALID_ARG
+    assert L.cat_transform_quant_noalloc_status(0, 64, 16, None) == B.CAT_ERR_INVALID_ARG
+    big = 1 << 20   # 2^20 tokens x 4096 channels: far beyond the scratch array
+    assert L.cat_transform_quant_workspace_bytes(big, 4096, 128) > L.cat_transform_quant_noalloc_max_bytes()
+    assert L.cat_transform_quant_noalloc_status(big, 4096, 128, None) == B.CAT_ERR_UNSUPPORTED
+    assert "scratch" in cat.cat_last_error()
+
+
 @pytest.mark.parametrize("fn", ["cat_w4a4_linear", "cat_int8_linear"])
 def test_linear_invalid_args(fn):
     L = cat.lib()

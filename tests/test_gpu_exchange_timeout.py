@@ -84,3 +84,61 @@ def test_forced_exchange_timeouts_are_loud(d, mode):
     assert np.array_equal(c, ref_c) and np.array_equal(s, ref_s)
     if not timed_out:
         pytest.skip("no exchange read was early enough to time out at one poll")
+
+
+def test_status_query_reports_and_clears_a_forced_timeout():
+    # the status query returns CAT_ERR_TIMEOUT after a call whose waits ran
+    # out and clears the word; after calls with the default bound it is
+    # CAT_OK, on a caller workspace and on the allocation-free scratch
+    say("tq status query: workspace and allocation-free scratch")
+    torch = torch_mod()
+    n, d, k = 8192, 4096, 128
+    X = dev(_wide_X(n, d, seed=42), "bf16")
+    T = dev(_rand_T(d, k, seed=43), "bf16")
+    ws = torch.zeros(cat.cat_transform_quant_workspace_bytes(n, d, k), dtype=torch.uint8,
+                     device="cuda")
+    codes = torch.empty((n, d // 2), dtype=torch.uint8, device="cuda")
+    s_x = torch.empty(n, dtype=torch.float32, device="cuda")
+    fo = cat.cat_transform_quant_flag_offset(n, d, k)
+    for noalloc in (False, True):
+        def call():
+            if noalloc:
+                cat.cat_transform_quant_noalloc(X, T, k, codes, s_x)
+            else:
+                cat.cat_transform_quant(X, T, k, codes, s_x, ws)
+
+        def status():
+            if noalloc:
+                cat.cat_transform_quant_noalloc_status(n, d, k)
+            else:
+                cat.cat_transform_quant_status(ws, n, d, k)
+
+        status()                      # clears whatever earlier calls left
+        call()
+        status()                      # default bound: no timeout
+        ref_s = host(s_x).copy()
+        assert not np.isnan(ref_s).any()
+        seen = False
+        try:
+            cat.cat_set_exchange_spin_limit(1)
+            for _ in range(3):
+                call()
+                s = host(s_x)
+                changed = np.isnan(s).any() or not np.array_equal(s, ref_s)
+                try:
+                    status()
+                except cat.CatError as e:
+                    assert e.code == cat.CAT_ERR_TIMEOUT
+                    seen = True
+                else:
+                    assert not changed, "results changed but the status query saw no timeout"
+        finally:
+            cat.cat_set_exchange_spin_limit(0)
+        # cleared by the query that reported it; exact again at the default bound
+        if not noalloc:
+            assert int(host(ws[fo:fo + 4].view(torch.int32))[0]) == 0
+        call()
+        status()
+        assert np.array_equal(host(s_x), ref_s)
+        if not seen:
+            say(f"  noalloc={noalloc}: no read timed out at one poll")
